@@ -1,0 +1,383 @@
+// Grouped shared-KV decode attention (Sec. 4.1, Eqs. (9) and (12); Sec. 4.4
+// "Decode": both attentions read the same primary cache).
+//
+// A workgroup owns one (sequence, KV head, split of the cache).  Its query
+// rows are the G primary heads of that KV head followed by the G branch heads
+// (2G <= 16), so each K/V page is read once for both paths.  Scores and the
+// value sum run on MFMA (v_mfma_f32_16x16x32_bf16): scores S = K Q^T with the
+// 16 positions of a page as rows; the output is accumulated transposed,
+// O^T = V^T P^T, with V pages stored dim-major so the operand loads are
+// contiguous and the probabilities never leave the lane that computed them.
+// Softmax is online per split (base-2 exponent, running max and sum), the
+// four waves of a workgroup merge through LDS, and a combine kernel merges
+// the splits in split order.  The split size is fixed (pages_per_split), so
+// a row's result depends only on its own query and the cache.
+#include "common.h"
+#include "kernels.h"
+
+namespace dbt {
+
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+__device__ __forceinline__ uint32_t pack2(float lo, float hi) {
+  return (uint32_t)f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
+}
+
+// Zero the bf16 halves of v whose slot (4*gq + k, k = 0..3) is >= nvalid.
+__device__ __forceinline__ u32x2 mask_slots(u32x2 v, int first_slot, int nvalid) {
+  if (first_slot + 0 >= nvalid) v[0] &= 0xffff0000u;
+  if (first_slot + 1 >= nvalid) v[0] &= 0x0000ffffu;
+  if (first_slot + 2 >= nvalid) v[1] &= 0xffff0000u;
+  if (first_slot + 3 >= nvalid) v[1] &= 0x0000ffffu;
+  return v;
+}
+
+// Requires d_h == 128 and np*G <= 16.
+__global__ __launch_bounds__(256) void k_attn_decode_bf16(AttnArgs a) {
+  constexpr int DH = 128;
+  const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  const int len = a.pos_arr[b] + 1;
+  const int npages = (len + 15) >> 4;
+  const int pb = split * a.pages_per_split;
+  if (pb >= npages) return;
+  const int pe = min(npages, pb + a.pages_per_split);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r = lane & 15, gq = lane >> 4;
+  const int n_kv = a.kv.n_kv;
+  const int G = a.n_q / n_kv;
+  const int nrows = a.rows.np * G;
+  const int dq = a.n_q * DH;
+  const float scale = kLog2e / sqrtf((float)DH);
+
+  // Query operand: lane (query r, group gq) holds Q[r][s*32 + gq*8 .. +8].
+  u32x4 qf[4];
+  {
+    const bool valid = r < nrows;
+    const int path = a.rows.p0 + (valid ? r / G : 0);
+    const int head = g * G + (valid ? r % G : 0);
+    const float *qp = a.Q + (size_t)(path * a.rows.Bp + b) * dq + head * DH + gq * 8;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      float x[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] = valid ? qp[s * 32 + e] : 0.f;
+      qf[s] = u32x4{pack2(x[0], x[1]), pack2(x[2], x[3]), pack2(x[4], x[5]), pack2(x[6], x[7])};
+    }
+  }
+
+  const uint16_t *kbase = (const uint16_t *)a.kv.k;
+  const uint16_t *vbase = (const uint16_t *)a.kv.v;
+  const int *ptab = a.kv.page_table + (size_t)b * a.kv.mpps;
+
+  float m_run = -INFINITY, l_run = 0.f;
+  floatx4 acc[8];
+#pragma unroll
+  for (int c = 0; c < 8; ++c) acc[c] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  const int npairs = (pe - pb + 1) >> 1;
+  for (int q = wave; q < npairs; q += 4) {
+    const int pg0 = pb + 2 * q;
+    const bool has1 = pg0 + 1 < pe;
+    const int phys0 = ptab[pg0];
+    const int phys1 = has1 ? ptab[pg0 + 1] : phys0;
+    const uint16_t *k0 = kbase + ((size_t)phys0 * n_kv + g) * 16 * DH;
+    const uint16_t *k1 = kbase + ((size_t)phys1 * n_kv + g) * 16 * DH;
+    const uint16_t *v0 = vbase + ((size_t)phys0 * n_kv + g) * DH * 16;
+    const uint16_t *v1 = vbase + ((size_t)phys1 * n_kv + g) * DH * 16;
+
+    u32x4 kf0[4], kf1[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      kf0[s] = *(const u32x4 *)(k0 + r * DH + s * 32 + gq * 8);
+      kf1[s] = has1 ? *(const u32x4 *)(k1 + r * DH + s * 32 + gq * 8) : u32x4{0u, 0u, 0u, 0u};
+    }
+    u32x2 vf0[8], vf1[8];
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      vf0[c] = *(const u32x2 *)(v0 + (c * 16 + r) * 16 + gq * 4);
+      vf1[c] = has1 ? *(const u32x2 *)(v1 + (c * 16 + r) * 16 + gq * 4) : u32x2{0u, 0u};
+    }
+
+    floatx4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kf0[s]),
+                                                   __builtin_bit_cast(bf16x8, qf[s]), s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kf1[s]),
+                                                   __builtin_bit_cast(bf16x8, qf[s]), s1, 0, 0, 0);
+    }
+    // lane holds scores of slots 4*gq+i (i = 0..3) of both pages for query r
+    const int nv0 = min(16, len - pg0 * 16);
+    const int nv1 = has1 ? min(16, len - (pg0 + 1) * 16) : 0;
+    float sc[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      sc[i] = (4 * gq + i < nv0) ? s0[i] * scale : -INFINITY;
+      sc[4 + i] = (4 * gq + i < nv1) ? s1[i] * scale : -INFINITY;
+    }
+    float mt = sc[0];
+#pragma unroll
+    for (int i = 1; i < 8; ++i) mt = fmaxf(mt, sc[i]);
+    mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
+    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+    const float m_new = fmaxf(m_run, mt);
+    const float corr = exp2f(m_run - m_new);
+    float p[8];
+    float ps = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      p[i] = exp2f(sc[i] - m_new);
+      ps += p[i];
+    }
+    l_run = l_run * corr + ps;
+    m_run = m_new;
+    const u32x4 pf = u32x4{pack2(p[0], p[1]), pack2(p[2], p[3]), pack2(p[4], p[5]), pack2(p[6], p[7])};
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      const u32x2 lo = mask_slots(vf0[c], 4 * gq, nv0);
+      const u32x2 hi = mask_slots(vf1[c], 4 * gq, nv1);
+      const u32x4 vv = u32x4{lo[0], lo[1], hi[0], hi[1]};
+      acc[c] = acc[c] * corr;
+      acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vv),
+                                                       __builtin_bit_cast(bf16x8, pf), acc[c], 0, 0, 0);
+    }
+  }
+  l_run += __shfl_xor(l_run, 16, 64);
+  l_run += __shfl_xor(l_run, 32, 64);
+
+  // merge the four waves: acc holds O^T[dh = 16c + 4gq + i][query r]
+  __shared__ float so[4][DH][17];
+  __shared__ float sm[4][16], sl[4][16];
+#pragma unroll
+  for (int c = 0; c < 8; ++c)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) so[wave][c * 16 + gq * 4 + i][r] = acc[c][i];
+  if (gq == 0) {
+    sm[wave][r] = m_run;
+    sl[wave][r] = l_run;
+  }
+  __syncthreads();
+  const size_t obase = (((size_t)b * n_kv + g) * a.max_splits + split) * 16;
+  for (int e = threadIdx.x; e < nrows * DH; e += 256) {
+    const int qr = e / DH, dh = e % DH;
+    float mx = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) mx = fmaxf(mx, sm[w][qr]);
+    float o = 0.f, l = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      if (sm[w][qr] != -INFINITY) {
+        const float f = exp2f(sm[w][qr] - mx);
+        o += so[w][dh][qr] * f;
+        l += sl[w][qr] * f;
+      }
+    }
+    a.opart[(obase + qr) * DH + dh] = o;
+    if (dh == 0) {
+      a.ostat[(obase + qr) * 2 + 0] = mx;
+      a.ostat[(obase + qr) * 2 + 1] = l;
+    }
+  }
+}
+
+// fp32 cache: scores in LDS, exact two-pass softmax over the split.
+__global__ __launch_bounds__(256) void k_attn_decode_f32(AttnArgs a) {
+  constexpr int MAXP = 512;  // positions per split (pages_per_split * 16)
+  __shared__ float qs[16][128];
+  __shared__ float sc[16][MAXP];
+  __shared__ float red[16];
+  const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  const int len = a.pos_arr[b] + 1;
+  const int npages = (len + 15) >> 4;
+  const int pb = split * a.pages_per_split;
+  if (pb >= npages) return;
+  const int p_lo = pb * 16, p_hi = min(len, (pb + a.pages_per_split) * 16);
+  const int np = p_hi - p_lo;
+  const int n_kv = a.kv.n_kv, DH = a.kv.d_h;
+  const int G = a.n_q / n_kv;
+  const int nrows = a.rows.np * G;
+  const int dq = a.n_q * DH;
+  const float scale = kLog2e / sqrtf((float)DH);
+  const float *kb = (const float *)a.kv.k;
+  const float *vb = (const float *)a.kv.v;
+  const int *ptab = a.kv.page_table + (size_t)b * a.kv.mpps;
+  for (int e = threadIdx.x; e < nrows * DH; e += blockDim.x) {
+    const int qr = e / DH, dh = e % DH;
+    const int path = a.rows.p0 + qr / G, head = g * G + qr % G;
+    qs[qr][dh] = a.Q[(size_t)(path * a.rows.Bp + b) * dq + head * DH + dh];
+  }
+  __syncthreads();
+  for (int t = threadIdx.x; t < np; t += blockDim.x) {
+    const int pos = p_lo + t;
+    const float *kr = kb + (((size_t)ptab[pos >> 4] * n_kv + g) * 16 + (pos & 15)) * DH;
+    for (int qr = 0; qr < nrows; ++qr) {
+      float s = 0.f;
+      for (int dh = 0; dh < DH; ++dh) s = fmaf(kr[dh], qs[qr][dh], s);
+      sc[qr][t] = s * scale;
+    }
+  }
+  __syncthreads();
+  const size_t obase = (((size_t)b * n_kv + g) * a.max_splits + split) * 16;
+  for (int qr = 0; qr < nrows; ++qr) {
+    float mx = -INFINITY;
+    for (int t = threadIdx.x; t < np; t += blockDim.x) mx = fmaxf(mx, sc[qr][t]);
+    mx = block_max(mx, red);
+    float l = 0.f;
+    for (int t = threadIdx.x; t < np; t += blockDim.x) {
+      const float pv = exp2f(sc[qr][t] - mx);
+      sc[qr][t] = pv;
+      l += pv;
+    }
+    l = block_sum(l, red);
+    if (threadIdx.x == 0) {
+      a.ostat[(obase + qr) * 2 + 0] = mx;
+      a.ostat[(obase + qr) * 2 + 1] = l;
+    }
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < nrows * DH; e += blockDim.x) {
+    const int qr = e / DH, dh = e % DH;
+    float o = 0.f;
+    for (int t = 0; t < np; ++t) {
+      const int pos = p_lo + t;
+      o = fmaf(sc[qr][t], vb[(((size_t)ptab[pos >> 4] * n_kv + g) * DH + dh) * 16 + (pos & 15)], o);
+    }
+    a.opart[(obase + qr) * DH + dh] = o;
+  }
+}
+
+// Merge the splits of one (sequence, KV head) in split order and write the
+// normalised head outputs to O (row path*Bp + b, column head*d_h + dh).
+template <typename T>
+__global__ void k_attn_combine(AttnArgs a, T *O, int ldo) {
+  const int g = blockIdx.x, b = blockIdx.y;
+  const int len = a.pos_arr[b] + 1;
+  const int npages = (len + 15) >> 4;
+  const int nsplit = (npages + a.pages_per_split - 1) / a.pages_per_split;
+  const int n_kv = a.kv.n_kv, DH = a.kv.d_h;
+  const int G = a.n_q / n_kv;
+  const int nrows = a.rows.np * G;
+  const size_t base = ((size_t)b * n_kv + g) * a.max_splits;
+  for (int e = threadIdx.x; e < nrows * DH; e += blockDim.x) {
+    const int qr = e / DH, dh = e % DH;
+    float mx = -INFINITY;
+    for (int s = 0; s < nsplit; ++s) mx = fmaxf(mx, a.ostat[((base + s) * 16 + qr) * 2]);
+    float o = 0.f, l = 0.f;
+    for (int s = 0; s < nsplit; ++s) {
+      const size_t ix = (base + s) * 16 + qr;
+      const float f = exp2f(a.ostat[ix * 2] - mx);
+      o += a.opart[ix * DH + dh] * f;
+      l += a.ostat[ix * 2 + 1] * f;
+    }
+    const int path = a.rows.p0 + qr / G, head = g * G + qr % G;
+    st<T>(O, (size_t)(path * a.rows.Bp + b) * ldo + head * DH + dh, o / l);
+  }
+}
+
+// Causal attention over the prompt of one sequence: workgroup per
+// (position t, KV head), keys 0..t in chunks of 256 with an online softmax.
+template <typename T>
+__global__ __launch_bounds__(256) void k_attn_prefill(const float *Q, int ldq, KVRef kv, int seq, int n_q,
+                                                      T *O, int ldo) {
+  constexpr int CH = 256;
+  __shared__ float qs[16][128];
+  __shared__ float sc[16][CH];
+  __shared__ float red[16];
+  const int t = blockIdx.x, g = blockIdx.y;
+  const int n_kv = kv.n_kv, DH = kv.d_h;
+  const int G = n_q / n_kv;
+  const float scale = kLog2e / sqrtf((float)DH);
+  const T *kb = (const T *)kv.k;
+  const T *vb = (const T *)kv.v;
+  const int *ptab = kv.page_table + (size_t)seq * kv.mpps;
+  for (int e = threadIdx.x; e < G * DH; e += blockDim.x)
+    qs[e / DH][e % DH] = Q[(size_t)t * ldq + (g * G + e / DH) * DH + e % DH];
+  float acc[8], mrun[16], lrun[16];
+  for (int k = 0; k < 8; ++k) acc[k] = 0.f;
+  for (int j = 0; j < 16; ++j) { mrun[j] = -INFINITY; lrun[j] = 0.f; }
+  const int nel = G * DH;  // <= 2048: thread owns elements threadIdx.x + 256k
+  for (int c0 = 0; c0 <= t; c0 += CH) {
+    const int nk = min(CH, t + 1 - c0);
+    __syncthreads();
+    if ((int)threadIdx.x < nk) {
+      const int pos = c0 + threadIdx.x;
+      const T *kr = kb + (((size_t)ptab[pos >> 4] * n_kv + g) * 16 + (pos & 15)) * DH;
+      for (int j = 0; j < G; ++j) {
+        float s = 0.f;
+        for (int dh = 0; dh < DH; ++dh) s = fmaf(ld<T>(kr, dh), qs[j][dh], s);
+        sc[j][threadIdx.x] = s * scale;
+      }
+    }
+    __syncthreads();
+    float corr[16];
+    for (int j = 0; j < G; ++j) {
+      float mx = -INFINITY;
+      for (int k = threadIdx.x; k < nk; k += blockDim.x) mx = fmaxf(mx, sc[j][k]);
+      mx = block_max(mx, red);
+      const float mn = fmaxf(mrun[j], mx);
+      corr[j] = exp2f(mrun[j] - mn);
+      float l = 0.f;
+      __syncthreads();
+      for (int k = threadIdx.x; k < nk; k += blockDim.x) {
+        const float pv = exp2f(sc[j][k] - mn);
+        sc[j][k] = pv;
+        l += pv;
+      }
+      l = block_sum(l, red);
+      lrun[j] = lrun[j] * corr[j] + l;
+      mrun[j] = mn;
+    }
+    __syncthreads();
+    for (int k = 0; k < 8; ++k) {
+      const int e = threadIdx.x + 256 * k;
+      if (e >= nel) break;
+      const int j = e / DH, dh = e % DH;
+      float o = acc[k] * corr[j];
+      for (int kk = 0; kk < nk; ++kk) {
+        const int pos = c0 + kk;
+        o = fmaf(sc[j][kk], ld<T>(vb, (((size_t)ptab[pos >> 4] * n_kv + g) * DH + dh) * 16 + (pos & 15)), o);
+      }
+      acc[k] = o;
+    }
+  }
+  for (int k = 0; k < 8; ++k) {
+    const int e = threadIdx.x + 256 * k;
+    if (e >= nel) break;
+    const int j = e / DH, dh = e % DH;
+    st<T>(O, (size_t)t * ldo + (g * G + j) * DH + dh, acc[k] / lrun[j]);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_attn_decode(const AttnArgs &a, hipStream_t st) {
+  dim3 grid(a.max_splits, a.kv.n_kv, a.rows.B);
+  if (a.dtype == 1)
+    hipLaunchKernelGGL(k_attn_decode_bf16, grid, dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL(k_attn_decode_f32, grid, dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_combine(const AttnArgs &a, void *O, int ldo, hipStream_t st) {
+  dim3 grid(a.kv.n_kv, a.rows.B);
+  if (a.dtype == 1)
+    hipLaunchKernelGGL(k_attn_combine<uint16_t>, grid, dim3(256), 0, st, a, (uint16_t *)O, ldo);
+  else
+    hipLaunchKernelGGL(k_attn_combine<float>, grid, dim3(256), 0, st, a, (float *)O, ldo);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_prefill(const float *Q, int ldq, int T, KVRef kv, int seq, int n_q, int dtype, void *O,
+                               int ldo, hipStream_t st) {
+  dim3 grid(T, kv.n_kv);
+  if (dtype == 1)
+    hipLaunchKernelGGL(k_attn_prefill<uint16_t>, grid, dim3(256), 0, st, Q, ldq, kv, seq, n_q, (uint16_t *)O, ldo);
+  else
+    hipLaunchKernelGGL(k_attn_prefill<float>, grid, dim3(256), 0, st, Q, ldq, kv, seq, n_q, (float *)O, ldo);
+  return hipGetLastError();
+}
+
+}  // namespace dbt

@@ -1,0 +1,770 @@
+// Host side of the decode library: argument checking, workspace layout, the
+// page allocator of the single primary KV cache, and the order in which the
+// kernels of prefill, boundary and continuation steps are enqueued
+// (Sec. 4.4 of the Decode-Branch Transformer paper).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <functional>
+#include <new>
+#include <queue>
+#include <string>
+#include <vector>
+
+#include "../../include/dbt.h"
+#include "kernels.h"
+
+using namespace dbt;
+
+namespace {
+
+thread_local std::string g_err;
+
+dbt_status fail(dbt_status s, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+#define HIPCHK(expr)                                                                         \
+  do {                                                                                       \
+    hipError_t e_ = (expr);                                                                  \
+    if (e_ != hipSuccess) return fail(DBT_ERR_HIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr int kPage = 16;
+constexpr int kPagesPerSplit = 32;  // attention split: 512 positions
+constexpr int kMixChunk = 4096;
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+int round16(int x) { return (x + 15) / 16 * 16; }
+
+// Offsets (bytes) of every workspace buffer.
+struct Layout {
+  int Bp_max = 0, R_max = 0, rows_max = 0, max_in = 0, nqkv = 0, f = 0;
+  int S_qkv = 1, S_o = 1, S_gu = 1, S_d = 1;
+  int max_splits = 0, nch = 0;
+  size_t rope = 0, pos = 0, S = 0, Xn = 0, Xh = 0, Q = 0, O = 0, P = 0, apart = 0, astat = 0,
+         logits = 0, mstats = 0, mcand = 0, ret_q = 0, ret_h = 0, ret_m = 0, btok = 0, slast = 0,
+         total = 0;
+};
+
+dbt_status check_config(const dbt_config *c) {
+  if (!c) return fail(DBT_ERR_ARG, "config is NULL");
+  if (c->n_layers <= 0 || c->d_model <= 0 || c->n_q_heads <= 0 || c->n_kv_heads <= 0 ||
+      c->head_dim <= 0 || c->vocab < 0 || c->max_batch <= 0 || c->max_pos <= 0 || c->max_prompt < 0)
+    return fail(DBT_ERR_ARG, "sizes must be positive");
+  if (c->dtype != DBT_F32 && c->dtype != DBT_BF16) return fail(DBT_ERR_ARG, "dtype must be DBT_F32 or DBT_BF16");
+  if (c->n_q_heads % c->n_kv_heads) return fail(DBT_ERR_SHAPE, "n_q_heads %% n_kv_heads != 0");
+  if (c->head_dim % 2) return fail(DBT_ERR_SHAPE, "head_dim must be even");
+  if (c->max_prompt > c->max_pos) return fail(DBT_ERR_SHAPE, "max_prompt > max_pos");
+  if (c->n_experts > 0) return fail(DBT_ERR_UNSUPPORTED, "MoE layers are not built in this library version");
+  if (c->d_ff <= 0) return fail(DBT_ERR_ARG, "d_ff must be positive");
+  if (c->has_embeddings && c->vocab <= 0) return fail(DBT_ERR_SHAPE, "token inputs need a vocabulary");
+  if (c->max_prompt > 0 && !c->has_embeddings) return fail(DBT_ERR_SHAPE, "prefill needs token inputs");
+  if (!(c->rms_eps >= 0.f) || !(c->rope_theta > 0.f)) return fail(DBT_ERR_ARG, "bad rms_eps/rope_theta");
+  const int G = c->n_q_heads / c->n_kv_heads;
+  if (2 * G > 16) return fail(DBT_ERR_UNSUPPORTED, "more than 8 query heads per KV head");
+  if (c->head_dim > 128) return fail(DBT_ERR_UNSUPPORTED, "head_dim > 128");
+  if (c->dtype == DBT_BF16) {
+    const int dq = c->n_q_heads * c->head_dim, dkv = c->n_kv_heads * c->head_dim;
+    if (c->head_dim != 128) return fail(DBT_ERR_UNSUPPORTED, "bf16 attention needs head_dim 128");
+    if (c->d_model % 128 || dq % 128 || c->d_ff % 128)
+      return fail(DBT_ERR_UNSUPPORTED, "bf16 projections need d_model, n_q*d_h, d_ff multiples of 128");
+    if (dkv % 64 || c->vocab % 64) return fail(DBT_ERR_UNSUPPORTED, "bf16 projections need n_kv*d_h, vocab multiples of 64");
+  }
+  return DBT_OK;
+}
+
+Layout make_layout(const dbt_config *c) {
+  Layout L;
+  const int d = c->d_model, dq = c->n_q_heads * c->head_dim, dkv = c->n_kv_heads * c->head_dim;
+  L.f = c->d_ff;
+  L.Bp_max = round16(c->max_batch);
+  L.R_max = 2 * L.Bp_max;
+  L.rows_max = std::max(L.R_max, c->max_prompt);
+  L.max_in = std::max(std::max(d, dq), L.f);
+  L.nqkv = dq + 2 * dkv;
+  L.S_qkv = gemm_splits(L.nqkv, d, c->dtype);
+  L.S_o = gemm_splits(d, dq, c->dtype);
+  L.S_gu = gemm_splits(2 * L.f, d, c->dtype);
+  L.S_d = gemm_splits(d, L.f, c->dtype);
+  const int maxpages = (c->max_pos + kPage - 1) / kPage;
+  L.max_splits = (maxpages + kPagesPerSplit - 1) / kPagesPerSplit;
+  L.nch = c->vocab > 0 ? (c->vocab + kMixChunk - 1) / kMixChunk : 0;
+  size_t part = std::max({(size_t)L.S_qkv * L.R_max * L.nqkv, (size_t)L.S_o * L.R_max * d,
+                          (size_t)L.S_gu * L.R_max * 2 * L.f, (size_t)L.S_d * L.R_max * d});
+  part = std::max(part, (size_t)c->max_prompt * std::max({L.nqkv, d, 2 * L.f}));
+  size_t o = 0;
+  auto take = [&](size_t bytes) { size_t at = o; o += align256(bytes); return at; };
+  L.rope = take((size_t)c->max_pos * (c->head_dim / 2) * 2 * sizeof(float));
+  L.pos = take((size_t)c->max_batch * sizeof(int));
+  L.S = take((size_t)L.rows_max * d * 4);
+  L.Xn = take((size_t)L.rows_max * L.max_in * 4);
+  L.Xh = take((size_t)L.rows_max * L.f * 4);
+  L.Q = take((size_t)L.rows_max * dq * 4);
+  L.O = take((size_t)L.rows_max * dq * 4);
+  L.P = take(part * 4);
+  L.apart = take((size_t)c->max_batch * c->n_kv_heads * L.max_splits * 16 * c->head_dim * 4);
+  L.astat = take((size_t)c->max_batch * c->n_kv_heads * L.max_splits * 16 * 2 * 4);
+  L.logits = take((size_t)L.R_max * std::max(c->vocab, 1) * 4);
+  L.mstats = take((size_t)L.R_max * std::max(L.nch, 1) * 3 * 4);
+  L.mcand = take((size_t)c->max_batch * std::max(L.nch, 1) * 2 * 4);
+  L.ret_q = take((size_t)c->n_layers * L.Bp_max * dq * 4);
+  L.ret_h = take((size_t)c->n_layers * L.Bp_max * L.f * 4);
+  L.ret_m = take((size_t)c->n_layers * L.Bp_max * d * 4);
+  L.btok = take((size_t)c->max_batch * 4);
+  L.slast = take((size_t)L.Bp_max * d * 4);
+  L.total = o;
+  return L;
+}
+
+}  // namespace
+
+struct dbt_model {
+  dbt_config cfg;
+  dbt_weights w;
+  std::vector<dbt_layer_weights> layers;
+  char *ws = nullptr;
+  Layout L;
+  std::vector<float> rope_host;
+  bool dev_ready = false;
+  // boundary state: set by dbt_prefill(run_boundary = 0)
+  const dbt_kv *bnd_kv = nullptr;
+  int bnd_batch = 0;
+  template <typename T> T *at(size_t off) const { return (T *)(ws + off); }
+};
+
+struct dbt_kv {
+  dbt_model *m;
+  char *k, *v;
+  int num_pages;
+  int *page_table;
+  int mpps;
+  std::priority_queue<int, std::vector<int>, std::greater<int>> free_pages;
+  std::vector<std::vector<int>> table;
+  std::vector<int> len;
+  struct Upd { int b, slot, page; };
+  std::vector<Upd> pending;
+
+  int take_page() {
+    const int p = free_pages.top();
+    free_pages.pop();
+    return p;
+  }
+};
+
+namespace {
+
+size_t esize(const dbt_config &c) { return c.dtype == DBT_BF16 ? 2 : 4; }
+
+// K/V pages of one layer.
+KVRef kv_layer(const dbt_kv *kv, int l) {
+  const dbt_config &c = kv->m->cfg;
+  KVRef r;
+  const size_t per_layer = (size_t)kv->num_pages * c.n_kv_heads * kPage * c.head_dim * esize(c);
+  r.k = kv->k + per_layer * l;
+  r.v = kv->v + per_layer * l;
+  r.page_table = kv->page_table;
+  r.mpps = kv->mpps;
+  r.n_kv = c.n_kv_heads;
+  r.d_h = c.head_dim;
+  return r;
+}
+
+dbt_status ensure_device(dbt_model *m, hipStream_t st) {
+  if (m->dev_ready) return DBT_OK;
+  HIPCHK(hipMemsetAsync(m->ws, 0, m->L.total, st));
+  HIPCHK(hipMemcpyAsync(m->ws + m->L.rope, m->rope_host.data(), m->rope_host.size() * sizeof(float),
+                        hipMemcpyHostToDevice, st));
+  m->dev_ready = true;
+  return DBT_OK;
+}
+
+// Enqueue pending page-table entries and (optionally) per-sequence positions.
+dbt_status flush(dbt_kv *kv, const int *h_pos, int npos, hipStream_t st) {
+  dbt_model *m = kv->m;
+  size_t ip = 0;
+  int ipos = 0;
+  while (ip < kv->pending.size() || ipos < npos) {
+    StepBegin sb;
+    std::memset(&sb, 0, sizeof sb);
+    sb.b0 = ipos;
+    sb.n_pos = std::min(64, npos - ipos);
+    for (int i = 0; i < sb.n_pos; ++i) sb.pos[i] = h_pos[ipos + i];
+    ipos += sb.n_pos;
+    sb.n_pt = (int)std::min<size_t>(64, kv->pending.size() - ip);
+    for (int i = 0; i < sb.n_pt; ++i) {
+      sb.pt_b[i] = kv->pending[ip + i].b;
+      sb.pt_slot[i] = kv->pending[ip + i].slot;
+      sb.pt_page[i] = kv->pending[ip + i].page;
+    }
+    ip += sb.n_pt;
+    HIPCHK(launch_step_begin(sb, m->at<int>(m->L.pos), kv->page_table, kv->mpps, st));
+  }
+  kv->pending.clear();
+  return DBT_OK;
+}
+
+// One layer for the active rows.  rows_layout: rows of the partial slabs.
+struct LayerCall {
+  Rows rows;
+  int mode;
+  bool retain;
+  int ret_src, ret_dst;
+  bool prefill;
+  int seq;           // prefill: the sequence
+  int rows_layout;   // prefill: T; decode: 2*Bp
+  bool last_norm;    // apply the next norm after the layer
+};
+
+dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStream_t st) {
+  const dbt_config &cf = m->cfg;
+  const Layout &L = m->L;
+  const dbt_layer_weights &W = m->layers[l];
+  const int d = cf.d_model, dq = cf.n_q_heads * cf.head_dim, dkv = cf.n_kv_heads * cf.head_dim, f = L.f;
+  const size_t es = esize(cf);
+  const int xrow0 = c.rows.p0 * c.rows.Bp;
+  const int M = c.rows.np * c.rows.Bp;
+  char *Xn = m->ws + L.Xn, *Xh = m->ws + L.Xh, *O = m->ws + L.O;
+  float *P = m->at<float>(L.P), *S = m->at<float>(L.S), *Q = m->at<float>(L.Q);
+  const int S_qkv = c.prefill ? 1 : L.S_qkv, S_o = c.prefill ? 1 : L.S_o, S_gu = c.prefill ? 1 : L.S_gu,
+            S_d = c.prefill ? 1 : L.S_d;
+  KVRef kvl = kv_layer(kv, l);
+  const size_t rq = (size_t)l * L.Bp_max;
+  float *ret_q = m->at<float>(L.ret_q) + rq * dq;
+  float *ret_h = m->at<float>(L.ret_h) + rq * f;
+  float *ret_m = m->at<float>(L.ret_m) + rq * d;
+
+  // 1. stacked QKV projection (branch rows need only W_Q)
+  WSegs qkv{};
+  int nq;
+  if (c.mode == MODE_BRANCH) {
+    qkv = WSegs{{W.wq, nullptr, nullptr}, {dq, 0, 0}};
+    nq = dq;
+  } else {
+    qkv = WSegs{{W.wq, W.wk, W.wv}, {dq, dkv, dkv}};
+    nq = L.nqkv;
+  }
+  long long stride = (long long)c.rows_layout * nq;
+  HIPCHK(launch_gemm(qkv, nq, d, cf.dtype, Xn + (size_t)xrow0 * d * es, d, M, P + (size_t)xrow0 * nq, nq,
+                     stride, S_qkv, st));
+  QKVFinish qf{};
+  qf.part = P;
+  qf.split_stride = stride;
+  qf.S = S_qkv;
+  qf.ldp = nq;
+  qf.n_q = cf.n_q_heads;
+  qf.n_kv = cf.n_kv_heads;
+  qf.d_h = cf.head_dim;
+  qf.rows = c.rows;
+  qf.mode = c.mode;
+  qf.rope = m->at<float2>(L.rope);
+  qf.pos_arr = c.prefill ? nullptr : m->at<int>(L.pos);
+  qf.seq_fixed = c.seq;
+  qf.a = W.a;
+  qf.Q = Q;
+  qf.Q1_in = ret_q;
+  qf.ret = Retain{c.retain ? ret_q : nullptr, c.ret_src, c.ret_dst};
+  qf.kv = kvl;
+  qf.dtype = cf.dtype;
+  HIPCHK(launch_qkv_finish(qf, st));
+
+  // 2. attention over the primary cache
+  if (c.prefill) {
+    HIPCHK(launch_attn_prefill(Q, dq, c.rows.B, kvl, c.seq, cf.n_q_heads, cf.dtype, O, dq, st));
+  } else {
+    AttnArgs aa{};
+    aa.Q = Q;
+    aa.kv = kvl;
+    aa.pos_arr = m->at<int>(L.pos);
+    aa.rows = c.rows;
+    aa.n_q = cf.n_q_heads;
+    aa.pages_per_split = kPagesPerSplit;
+    aa.max_splits = L.max_splits;
+    aa.opart = m->at<float>(L.apart);
+    aa.ostat = m->at<float>(L.astat);
+    aa.dtype = cf.dtype;
+    HIPCHK(launch_attn_decode(aa, st));
+    HIPCHK(launch_attn_combine(aa, O, dq, st));
+  }
+
+  // 3. output projection + residual + MLP norm
+  WSegs wo{{W.wo, nullptr, nullptr}, {d, 0, 0}};
+  stride = (long long)c.rows_layout * d;
+  HIPCHK(launch_gemm(wo, d, dq, cf.dtype, O + (size_t)xrow0 * dq * es, dq, M, P + (size_t)xrow0 * d, d,
+                     stride, S_o, st));
+  HIPCHK(launch_resid_norm(P, stride, S_o, d, S, W.mlp_norm, cf.rms_eps, d, cf.dtype, c.rows, Xn, d, st));
+
+  // 4. gate/up + SwiGLU + b coupling
+  WSegs gu{{W.w_gate, W.w_up, nullptr}, {f, f, 0}};
+  stride = (long long)c.rows_layout * 2 * f;
+  HIPCHK(launch_gemm(gu, 2 * f, d, cf.dtype, Xn + (size_t)xrow0 * d * es, d, M, P + (size_t)xrow0 * 2 * f,
+                     2 * f, stride, S_gu, st));
+  HIPCHK(launch_swiglu_finish(P, stride, S_gu, 2 * f, f, c.mode, c.rows, W.b, ret_h,
+                              Retain{c.retain ? ret_h : nullptr, c.ret_src, c.ret_dst}, cf.dtype, Xh, f, st));
+
+  // 5. down projection + c coupling + residual + next norm
+  WSegs wd{{W.w_down, nullptr, nullptr}, {d, 0, 0}};
+  stride = (long long)c.rows_layout * d;
+  HIPCHK(launch_gemm(wd, d, f, cf.dtype, Xh + (size_t)xrow0 * f * es, f, M, P + (size_t)xrow0 * d, d, stride,
+                     S_d, st));
+  const float *g_next = nullptr;
+  if (l + 1 < cf.n_layers) g_next = m->layers[l + 1].attn_norm;
+  else if (cf.vocab > 0 && c.last_norm) g_next = m->w.final_norm;
+  HIPCHK(launch_down_finish(P, stride, S_d, d, d, c.mode, c.rows, W.c, ret_m,
+                            Retain{c.retain ? ret_m : nullptr, c.ret_src, c.ret_dst}, S, g_next, cf.rms_eps,
+                            cf.dtype, Xn, d, st));
+  return DBT_OK;
+}
+
+// Step inputs for the active rows: embeddings (Eq. (7)) or given residuals,
+// then the first layer's attention norm.
+dbt_status load_inputs(dbt_model *m, const dbt_step_in *in, const int *tokens, Rows rows, hipStream_t st) {
+  const dbt_config &cf = m->cfg;
+  const Layout &L = m->L;
+  const float *g0 = m->layers[0].attn_norm;
+  if (cf.has_embeddings) {
+    HIPCHK(launch_embed(tokens, cf.vocab, m->w.emb1, m->w.emb2, m->w.emb_norm, g0, cf.rms_eps, cf.d_model, cf.dtype, rows,
+                        m->at<float>(L.S), m->ws + L.Xn, cf.d_model, st));
+  } else {
+    HIPCHK(launch_load_hidden(in->h1_in, in->h2_in, g0, cf.rms_eps, cf.d_model, cf.dtype, rows, m->at<float>(L.S),
+                              m->ws + L.Xn, cf.d_model, st));
+  }
+  return DBT_OK;
+}
+
+// Final norm is already in Xn (applied by the last layer); output matrix for the active rows.
+dbt_status lm_head(dbt_model *m, Rows rows, hipStream_t st) {
+  const dbt_config &cf = m->cfg;
+  const Layout &L = m->L;
+  const int xrow0 = rows.p0 * rows.Bp;
+  WSegs lm{{m->w.lm_head, nullptr, nullptr}, {cf.vocab, 0, 0}};
+  HIPCHK(launch_gemm(lm, cf.vocab, cf.d_model, cf.dtype, m->ws + L.Xn + (size_t)xrow0 * cf.d_model * esize(cf),
+                     cf.d_model, rows.np * rows.Bp, m->at<float>(L.logits) + (size_t)xrow0 * cf.vocab, cf.vocab,
+                     0, 1, st));
+  return DBT_OK;
+}
+
+dbt_status readout(dbt_model *m, int B, int Bp, bool branch, dbt_step_out *out, hipStream_t st) {
+  const dbt_config &cf = m->cfg;
+  const Layout &L = m->L;
+  if (cf.vocab <= 0) return DBT_OK;
+  MixArgs mx{};
+  mx.logits = m->at<float>(L.logits);
+  mx.V = cf.vocab;
+  mx.rows = Rows{B, Bp, 0, branch ? 2 : 1};
+  mx.chunk = kMixChunk;
+  mx.stats = m->at<float>(L.mstats);
+  mx.cand = m->at<float>(L.mcand);
+  mx.alpha = out ? out->alpha : nullptr;
+  mx.next = out ? out->next_token : nullptr;
+  if (mx.alpha || mx.next) HIPCHK(launch_mixture(mx, st));
+  if (out && out->logits1)
+    HIPCHK(hipMemcpyAsync(out->logits1, m->at<float>(L.logits), (size_t)B * cf.vocab * 4, hipMemcpyDeviceToDevice, st));
+  if (out && out->logits2 && branch)
+    HIPCHK(hipMemcpyAsync(out->logits2, m->at<float>(L.logits) + (size_t)Bp * cf.vocab, (size_t)B * cf.vocab * 4,
+                          hipMemcpyDeviceToDevice, st));
+  return DBT_OK;
+}
+
+dbt_status check_model_kv(dbt_model *m, dbt_kv *kv) {
+  if (!m || !kv) return fail(DBT_ERR_ARG, "model or cache is NULL");
+  if (kv->m != m) return fail(DBT_ERR_ARG, "cache belongs to another model");
+  return DBT_OK;
+}
+
+dbt_status check_step_in(dbt_model *m, dbt_kv *kv, const dbt_step_in *in, int need_branch_input) {
+  const dbt_config &cf = m->cfg;
+  if (!in) return fail(DBT_ERR_ARG, "step input is NULL");
+  if (in->batch <= 0 || in->batch > cf.max_batch) return fail(DBT_ERR_ARG, "batch %d out of [1, %d]", in->batch, cf.max_batch);
+  if (cf.has_embeddings) {
+    if (!in->tokens) return fail(DBT_ERR_ARG, "tokens are NULL");
+  } else {
+    if (!in->h1_in || (need_branch_input && !in->h2_in)) return fail(DBT_ERR_ARG, "residual inputs are NULL");
+  }
+  int need = 0;
+  for (int b = 0; b < in->batch; ++b) {
+    if (kv->len[b] + 1 > cf.max_pos) return fail(DBT_ERR_SHAPE, "sequence %d would exceed max_pos", b);
+    if (kv->len[b] % kPage == 0) {
+      if (kv->len[b] / kPage >= kv->mpps) return fail(DBT_ERR_NO_PAGES, "sequence %d page table full", b);
+      ++need;
+    }
+  }
+  if (need > (int)kv->free_pages.size()) return fail(DBT_ERR_NO_PAGES, "need %d free pages, have %zu", need, kv->free_pages.size());
+  return DBT_OK;
+}
+
+// Take pages for the new position of each sequence (batch order) and return
+// the positions pos_b = len_b.
+std::vector<int> begin_step(dbt_kv *kv, int B) {
+  std::vector<int> pos(B);
+  for (int b = 0; b < B; ++b) {
+    pos[b] = kv->len[b];
+    if (kv->len[b] % kPage == 0) {
+      const int p = kv->take_page();
+      kv->table[b].push_back(p);
+      kv->pending.push_back({b, (int)kv->table[b].size() - 1, p});
+    }
+  }
+  return pos;
+}
+
+dbt_status copy_rows(float *dst, const float *src, int B, int d, hipStream_t st) {
+  if (!dst) return DBT_OK;
+  HIPCHK(hipMemcpyAsync(dst, src, (size_t)B * d * 4, hipMemcpyDeviceToDevice, st));
+  return DBT_OK;
+}
+
+// Branch-only pass over all layers (ungrouped pass 2 and the boundary).
+dbt_status branch_pass(dbt_model *m, dbt_kv *kv, int B, int Bp, hipStream_t st) {
+  LayerCall lc{};
+  lc.rows = Rows{B, Bp, 1, 1};
+  lc.mode = MODE_BRANCH;
+  lc.retain = false;
+  lc.ret_src = -1;
+  lc.ret_dst = 0;
+  lc.prefill = false;
+  lc.rows_layout = 2 * Bp;
+  lc.last_norm = true;
+  for (int l = 0; l < m->cfg.n_layers; ++l) {
+    dbt_status s = run_layer(m, kv, l, lc, st);
+    if (s) return s;
+  }
+  if (m->cfg.vocab > 0) return lm_head(m, lc.rows, st);
+  return DBT_OK;
+}
+
+}  // namespace
+
+// ===========================================================================
+
+extern "C" {
+
+const char *dbt_last_error(void) { return g_err.c_str(); }
+
+size_t dbt_workspace_bytes(const dbt_config *cfg) {
+  if (check_config(cfg) != DBT_OK) return 0;
+  return make_layout(cfg).total;
+}
+
+size_t dbt_kv_pages_bytes(const dbt_config *cfg, int32_t num_pages) {
+  if (check_config(cfg) != DBT_OK || num_pages <= 0) return 0;
+  return (size_t)cfg->n_layers * num_pages * cfg->n_kv_heads * kPage * cfg->head_dim * (cfg->dtype == DBT_BF16 ? 2 : 4);
+}
+
+dbt_status dbt_create(const dbt_config *cfg, const dbt_weights *w, void *workspace, dbt_model **out) {
+  if (!out) return fail(DBT_ERR_ARG, "out is NULL");
+  *out = nullptr;
+  if (dbt_status cs = check_config(cfg)) return cs;
+  if (!w || !w->h_layers) return fail(DBT_ERR_ARG, "weights are NULL");
+  if (!workspace || ((uintptr_t)workspace & 255)) return fail(DBT_ERR_ARG, "workspace NULL or not 256-byte aligned");
+  if (cfg->has_embeddings && (!w->emb1 || !w->emb2 || !w->emb_norm)) return fail(DBT_ERR_ARG, "embeddings are NULL");
+  if (cfg->vocab > 0 && (!w->lm_head || !w->final_norm)) return fail(DBT_ERR_ARG, "output matrix or final norm is NULL");
+  for (int l = 0; l < cfg->n_layers; ++l) {
+    const dbt_layer_weights &L = w->h_layers[l];
+    if (!L.attn_norm || !L.wq || !L.wk || !L.wv || !L.wo || !L.mlp_norm || !L.w_gate || !L.w_up || !L.w_down ||
+        !L.a || !L.b || !L.c)
+      return fail(DBT_ERR_ARG, "layer %d has a NULL parameter", l);
+  }
+  dbt_model *m = new (std::nothrow) dbt_model();
+  if (!m) return fail(DBT_ERR_ARG, "out of host memory");
+  m->cfg = *cfg;
+  m->w = *w;
+  m->layers.assign(w->h_layers, w->h_layers + cfg->n_layers);
+  m->w.h_layers = nullptr;
+  m->ws = (char *)workspace;
+  m->L = make_layout(cfg);
+  // RoPE table (Eq. (8)): angle pos * theta^(-2i/d_h), evaluated in double.
+  const int half = cfg->head_dim / 2;
+  m->rope_host.resize((size_t)cfg->max_pos * half * 2);
+  for (int p = 0; p < cfg->max_pos; ++p)
+    for (int i = 0; i < half; ++i) {
+      const double ang = (double)p * std::pow((double)cfg->rope_theta, -2.0 * i / cfg->head_dim);
+      m->rope_host[((size_t)p * half + i) * 2 + 0] = (float)std::cos(ang);
+      m->rope_host[((size_t)p * half + i) * 2 + 1] = (float)std::sin(ang);
+    }
+  *out = m;
+  return DBT_OK;
+}
+
+dbt_status dbt_destroy(dbt_model *m) {
+  delete m;
+  return DBT_OK;
+}
+
+dbt_status dbt_kv_create(dbt_model *m, void *k_pages, void *v_pages, int32_t num_pages, int32_t *page_table,
+                         int32_t max_pages_per_seq, dbt_kv **out) {
+  if (!out) return fail(DBT_ERR_ARG, "out is NULL");
+  *out = nullptr;
+  if (!m || !k_pages || !v_pages || !page_table) return fail(DBT_ERR_ARG, "NULL argument");
+  if (num_pages <= 0 || max_pages_per_seq <= 0) return fail(DBT_ERR_ARG, "num_pages and max_pages_per_seq must be positive");
+  if ((long long)max_pages_per_seq * kPage < m->cfg.max_pos) return fail(DBT_ERR_SHAPE, "max_pages_per_seq * 16 < max_pos");
+  dbt_kv *kv = new (std::nothrow) dbt_kv();
+  if (!kv) return fail(DBT_ERR_ARG, "out of host memory");
+  kv->m = m;
+  kv->k = (char *)k_pages;
+  kv->v = (char *)v_pages;
+  kv->num_pages = num_pages;
+  kv->page_table = page_table;
+  kv->mpps = max_pages_per_seq;
+  std::vector<int> all(num_pages);
+  for (int i = 0; i < num_pages; ++i) all[i] = i;
+  kv->free_pages = std::priority_queue<int, std::vector<int>, std::greater<int>>(std::greater<int>(), std::move(all));
+  kv->table.assign(m->cfg.max_batch, {});
+  kv->len.assign(m->cfg.max_batch, 0);
+  *out = kv;
+  return DBT_OK;
+}
+
+dbt_status dbt_kv_destroy(dbt_kv *kv) {
+  delete kv;
+  return DBT_OK;
+}
+
+dbt_status dbt_kv_reserve(dbt_kv *kv, int32_t b, int32_t len, int32_t *h_pages_out) {
+  if (!kv) return fail(DBT_ERR_ARG, "cache is NULL");
+  if (b < 0 || b >= kv->m->cfg.max_batch) return fail(DBT_ERR_ARG, "sequence %d out of range", b);
+  if (len < kv->len[b]) return fail(DBT_ERR_ARG, "len %d below current length %d", len, kv->len[b]);
+  if (len > kv->m->cfg.max_pos) return fail(DBT_ERR_SHAPE, "len %d exceeds max_pos", len);
+  const int need_pages = (len + kPage - 1) / kPage;
+  if (need_pages > kv->mpps) return fail(DBT_ERR_NO_PAGES, "page table row too short");
+  const int extra = need_pages - (int)kv->table[b].size();
+  if (extra > (int)kv->free_pages.size()) return fail(DBT_ERR_NO_PAGES, "need %d free pages, have %zu", extra, kv->free_pages.size());
+  for (int i = 0; i < extra; ++i) {
+    const int p = kv->take_page();
+    kv->table[b].push_back(p);
+    kv->pending.push_back({b, (int)kv->table[b].size() - 1, p});
+  }
+  kv->len[b] = len;
+  if (h_pages_out)
+    for (size_t i = 0; i < kv->table[b].size(); ++i) h_pages_out[i] = kv->table[b][i];
+  if (kv->m->bnd_kv == kv) kv->m->bnd_kv = nullptr;
+  return DBT_OK;
+}
+
+dbt_status dbt_kv_truncate(dbt_kv *kv, int32_t b, int32_t len) {
+  if (!kv) return fail(DBT_ERR_ARG, "cache is NULL");
+  if (b < 0 || b >= kv->m->cfg.max_batch) return fail(DBT_ERR_ARG, "sequence %d out of range", b);
+  if (len < 0 || len > kv->len[b]) return fail(DBT_ERR_ARG, "len %d outside [0, %d]", len, kv->len[b]);
+  const size_t keep = (len + kPage - 1) / kPage;
+  for (size_t i = keep; i < kv->table[b].size(); ++i) kv->free_pages.push(kv->table[b][i]);
+  kv->table[b].resize(keep);
+  kv->len[b] = len;
+  // entries of pages given back may still sit in the pending list; they are
+  // harmless (a later take re-sends the slot) but drop those of this sequence
+  kv->pending.erase(std::remove_if(kv->pending.begin(), kv->pending.end(),
+                                   [&](const dbt_kv::Upd &u) { return u.b == b && (size_t)u.slot >= keep; }),
+                    kv->pending.end());
+  if (kv->m->bnd_kv == kv) kv->m->bnd_kv = nullptr;
+  return DBT_OK;
+}
+
+int32_t dbt_kv_length(const dbt_kv *kv, int32_t b) {
+  if (!kv || b < 0 || b >= kv->m->cfg.max_batch) return -1;
+  return kv->len[b];
+}
+
+int32_t dbt_kv_pages(const dbt_kv *kv, int32_t b, int32_t *h_out, int32_t cap) {
+  if (!kv || b < 0 || b >= kv->m->cfg.max_batch) return -1;
+  const int n = (int)kv->table[b].size();
+  for (int i = 0; i < n && i < cap && h_out; ++i) h_out[i] = kv->table[b][i];
+  return n;
+}
+
+dbt_status dbt_kv_fill(dbt_kv *kv, int32_t layer, int32_t b, int32_t start, int32_t count, const void *k_src,
+                       const void *v_src, dbt_stream stream) {
+  if (!kv || !k_src || !v_src) return fail(DBT_ERR_ARG, "NULL argument");
+  const dbt_config &cf = kv->m->cfg;
+  if (layer < 0 || layer >= cf.n_layers) return fail(DBT_ERR_ARG, "layer %d out of range", layer);
+  if (b < 0 || b >= cf.max_batch) return fail(DBT_ERR_ARG, "sequence %d out of range", b);
+  if (start < 0 || count < 0 || start + count > kv->len[b]) return fail(DBT_ERR_ARG, "positions outside the reserved length");
+  hipStream_t st = (hipStream_t)stream;
+  dbt_status s = ensure_device(kv->m, st);
+  if (s) return s;
+  s = flush(kv, nullptr, 0, st);
+  if (s) return s;
+  HIPCHK(launch_kv_fill(kv_layer(kv, layer), b, start, count, k_src, v_src, cf.dtype, st));
+  return DBT_OK;
+}
+
+dbt_status dbt_decode_step(dbt_model *m, dbt_kv *kv, const dbt_step_in *in, int32_t branch_on, dbt_step_out *out,
+                           dbt_stream stream) {
+  dbt_status s = check_model_kv(m, kv);
+  if (s) return s;
+  s = check_step_in(m, kv, in, branch_on);
+  if (s) return s;
+  hipStream_t st = (hipStream_t)stream;
+  const dbt_config &cf = m->cfg;
+  const int B = in->batch, Bp = round16(B);
+  m->bnd_kv = nullptr;
+  std::vector<int> pos = begin_step(kv, B);
+  if ((s = ensure_device(m, st))) return s;
+  if ((s = flush(kv, pos.data(), B, st))) return s;
+  const bool on = branch_on != 0;
+  const Rows rows{B, Bp, 0, on ? 2 : 1};
+  if ((s = load_inputs(m, in, in->tokens, rows, st))) return s;
+  LayerCall lc{};
+  lc.rows = rows;
+  lc.mode = on ? MODE_GROUPED : MODE_PRIMARY;
+  lc.retain = false;
+  lc.ret_src = -1;
+  lc.prefill = false;
+  lc.rows_layout = 2 * Bp;
+  lc.last_norm = true;
+  for (int l = 0; l < cf.n_layers; ++l)
+    if ((s = run_layer(m, kv, l, lc, st))) return s;
+  if (cf.vocab > 0 && (s = lm_head(m, rows, st))) return s;
+  for (int b = 0; b < B; ++b) kv->len[b] += 1;
+  if (out) {
+    if ((s = readout(m, B, Bp, on, out, st))) return s;
+    if ((s = copy_rows(out->h1_out, m->at<float>(m->L.S), B, cf.d_model, st))) return s;
+    if (on && (s = copy_rows(out->h2_out, m->at<float>(m->L.S) + (size_t)Bp * cf.d_model, B, cf.d_model, st))) return s;
+  }
+  return DBT_OK;
+}
+
+dbt_status dbt_decode_step_ungrouped(dbt_model *m, dbt_kv *kv, const dbt_step_in *in, dbt_step_out *out,
+                                     dbt_stream stream) {
+  dbt_status s = check_model_kv(m, kv);
+  if (s) return s;
+  s = check_step_in(m, kv, in, 1);
+  if (s) return s;
+  hipStream_t st = (hipStream_t)stream;
+  const dbt_config &cf = m->cfg;
+  const int B = in->batch, Bp = round16(B);
+  m->bnd_kv = nullptr;
+  std::vector<int> pos = begin_step(kv, B);
+  if ((s = ensure_device(m, st))) return s;
+  if ((s = flush(kv, pos.data(), B, st))) return s;
+  // pass 1: every primary layer, keeping Q1, H1, M1
+  const Rows prim{B, Bp, 0, 1};
+  if ((s = load_inputs(m, in, in->tokens, prim, st))) return s;
+  LayerCall lc{};
+  lc.rows = prim;
+  lc.mode = MODE_PRIMARY;
+  lc.retain = true;
+  lc.ret_src = -1;
+  lc.prefill = false;
+  lc.rows_layout = 2 * Bp;
+  lc.last_norm = true;
+  for (int l = 0; l < cf.n_layers; ++l)
+    if ((s = run_layer(m, kv, l, lc, st))) return s;
+  if (cf.vocab > 0 && (s = lm_head(m, prim, st))) return s;
+  // pass 2: every branch layer
+  const Rows br{B, Bp, 1, 1};
+  if ((s = load_inputs(m, in, in->tokens, br, st))) return s;
+  if ((s = branch_pass(m, kv, B, Bp, st))) return s;
+  for (int b = 0; b < B; ++b) kv->len[b] += 1;
+  if (out) {
+    if ((s = readout(m, B, Bp, true, out, st))) return s;
+    if ((s = copy_rows(out->h1_out, m->at<float>(m->L.S), B, cf.d_model, st))) return s;
+    if ((s = copy_rows(out->h2_out, m->at<float>(m->L.S) + (size_t)Bp * cf.d_model, B, cf.d_model, st))) return s;
+  }
+  return DBT_OK;
+}
+
+dbt_status dbt_prefill(dbt_model *m, dbt_kv *kv, const int32_t *tokens, const int32_t *h_prompt_lens, int32_t batch,
+                       int32_t run_boundary, dbt_step_out *out, dbt_stream stream) {
+  dbt_status s = check_model_kv(m, kv);
+  if (s) return s;
+  const dbt_config &cf = m->cfg;
+  if (!tokens || !h_prompt_lens) return fail(DBT_ERR_ARG, "tokens or prompt lengths NULL");
+  if (cf.max_prompt <= 0) return fail(DBT_ERR_STATE, "model created without prefill support (max_prompt = 0)");
+  if (batch <= 0 || batch > cf.max_batch) return fail(DBT_ERR_ARG, "batch %d out of [1, %d]", batch, cf.max_batch);
+  int need = 0;
+  for (int b = 0; b < batch; ++b) {
+    const int T = h_prompt_lens[b];
+    if (T <= 0 || T > cf.max_prompt) return fail(DBT_ERR_SHAPE, "prompt %d length %d outside [1, %d]", b, T, cf.max_prompt);
+    if (kv->len[b] != 0) return fail(DBT_ERR_STATE, "sequence %d is not empty", b);
+    need += (T + kPage - 1) / kPage;
+  }
+  if (need > (int)kv->free_pages.size()) return fail(DBT_ERR_NO_PAGES, "need %d free pages, have %zu", need, kv->free_pages.size());
+  hipStream_t st = (hipStream_t)stream;
+  for (int b = 0; b < batch; ++b) {  // pages for every sequence first, in batch order
+    const int np = (h_prompt_lens[b] + kPage - 1) / kPage;
+    for (int i = 0; i < np; ++i) {
+      const int p = kv->take_page();
+      kv->table[b].push_back(p);
+      kv->pending.push_back({b, i, p});
+    }
+    kv->len[b] = h_prompt_lens[b];
+  }
+  if ((s = ensure_device(m, st))) return s;
+  if ((s = flush(kv, nullptr, 0, st))) return s;
+  const Layout &L = m->L;
+  const int d = cf.d_model;
+  const int Bp = round16(batch);
+  size_t off = 0;
+  for (int b = 0; b < batch; ++b) {
+    const int T = h_prompt_lens[b];
+    const Rows rows{T, T, 0, 1};
+    HIPCHK(launch_embed(tokens + off, cf.vocab, m->w.emb1, m->w.emb2, m->w.emb_norm, m->layers[0].attn_norm, cf.rms_eps, d,
+                        cf.dtype, rows, m->at<float>(L.S), m->ws + L.Xn, d, st));
+    LayerCall lc{};
+    lc.rows = rows;
+    lc.mode = MODE_PRIMARY;
+    lc.retain = true;
+    lc.ret_src = T - 1;
+    lc.ret_dst = b;
+    lc.prefill = true;
+    lc.seq = b;
+    lc.rows_layout = T;
+    lc.last_norm = false;
+    for (int l = 0; l < cf.n_layers; ++l)
+      if ((s = run_layer(m, kv, l, lc, st))) return s;
+    HIPCHK(hipMemcpyAsync(m->at<float>(L.slast) + (size_t)b * d, m->at<float>(L.S) + (size_t)(T - 1) * d, d * 4,
+                          hipMemcpyDeviceToDevice, st));
+    HIPCHK(hipMemcpyAsync(m->at<int>(L.btok) + b, tokens + off + T - 1, 4, hipMemcpyDeviceToDevice, st));
+    off += T;
+  }
+  // primary logits at each prompt's final position
+  if (cf.vocab > 0) {
+    HIPCHK(launch_rmsnorm_rows(m->at<float>(L.slast), m->w.final_norm, cf.rms_eps, d, cf.dtype, Rows{batch, 0, 0, 1},
+                               m->ws + L.Xn, d, st));
+    if ((s = lm_head(m, Rows{batch, Bp, 0, 1}, st))) return s;
+  }
+  if (out) {
+    if ((s = copy_rows(out->h1_out, m->at<float>(L.slast), batch, d, st))) return s;
+  }
+  m->bnd_kv = kv;
+  m->bnd_batch = batch;
+  if (run_boundary) return dbt_boundary(m, kv, batch, out, stream);
+  if (out && (s = readout(m, batch, Bp, false, out, st))) return s;
+  return DBT_OK;
+}
+
+dbt_status dbt_boundary(dbt_model *m, dbt_kv *kv, int32_t batch, dbt_step_out *out, dbt_stream stream) {
+  dbt_status s = check_model_kv(m, kv);
+  if (s) return s;
+  if (m->bnd_kv != kv || batch != m->bnd_batch)
+    return fail(DBT_ERR_STATE, "boundary must directly follow dbt_prefill on the same cache and batch");
+  hipStream_t st = (hipStream_t)stream;
+  const dbt_config &cf = m->cfg;
+  const Layout &L = m->L;
+  const int B = batch, Bp = round16(B);
+  if ((s = ensure_device(m, st))) return s;
+  std::vector<int> pos(B);
+  for (int b = 0; b < B; ++b) pos[b] = kv->len[b] - 1;
+  if ((s = flush(kv, pos.data(), B, st))) return s;
+  const Rows br{B, Bp, 1, 1};
+  HIPCHK(launch_embed(m->at<int>(L.btok), cf.vocab, m->w.emb1, m->w.emb2, m->w.emb_norm, m->layers[0].attn_norm, cf.rms_eps,
+                      cf.d_model, cf.dtype, br, m->at<float>(L.S), m->ws + L.Xn, cf.d_model, st));
+  if ((s = branch_pass(m, kv, B, Bp, st))) return s;
+  m->bnd_kv = nullptr;
+  if (out) {
+    if ((s = readout(m, B, Bp, true, out, st))) return s;
+    if ((s = copy_rows(out->h2_out, m->at<float>(L.S) + (size_t)Bp * cf.d_model, B, cf.d_model, st))) return s;
+  }
+  return DBT_OK;
+}
+
+}  // extern "C"

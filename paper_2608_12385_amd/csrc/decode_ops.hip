@@ -1,0 +1,475 @@
+// Row-wise stages of the decode step: embeddings (Eq. (7)), RMSNorms, the
+// epilogues that finish each projection (RoPE + query coupling + cache
+// append, Eqs. (8)-(11); residual adds; SwiGLU + MLP coupling, Eq. (14);
+// output coupling, Eq. (15)), direct cache fill, and the mixture readout
+// (Sec. 4.2, Eqs. (17)-(18)).
+//
+// Split-K partial slabs are always added in split order, and every reduction
+// has a fixed order, so results are deterministic and a row's value does not
+// depend on which other rows are active.
+#include "common.h"
+#include "kernels.h"
+
+namespace dbt {
+
+namespace {
+
+__device__ __forceinline__ int phys_row(const Rows &r, int path, int b) { return path * r.Bp + b; }
+
+__device__ __forceinline__ float psum(const float *part, long long stride, int S, size_t idx) {
+  float s = 0.f;
+  for (int k = 0; k < S; ++k) s += part[k * stride + idx];
+  return s;
+}
+
+// ---------------------------------------------------------------------------
+
+__global__ void k_step_begin(StepBegin sb, int *pos_arr, int *page_table, int mpps) {
+  const int t = threadIdx.x;
+  if (t < sb.n_pos) pos_arr[sb.b0 + t] = sb.pos[t];
+  if (t < sb.n_pt) page_table[(size_t)sb.pt_b[t] * mpps + sb.pt_slot[t]] = sb.pt_page[t];
+}
+
+// y = x / sqrt(mean(x^2) + eps) * g written to out (dtype T); x read from src.
+template <typename T>
+__device__ void norm_row(const float *x, const float *g, float eps, int d, T *out, float *red) {
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) ss += x[i] * x[i];
+  ss = block_sum(ss, red);
+  const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+  for (int i = threadIdx.x; i < d; i += blockDim.x) st<T>(out, i, x[i] * inv * g[i]);
+}
+
+// Tokens outside [0, vocab) read as a zero embedding row (no out-of-bounds read).
+template <typename T>
+__global__ void k_embed(const int *tokens, int vocab, const T *e1, const T *e2, const float *g_emb,
+                        const float *g_next, float eps, int d, Rows rows, float *S, T *Xn, int ldx) {
+  __shared__ float red[16];
+  const int b = blockIdx.x, path = rows.p0 + blockIdx.y;
+  const int row = phys_row(rows, path, b);
+  const int tok = tokens[b];
+  const bool valid = tok >= 0 && tok < vocab;
+  const T *e = (path == 0 ? e1 : e2) + (size_t)(valid ? tok : 0) * d;
+  float *s = S + (size_t)row * d;
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) {
+    const float v = valid ? ld<T>(e, i) : 0.f;
+    s[i] = v;
+    ss += v * v;
+  }
+  ss = block_sum(ss, red);
+  const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+  for (int i = threadIdx.x; i < d; i += blockDim.x) s[i] = s[i] * inv * g_emb[i];
+  __syncthreads();
+  norm_row<T>(s, g_next, eps, d, Xn + (size_t)row * ldx, red);
+}
+
+template <typename T>
+__global__ void k_load_hidden(const float *h1, const float *h2, const float *g_next, float eps, int d,
+                              Rows rows, float *S, T *Xn, int ldx) {
+  __shared__ float red[16];
+  const int b = blockIdx.x, path = rows.p0 + blockIdx.y;
+  const int row = phys_row(rows, path, b);
+  const float *h = (path == 0 ? h1 : h2) + (size_t)b * d;
+  float *s = S + (size_t)row * d;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) s[i] = h[i];
+  __syncthreads();
+  norm_row<T>(s, g_next, eps, d, Xn + (size_t)row * ldx, red);
+}
+
+template <typename T>
+__global__ void k_rmsnorm_rows(const float *S, const float *g, float eps, int d, Rows rows, T *Xn, int ldx) {
+  __shared__ float red[16];
+  const int row = phys_row(rows, rows.p0 + blockIdx.y, blockIdx.x);
+  norm_row<T>(S + (size_t)row * d, g, eps, d, Xn + (size_t)row * ldx, red);
+}
+
+// ---------------------------------------------------------------------------
+// QKV epilogue: one thread per rotation pair (i, i + d_h/2) of a query head,
+// a key head or a value head.  Primary: Q1, K1 = RoPE(.), V1; K1/V1 go to the
+// cache slot of position pos (Sec. 4.4: the primary appends).  Branch:
+// Q2 = RoPE(.), Q2~ = Q2 + a * Q1 (Eq. (11)); the branch writes no cache.
+template <typename T>
+__global__ void k_qkv_finish(QKVFinish f) {
+  const int b = blockIdx.y;
+  const int half = f.d_h / 2;
+  const int nqp = f.n_q * half, nkp = f.n_kv * half;
+  const bool prim = f.mode != MODE_BRANCH, br = f.mode != MODE_PRIMARY;
+  const int total = prim ? nqp + 2 * nkp : nqp;
+  const int pi = blockIdx.x * blockDim.x + threadIdx.x;
+  if (pi >= total) return;
+  const int pos = f.pos_arr ? f.pos_arr[b] : b;
+  const int seq = f.pos_arr ? b : f.seq_fixed;
+  const int dq = f.n_q * f.d_h, dkv = f.n_kv * f.d_h;
+  const int r1 = phys_row(f.rows, 0, b), r2 = phys_row(f.rows, 1, b);
+  const int i = pi % half;
+  const float2 cs = f.rope[(size_t)pos * half + i];
+  if (pi < nqp) {
+    const int c0 = (pi / half) * f.d_h + i, c1 = c0 + half;
+    float q1a = 0.f, q1b = 0.f;
+    if (prim) {
+      const float x0 = psum(f.part, f.split_stride, f.S, (size_t)r1 * f.ldp + c0);
+      const float x1 = psum(f.part, f.split_stride, f.S, (size_t)r1 * f.ldp + c1);
+      q1a = x0 * cs.x - x1 * cs.y;
+      q1b = x0 * cs.y + x1 * cs.x;
+      f.Q[(size_t)r1 * dq + c0] = q1a;
+      f.Q[(size_t)r1 * dq + c1] = q1b;
+      if (f.ret.ptr && (f.ret.src_row < 0 || f.ret.src_row == b)) {
+        const int dst = f.ret.src_row < 0 ? b : f.ret.dst_row;
+        f.ret.ptr[(size_t)dst * dq + c0] = q1a;
+        f.ret.ptr[(size_t)dst * dq + c1] = q1b;
+      }
+    } else {
+      q1a = f.Q1_in[(size_t)b * dq + c0];
+      q1b = f.Q1_in[(size_t)b * dq + c1];
+    }
+    if (br) {
+      const float y0 = psum(f.part, f.split_stride, f.S, (size_t)r2 * f.ldp + c0);
+      const float y1 = psum(f.part, f.split_stride, f.S, (size_t)r2 * f.ldp + c1);
+      const float q2a = y0 * cs.x - y1 * cs.y;
+      const float q2b = y0 * cs.y + y1 * cs.x;
+      f.Q[(size_t)r2 * dq + c0] = q2a + f.a[c0] * q1a;
+      f.Q[(size_t)r2 * dq + c1] = q2b + f.a[c1] * q1b;
+    }
+    return;
+  }
+  // keys and values (primary only): cache slot of position pos
+  const int page = f.kv.page_table[(size_t)seq * f.kv.mpps + pos / 16];
+  const int slot = pos % 16;
+  const int j = pi - nqp;
+  T *kp = (T *)f.kv.k;
+  T *vp = (T *)f.kv.v;
+  if (j < nkp) {
+    const int g = j / half;
+    const int c0 = dq + g * f.d_h + i;
+    const float x0 = psum(f.part, f.split_stride, f.S, (size_t)r1 * f.ldp + c0);
+    const float x1 = psum(f.part, f.split_stride, f.S, (size_t)r1 * f.ldp + c0 + half);
+    const size_t base = (((size_t)page * f.n_kv + g) * 16 + slot) * f.d_h;
+    st<T>(kp, base + i, x0 * cs.x - x1 * cs.y);
+    st<T>(kp, base + i + half, x0 * cs.y + x1 * cs.x);
+  } else {
+    const int g = (j - nkp) / half;
+    const int c0 = dq + dkv + g * f.d_h + i;
+    const float v0 = psum(f.part, f.split_stride, f.S, (size_t)r1 * f.ldp + c0);
+    const float v1 = psum(f.part, f.split_stride, f.S, (size_t)r1 * f.ldp + c0 + half);
+    const size_t base = ((size_t)page * f.n_kv + g) * f.d_h;
+    st<T>(vp, (base + i) * 16 + slot, v0);
+    st<T>(vp, (base + i + half) * 16 + slot, v1);
+  }
+}
+
+// After the attention output projection: S_bar = S + A (in place), then the
+// MLP input RMSNorm.
+template <typename T>
+__global__ void k_resid_norm(const float *part, long long stride, int S, int ldp, float *Sres,
+                             const float *g, float eps, int d, Rows rows, T *Xn, int ldx) {
+  __shared__ float red[16];
+  const int row = phys_row(rows, rows.p0 + blockIdx.y, blockIdx.x);
+  float *s = Sres + (size_t)row * d;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) s[i] += psum(part, stride, S, (size_t)row * ldp + i);
+  __syncthreads();
+  norm_row<T>(s, g, eps, d, Xn + (size_t)row * ldx, red);
+}
+
+// SwiGLU and the MLP-intermediate coupling H2~ = H2 + b * H1 (Eq. (14)).
+// Gate rows are columns [0, f) of the projection, up rows [f, 2f).
+template <typename T>
+__global__ void k_swiglu_finish(const float *part, long long stride, int S, int ldp, int f, int mode,
+                                Rows rows, const float *bvec, const float *H1_in, Retain ret, T *Xh,
+                                int ldh) {
+  const int b = blockIdx.y;
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= f) return;
+  const bool prim = mode != MODE_BRANCH, br = mode != MODE_PRIMARY;
+  const int r1 = phys_row(rows, 0, b), r2 = phys_row(rows, 1, b);
+  float h1;
+  if (prim) {
+    const float gt = psum(part, stride, S, (size_t)r1 * ldp + j);
+    const float up = psum(part, stride, S, (size_t)r1 * ldp + f + j);
+    h1 = gt / (1.0f + expf(-gt)) * up;
+    st<T>(Xh, (size_t)r1 * ldh + j, h1);
+    if (ret.ptr && (ret.src_row < 0 || ret.src_row == b))
+      ret.ptr[(size_t)(ret.src_row < 0 ? b : ret.dst_row) * f + j] = h1;
+  } else {
+    h1 = H1_in[(size_t)b * f + j];
+  }
+  if (br) {
+    const float gt = psum(part, stride, S, (size_t)r2 * ldp + j);
+    const float up = psum(part, stride, S, (size_t)r2 * ldp + f + j);
+    const float h2 = gt / (1.0f + expf(-gt)) * up;
+    st<T>(Xh, (size_t)r2 * ldh + j, h2 + bvec[j] * h1);
+  }
+}
+
+// After the MLP down projection: M1, M2 = M2' + c * M1 (Eq. (15)),
+// S <- S_bar + M (Eq. (16)), then the next RMSNorm (next layer's attention
+// norm, or the final norm before the output matrix).
+template <typename T>
+__global__ void k_down_finish(const float *part, long long stride, int S, int ldp, int d, int mode,
+                              Rows rows, const float *cvec, const float *M1_in, Retain ret,
+                              float *Sres, const float *g_next, float eps, T *Xn, int ldx) {
+  __shared__ float red[16];
+  const int b = blockIdx.x;
+  const bool prim = mode != MODE_BRANCH, br = mode != MODE_PRIMARY;
+  const int r1 = phys_row(rows, 0, b), r2 = phys_row(rows, 1, b);
+  float *s1 = Sres + (size_t)r1 * d;
+  float *s2 = Sres + (size_t)r2 * d;
+  const bool keep = ret.ptr && (ret.src_row < 0 || ret.src_row == b);
+  float *kept = keep ? ret.ptr + (size_t)(ret.src_row < 0 ? b : ret.dst_row) * d : nullptr;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) {
+    float m1;
+    if (prim) {
+      m1 = psum(part, stride, S, (size_t)r1 * ldp + i);
+      s1[i] += m1;
+      if (keep) kept[i] = m1;
+    } else {
+      m1 = M1_in[(size_t)b * d + i];
+    }
+    if (br) s2[i] += psum(part, stride, S, (size_t)r2 * ldp + i) + cvec[i] * m1;
+  }
+  if (!g_next) return;
+  __syncthreads();
+  if (prim) norm_row<T>(s1, g_next, eps, d, Xn + (size_t)r1 * ldx, red);
+  if (br) {
+    __syncthreads();
+    norm_row<T>(s2, g_next, eps, d, Xn + (size_t)r2 * ldx, red);
+  }
+}
+
+// ---------------------------------------------------------------------------
+
+template <typename E>
+__global__ void k_kv_fill(KVRef kv, int seq, int start, const E *ksrc, const E *vsrc) {
+  const int x = blockIdx.x, g = blockIdx.y, t = threadIdx.x;
+  const int pos = start + x;
+  const int page = kv.page_table[(size_t)seq * kv.mpps + pos / 16];
+  const int slot = pos % 16;
+  const size_t src = ((size_t)x * kv.n_kv + g) * kv.d_h + t;
+  ((E *)kv.k)[(((size_t)page * kv.n_kv + g) * 16 + slot) * kv.d_h + t] = ksrc[src];
+  ((E *)kv.v)[(((size_t)page * kv.n_kv + g) * kv.d_h + t) * 16 + slot] = vsrc[src];
+}
+
+// ---------------------------------------------------------------------------
+// Mixture readout.  Per (row, chunk) statistics (max, sum e^(z-max),
+// sum e^(2(z-max))) give, after a fixed-order merge, lse and the collision
+// probability sum p^2 = sum e^(2z) / (sum e^z)^2 (Eq. (18)); then the greedy
+// token of alpha p + (1 - alpha) q, lowest index on ties.
+
+__device__ __forceinline__ void argmax_merge(float &v, int &i, float v2, int i2) {
+  if (v2 > v || (v2 == v && i2 < i)) { v = v2; i = i2; }
+}
+
+__global__ void k_mix_stats(MixArgs m) {
+  __shared__ float red[16];
+  const int c = blockIdx.x;
+  const int y = blockIdx.y;
+  const int path = m.rows.p0 + y / m.rows.B, b = y % m.rows.B;
+  const int row = phys_row(m.rows, path, b);
+  const int nch = (m.V + m.chunk - 1) / m.chunk;
+  const int lo = c * m.chunk, hi = min(m.V, lo + m.chunk);
+  const float *z = m.logits + (size_t)row * m.V;
+  float mx = -INFINITY;
+  for (int v = lo + threadIdx.x; v < hi; v += blockDim.x) mx = fmaxf(mx, z[v]);
+  mx = block_max(mx, red);
+  float s1 = 0.f, s2 = 0.f;
+  for (int v = lo + threadIdx.x; v < hi; v += blockDim.x) {
+    const float e = expf(z[v] - mx);
+    s1 += e;
+    s2 += e * e;
+  }
+  s1 = block_sum(s1, red);
+  s2 = block_sum(s2, red);
+  if (threadIdx.x == 0) {
+    float *o = m.stats + ((size_t)row * nch + c) * 3;
+    o[0] = mx;
+    o[1] = s1;
+    o[2] = s2;
+  }
+}
+
+__device__ void merged_stats(const MixArgs &m, int row, float &lse, float &p2) {
+  const int nch = (m.V + m.chunk - 1) / m.chunk;
+  const float *st = m.stats + (size_t)row * nch * 3;
+  float mx = -INFINITY;
+  for (int c = 0; c < nch; ++c) mx = fmaxf(mx, st[c * 3]);
+  float z = 0.f, y = 0.f;
+  for (int c = 0; c < nch; ++c) {
+    const float e = expf(st[c * 3] - mx);
+    z += st[c * 3 + 1] * e;
+    y += st[c * 3 + 2] * e * e;
+  }
+  lse = mx + logf(z);
+  p2 = y / (z * z);
+}
+
+__global__ void k_mix_argmax(MixArgs m) {
+  __shared__ float rv[16];
+  __shared__ int ri[16];
+  const int c = blockIdx.x, b = blockIdx.y;
+  const bool on = m.rows.np == 2;
+  const int nch = (m.V + m.chunk - 1) / m.chunk;
+  const int r1 = phys_row(m.rows, 0, b), r2 = phys_row(m.rows, 1, b);
+  float lse1 = 0.f, p2 = 0.f, lse2 = 0.f, alpha = 1.f;
+  if (on) {
+    merged_stats(m, r1, lse1, p2);
+    float dummy;
+    merged_stats(m, r2, lse2, dummy);
+    alpha = fminf(1.f, fmaxf(0.5f, p2));
+  }
+  const int lo = c * m.chunk, hi = min(m.V, lo + m.chunk);
+  const float *z1 = m.logits + (size_t)r1 * m.V;
+  const float *z2 = m.logits + (size_t)r2 * m.V;
+  float best = -INFINITY;
+  int bi = 0x7fffffff;
+  for (int v = lo + threadIdx.x; v < hi; v += blockDim.x) {
+    const float val = on ? alpha * expf(z1[v] - lse1) + (1.f - alpha) * expf(z2[v] - lse2) : z1[v];
+    argmax_merge(best, bi, val, v);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float v2 = __shfl_xor(best, o, 64);
+    const int i2 = __shfl_xor(bi, o, 64);
+    argmax_merge(best, bi, v2, i2);
+  }
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  if (lane == 0) { rv[w] = best; ri[w] = bi; }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int k = 1; k < (int)(blockDim.x >> 6); ++k) argmax_merge(best, bi, rv[k], ri[k]);
+    float *o = m.cand + ((size_t)b * nch + c) * 2;
+    o[0] = best;
+    o[1] = __int_as_float(bi);
+    if (c == 0 && m.alpha) m.alpha[b] = alpha;
+  }
+}
+
+__global__ void k_mix_final(MixArgs m) {
+  const int b = blockIdx.x;
+  if (threadIdx.x != 0) return;
+  const int nch = (m.V + m.chunk - 1) / m.chunk;
+  float best = -INFINITY;
+  int bi = 0x7fffffff;
+  for (int c = 0; c < nch; ++c) {
+    const float *o = m.cand + ((size_t)b * nch + c) * 2;
+    argmax_merge(best, bi, o[0], __float_as_int(o[1]));
+  }
+  if (m.next) m.next[b] = bi;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+
+hipError_t launch_step_begin(const StepBegin &sb, int *pos_arr, int *page_table, int mpps, hipStream_t st) {
+  if (sb.n_pos == 0 && sb.n_pt == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_step_begin, dim3(1), dim3(64), 0, st, sb, pos_arr, page_table, mpps);
+  return hipGetLastError();
+}
+
+hipError_t launch_embed(const int *tokens, int vocab, const void *e1, const void *e2, const float *g_emb,
+                        const float *g_next, float eps, int d, int dtype, Rows rows, float *S,
+                        void *Xn, int ldx, hipStream_t st) {
+  dim3 grid(rows.B, rows.np);
+  if (dtype == 1)
+    hipLaunchKernelGGL(k_embed<uint16_t>, grid, dim3(256), 0, st, tokens, vocab, (const uint16_t *)e1,
+                       (const uint16_t *)e2, g_emb, g_next, eps, d, rows, S, (uint16_t *)Xn, ldx);
+  else
+    hipLaunchKernelGGL(k_embed<float>, grid, dim3(256), 0, st, tokens, vocab, (const float *)e1,
+                       (const float *)e2, g_emb, g_next, eps, d, rows, S, (float *)Xn, ldx);
+  return hipGetLastError();
+}
+
+hipError_t launch_load_hidden(const float *h1, const float *h2, const float *g_next, float eps,
+                              int d, int dtype, Rows rows, float *S, void *Xn, int ldx, hipStream_t st) {
+  dim3 grid(rows.B, rows.np);
+  if (dtype == 1)
+    hipLaunchKernelGGL(k_load_hidden<uint16_t>, grid, dim3(256), 0, st, h1, h2, g_next, eps, d, rows, S,
+                       (uint16_t *)Xn, ldx);
+  else
+    hipLaunchKernelGGL(k_load_hidden<float>, grid, dim3(256), 0, st, h1, h2, g_next, eps, d, rows, S,
+                       (float *)Xn, ldx);
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm_rows(const float *S, const float *g, float eps, int d, int dtype, Rows rows,
+                               void *Xn, int ldx, hipStream_t st) {
+  dim3 grid(rows.B, rows.np);
+  if (dtype == 1)
+    hipLaunchKernelGGL(k_rmsnorm_rows<uint16_t>, grid, dim3(256), 0, st, S, g, eps, d, rows, (uint16_t *)Xn, ldx);
+  else
+    hipLaunchKernelGGL(k_rmsnorm_rows<float>, grid, dim3(256), 0, st, S, g, eps, d, rows, (float *)Xn, ldx);
+  return hipGetLastError();
+}
+
+hipError_t launch_qkv_finish(const QKVFinish &f, hipStream_t st) {
+  const int half = f.d_h / 2;
+  const int total = f.mode != MODE_BRANCH ? (f.n_q + 2 * f.n_kv) * half : f.n_q * half;
+  dim3 grid((total + 255) / 256, f.rows.B);
+  if (f.dtype == 1)
+    hipLaunchKernelGGL(k_qkv_finish<uint16_t>, grid, dim3(256), 0, st, f);
+  else
+    hipLaunchKernelGGL(k_qkv_finish<float>, grid, dim3(256), 0, st, f);
+  return hipGetLastError();
+}
+
+hipError_t launch_resid_norm(const float *part, long long stride, int S, int ldp, float *Sres,
+                             const float *g, float eps, int d, int dtype, Rows rows, void *Xn, int ldx,
+                             hipStream_t st) {
+  dim3 grid(rows.B, rows.np);
+  if (dtype == 1)
+    hipLaunchKernelGGL(k_resid_norm<uint16_t>, grid, dim3(256), 0, st, part, stride, S, ldp, Sres, g, eps, d,
+                       rows, (uint16_t *)Xn, ldx);
+  else
+    hipLaunchKernelGGL(k_resid_norm<float>, grid, dim3(256), 0, st, part, stride, S, ldp, Sres, g, eps, d,
+                       rows, (float *)Xn, ldx);
+  return hipGetLastError();
+}
+
+hipError_t launch_swiglu_finish(const float *part, long long stride, int S, int ldp, int f, int mode,
+                                Rows rows, const float *bvec, const float *H1_in, Retain ret, int dtype,
+                                void *Xh, int ldh, hipStream_t st) {
+  dim3 grid((f + 255) / 256, rows.B);
+  if (dtype == 1)
+    hipLaunchKernelGGL(k_swiglu_finish<uint16_t>, grid, dim3(256), 0, st, part, stride, S, ldp, f, mode, rows,
+                       bvec, H1_in, ret, (uint16_t *)Xh, ldh);
+  else
+    hipLaunchKernelGGL(k_swiglu_finish<float>, grid, dim3(256), 0, st, part, stride, S, ldp, f, mode, rows,
+                       bvec, H1_in, ret, (float *)Xh, ldh);
+  return hipGetLastError();
+}
+
+hipError_t launch_down_finish(const float *part, long long stride, int S, int ldp, int d, int mode,
+                              Rows rows, const float *cvec, const float *M1_in, Retain ret, float *Sres,
+                              const float *g_next, float eps, int dtype, void *Xn, int ldx, hipStream_t st) {
+  dim3 grid(rows.B);
+  if (dtype == 1)
+    hipLaunchKernelGGL(k_down_finish<uint16_t>, grid, dim3(256), 0, st, part, stride, S, ldp, d, mode, rows,
+                       cvec, M1_in, ret, Sres, g_next, eps, (uint16_t *)Xn, ldx);
+  else
+    hipLaunchKernelGGL(k_down_finish<float>, grid, dim3(256), 0, st, part, stride, S, ldp, d, mode, rows,
+                       cvec, M1_in, ret, Sres, g_next, eps, (float *)Xn, ldx);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_fill(KVRef kv, int seq, int start, int count, const void *ksrc, const void *vsrc,
+                          int dtype, hipStream_t st) {
+  if (count <= 0) return hipSuccess;
+  dim3 grid(count, kv.n_kv);
+  if (dtype == 1)
+    hipLaunchKernelGGL(k_kv_fill<uint16_t>, grid, dim3(kv.d_h), 0, st, kv, seq, start,
+                       (const uint16_t *)ksrc, (const uint16_t *)vsrc);
+  else
+    hipLaunchKernelGGL(k_kv_fill<uint32_t>, grid, dim3(kv.d_h), 0, st, kv, seq, start,
+                       (const uint32_t *)ksrc, (const uint32_t *)vsrc);
+  return hipGetLastError();
+}
+
+hipError_t launch_mixture(const MixArgs &m, hipStream_t st) {
+  const int nch = (m.V + m.chunk - 1) / m.chunk;
+  hipLaunchKernelGGL(k_mix_stats, dim3(nch, m.rows.np * m.rows.B), dim3(256), 0, st, m);
+  hipLaunchKernelGGL(k_mix_argmax, dim3(nch, m.rows.B), dim3(256), 0, st, m);
+  hipLaunchKernelGGL(k_mix_final, dim3(m.rows.B), dim3(64), 0, st, m);
+  return hipGetLastError();
+}
+
+}  // namespace dbt

@@ -1,0 +1,137 @@
+// Launchers of the device kernels (internal to the library; the public
+// interface is include/dbt.h).  Every launcher enqueues on `st` and returns
+// hipGetLastError() of its launches.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dbt {
+
+// Up to three stacked weight matrices that one projection reads as one
+// [sum rows][K] operand (e.g. W_Q; W_K; W_V).  Unused entries have rows 0.
+struct WSegs {
+  const void *w[3];
+  int rows[3];
+};
+
+// Which activation rows a kernel processes.  Activations of a call are laid
+// out [2][Bp][width]: path p (0 primary, 1 branch) sequence b sits at
+// physical row p*Bp + b, Bp = batch rounded up to 16.
+struct Rows {
+  int B;   // sequences
+  int Bp;  // row stride between the two paths
+  int p0;  // first active path
+  int np;  // active paths (1 or 2)
+};
+
+enum Mode { MODE_GROUPED = 0, MODE_PRIMARY = 1, MODE_BRANCH = 2 };
+
+// Retention of primary intermediates for a later branch evaluation.
+// src_row < 0: row b of the call is kept at retained row b (all rows);
+// src_row >= 0: only that row is kept, at retained row dst_row.
+struct Retain {
+  float *ptr;  // NULL: nothing kept
+  int src_row, dst_row;
+};
+
+struct KVRef {
+  void *k, *v;            // pages of this layer: k/v base + layer offset already applied
+  const int *page_table;  // [max_batch][mpps]
+  int mpps;               // entries per sequence
+  int n_kv, d_h;
+};
+
+// ---- projections ----
+int gemm_splits(int n_full, int K, int dtype);
+hipError_t launch_gemm(const WSegs &segs, int N, int K, int dtype, const void *X, int ldx, int M,
+                       float *Y, int ldy, long long y_split_stride, int S, hipStream_t st);
+
+// ---- row-wise and elementwise stages ----
+struct StepBegin {
+  int n_pos, b0;
+  int pos[64];
+  int n_pt;
+  int pt_b[64], pt_slot[64], pt_page[64];
+};
+hipError_t launch_step_begin(const StepBegin &sb, int *pos_arr, int *page_table, int mpps,
+                             hipStream_t st);
+
+hipError_t launch_embed(const int *tokens, int vocab, const void *e1, const void *e2, const float *g_emb,
+                        const float *g_next, float eps, int d, int dtype, Rows rows, float *S,
+                        void *Xn, int ldx, hipStream_t st);
+hipError_t launch_load_hidden(const float *h1, const float *h2, const float *g_next, float eps,
+                              int d, int dtype, Rows rows, float *S, void *Xn, int ldx,
+                              hipStream_t st);
+hipError_t launch_rmsnorm_rows(const float *S, const float *g, float eps, int d, int dtype,
+                               Rows rows, void *Xn, int ldx, hipStream_t st);
+
+struct QKVFinish {
+  const float *part;
+  long long split_stride;
+  int S, ldp;
+  int n_q, n_kv, d_h;
+  Rows rows;
+  int mode;
+  const float2 *rope;  // [max_pos][d_h/2] (cos, sin)
+  const int *pos_arr;  // decode: position of sequence b (NULL: prefill)
+  int seq_fixed;       // prefill: the sequence; the row index is the position
+  const float *a;
+  float *Q;            // [2Bp][n_q*d_h]
+  const float *Q1_in;  // branch mode: retained primary queries [*, n_q*d_h]
+  Retain ret;
+  KVRef kv;
+  int dtype;
+};
+hipError_t launch_qkv_finish(const QKVFinish &f, hipStream_t st);
+
+hipError_t launch_resid_norm(const float *part, long long split_stride, int S, int ldp, float *Sres,
+                             const float *g, float eps, int d, int dtype, Rows rows, void *Xn,
+                             int ldx, hipStream_t st);
+
+hipError_t launch_swiglu_finish(const float *part, long long split_stride, int S, int ldp, int f,
+                                int mode, Rows rows, const float *bvec, const float *H1_in,
+                                Retain ret, int dtype, void *Xh, int ldh, hipStream_t st);
+
+hipError_t launch_down_finish(const float *part, long long split_stride, int S, int ldp, int d,
+                              int mode, Rows rows, const float *cvec, const float *M1_in,
+                              Retain ret, float *Sres, const float *g_next, float eps, int dtype,
+                              void *Xn, int ldx, hipStream_t st);
+
+// ---- attention ----
+struct AttnArgs {
+  const float *Q;  // [2Bp][n_q*d_h]
+  KVRef kv;
+  const int *pos_arr;  // length of sequence b = pos_arr[b] + 1
+  Rows rows;
+  int n_q;
+  int pages_per_split;
+  int max_splits;
+  float *opart;  // [B][n_kv][max_splits][16][d_h]
+  float *ostat;  // [B][n_kv][max_splits][16][2]
+  int dtype;
+};
+hipError_t launch_attn_decode(const AttnArgs &a, hipStream_t st);
+hipError_t launch_attn_combine(const AttnArgs &a, void *O, int ldo, hipStream_t st);
+
+// Causal attention of prompt positions 0..T-1 of one sequence (rows = positions).
+hipError_t launch_attn_prefill(const float *Q, int ldq, int T, KVRef kv, int seq, int n_q,
+                               int dtype, void *O, int ldo, hipStream_t st);
+
+// ---- cache fill ----
+hipError_t launch_kv_fill(KVRef kv, int seq, int start, int count, const void *ksrc,
+                          const void *vsrc, int dtype, hipStream_t st);
+
+// ---- mixture readout (Sec. 4.2) ----
+struct MixArgs {
+  const float *logits;  // [2Bp][V]
+  int V;
+  Rows rows;            // np = 2 with the branch on, 1 (primary) otherwise
+  int chunk;            // vocabulary entries per chunk
+  float *stats;         // [2Bp][nchunks][3]
+  float *cand;          // [B][nchunks][2] (value, index as float bits)
+  float *alpha;         // [B] or NULL
+  int *next;            // [B] or NULL
+};
+hipError_t launch_mixture(const MixArgs &m, hipStream_t st);
+
+}  // namespace dbt

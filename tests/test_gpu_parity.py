@@ -1,0 +1,244 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Bars: fp32 workloads max relative error 1e-5, bf16 workloads 2e-2 (per row:
+max |gpu - oracle| / max |oracle|), fp32 accumulation; cache indexing and
+page tables bit-exact; greedy tokens equal except at certified near-ties.
+"""
+import numpy as np
+import pytest
+
+import synth
+from oracle import Oracle
+from tests.gpu_util import fill_cache, make_session, near_tie_ok, row_err
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+F32_TOL = 1e-5
+BF16_TOL = 2e-2
+
+
+def _np(t):
+    return t.detach().cpu().numpy()
+
+
+def _check_readout(t, outs, tol, tag, branch=True):
+    z1 = np.stack([o["z1"] for o in outs])
+    assert row_err(_np(t["logits1"]), z1).max() <= tol, (tag, row_err(_np(t["logits1"]), z1))
+    if branch:
+        z2 = np.stack([o["z2"] for o in outs])
+        assert row_err(_np(t["logits2"]), z2).max() <= tol, (tag, row_err(_np(t["logits2"]), z2))
+    alpha = np.array([o["alpha"] for o in outs])
+    np.testing.assert_allclose(_np(t["alpha"]), alpha, rtol=max(tol, 1e-6), atol=1e-7, err_msg=tag)
+    for i, o in enumerate(outs):
+        tok = int(_np(t["next_token"])[i])
+        if tok != o["next"]:
+            assert near_tie_ok(o["m"], tok, 10 * tol * np.max(o["m"])), (tag, i, tok, o["next"])
+
+
+# ----------------------------------------------------------------------------
+# tiny fp32 model: prompt of 128, boundary, 16 continuation steps
+# ----------------------------------------------------------------------------
+
+def test_tiny_f32_prefill_boundary_and_16_steps():
+    w = synth.workload("tiny_f32")
+    shape = w["shape"]
+    W = synth.make_weights(shape, seed=0)
+    prompt = synth.make_tokens(1, 0, (w["prompt_len"],), shape.vocab)
+    orc = Oracle(shape, W.values)
+    ob = orc.prefill([prompt], run_boundary=True)[0]
+    sess = make_session(shape, W, max_batch=1, max_pos=w["prompt_len"] + w["steps"] + 1,
+                        max_prompt=w["prompt_len"])
+    t = sess.prefill([prompt], run_boundary=True)
+    _check_readout(t, [ob], F32_TOL, "boundary")
+    assert int(_np(t["next_token"])[0]) == ob["next"]
+    assert row_err(_np(t["h1_out"]), ob["h1"][None]).max() <= F32_TOL
+    assert row_err(_np(t["h2_out"]), ob["h2"][None]).max() <= F32_TOL
+    tok = ob["next"]
+    for step in range(w["steps"]):
+        o = orc.decode_step(tokens=[tok])[0]
+        t = sess.decode(tokens=[tok])
+        _check_readout(t, [o], F32_TOL, f"step {step}")
+        assert int(_np(t["next_token"])[0]) == o["next"], step
+        tok = o["next"]
+    assert sess.torch is torch
+
+
+# ----------------------------------------------------------------------------
+# small bf16 model with embeddings: ragged prompts, several pages/splits
+# ----------------------------------------------------------------------------
+
+def _small_bf16(**kw):
+    base = dict(n_layers=2, d_model=512, n_q_heads=8, n_kv_heads=2, head_dim=128, d_ff=1024,
+                vocab=1024, dtype="bf16", has_embeddings=True, std=0.05, coupling_std=0.5)
+    base.update(kw)
+    return synth.ModelShape(**base)
+
+
+def test_small_bf16_prefill_boundary_steps():
+    shape = _small_bf16()
+    W = synth.make_weights(shape, seed=0)
+    lens = [37, 100, 529, 1, 16]
+    prompts = [synth.make_tokens(1, 10 + i, (L,), shape.vocab) for i, L in enumerate(lens)]
+    orc = Oracle(shape, W.values)
+    obs = orc.prefill(prompts, run_boundary=True)
+    sess = make_session(shape, W, max_batch=5, max_pos=600, max_prompt=529)
+    t = sess.prefill(prompts, run_boundary=True)
+    _check_readout(t, obs, BF16_TOL, "boundary")
+    # page tables: bit-exact with the oracle allocator
+    for b in range(5):
+        assert sess_pages(sess, b) == orc.alloc.table[b]
+    toks = [o["next"] for o in obs]
+    for step in range(3):
+        outs = orc.decode_step(tokens=toks)
+        t = sess.decode(tokens=toks)
+        _check_readout(t, outs, BF16_TOL, f"step {step}")
+        h1 = np.stack([o["h1"] for o in outs])
+        h2 = np.stack([o["h2"] for o in outs])
+        assert row_err(_np(t["h1_out"]), h1).max() <= BF16_TOL
+        assert row_err(_np(t["h2_out"]), h2).max() <= BF16_TOL
+        toks = [o["next"] for o in outs]
+    for b in range(5):
+        assert sess_pages(sess, b) == orc.alloc.table[b]
+    dev_tab = _np(sess.page_table)
+    for b in range(5):
+        tab = orc.alloc.table[b]
+        np.testing.assert_array_equal(dev_tab[b, :len(tab)], tab)
+
+
+def sess_pages(sess, b):
+    from paper_2608_12385_amd import binding
+    return binding.dbt_kv_pages(sess.kv, b)
+
+
+# ----------------------------------------------------------------------------
+# layer-only bf16 model with hidden-state inputs and a ragged cache
+# ----------------------------------------------------------------------------
+
+def _layer_case(lengths, steps=2, vocab=512, seed_h=2):
+    shape = _small_bf16(n_layers=1, vocab=vocab, has_embeddings=False, coupling_std=0.5)
+    W = synth.make_weights(shape, seed=0)
+    B = len(lengths)
+    orc = Oracle(shape, W.values)
+    sess = make_session(shape, W, max_batch=B, max_pos=max(lengths) + steps + 1)
+    sess.k_pages.zero_()
+    sess.v_pages.zero_()
+    fill_cache(sess, orc, shape, lengths)
+    return shape, W, orc, sess
+
+
+@pytest.mark.parametrize("lengths", [[1, 15, 16, 17, 600], [511, 512, 513]])
+def test_layer_bf16_ragged_cache(lengths):
+    shape, W, orc, sess = _layer_case(lengths)
+    B = len(lengths)
+    for step in range(2):
+        h = synth.make_hidden(shape, B, step=step, seed=2)
+        outs = orc.decode_step(h1=h[0], h2=h[1])
+        t = sess.decode(h1=h[0], h2=h[1])
+        _check_readout(t, outs, BF16_TOL, f"step {step}")
+        assert row_err(_np(t["h1_out"]), np.stack([o["h1"] for o in outs])).max() <= BF16_TOL
+        assert row_err(_np(t["h2_out"]), np.stack([o["h2"] for o in outs])).max() <= BF16_TOL
+
+
+def test_primary_bitwise_branch_on_off_and_grouped_equals_ungrouped():
+    lengths = [3, 40, 530, 16]
+    B = len(lengths)
+    res = {}
+    for mode in ("on", "off", "ungrouped"):
+        shape, W, orc, sess = _layer_case(lengths)
+        h = synth.make_hidden(shape, B, step=0, seed=2)
+        if mode == "ungrouped":
+            t = sess.decode(h1=h[0], h2=h[1], grouped=False)
+        else:
+            t = sess.decode(h1=h[0], h2=h[1], branch_on=(mode == "on"))
+        res[mode] = {k: _np(v).copy() for k, v in t.items()}
+        res[mode]["k"] = _np(sess.k_pages).copy()
+        res[mode]["v"] = _np(sess.v_pages).copy()
+        sess.close()
+    on, off, ug = res["on"], res["off"], res["ungrouped"]
+    np.testing.assert_array_equal(on["h1_out"], off["h1_out"])
+    np.testing.assert_array_equal(on["logits1"], off["logits1"])
+    np.testing.assert_array_equal(on["k"], off["k"])
+    np.testing.assert_array_equal(on["v"], off["v"])
+    assert np.all(off["alpha"] == 1.0)
+    np.testing.assert_array_equal(off["next_token"], np.argmax(off["logits1"], axis=1))
+    for k in ("h1_out", "h2_out", "logits1", "logits2", "alpha", "next_token", "k", "v"):
+        np.testing.assert_array_equal(on[k], ug[k], err_msg=k)
+
+
+def test_cache_append_exactly_one_slot_per_layer_and_no_branch_entries():
+    """Poison the pages, fill B sequences, run one grouped step: the only
+    changed cache bytes are the B appended key/value slots per layer."""
+    lengths = [5, 16, 33]
+    shape = _small_bf16(n_layers=2, vocab=0, has_embeddings=False)
+    W = synth.make_weights(shape, seed=0)
+    B = len(lengths)
+    sess = make_session(shape, W, max_batch=B, max_pos=64)
+    sess.k_pages.fill_(0x7F)   # bf16 pattern 0x7F7F: a large finite value
+    sess.v_pages.fill_(0x7F)
+    orc = Oracle(shape, W.values)
+    fill_cache(sess, orc, shape, lengths)
+    k0, v0 = _np(sess.k_pages).copy(), _np(sess.v_pages).copy()
+    h = synth.make_hidden(shape, B)
+    sess.decode(h1=h[0], h2=h[1])
+    orc.decode_step(h1=h[0], h2=h[1])
+    k1, v1 = _np(sess.k_pages), _np(sess.v_pages)
+    changed_k = np.flatnonzero((k0 != k1).reshape(-1, 2).any(axis=1))
+    changed_v = np.flatnonzero((v0 != v1).reshape(-1, 2).any(axis=1))
+    # expected element offsets of the appended slots (page layout of dbt.h)
+    exp_k, exp_v = set(), set()
+    for l in range(shape.n_layers):
+        for b, L in enumerate(lengths):
+            page = orc.alloc.table[b][L // 16]
+            slot = L % 16
+            for g in range(shape.n_kv_heads):
+                base = ((l * sess.num_pages + page) * shape.n_kv_heads + g)
+                for dh in range(shape.head_dim):
+                    exp_k.add((base * 16 + slot) * shape.head_dim + dh)
+                    exp_v.add((base * shape.head_dim + dh) * 16 + slot)
+    assert set(changed_k.tolist()) == exp_k
+    assert set(changed_v.tolist()) == exp_v
+    # appended values equal the oracle's rounded keys/values
+    kk = k1.view(np.uint16)
+    for l in range(shape.n_layers):
+        for b, L in enumerate(lengths):
+            page = orc.alloc.table[b][L // 16]
+            for g in range(shape.n_kv_heads):
+                base = ((l * sess.num_pages + page) * shape.n_kv_heads + g)
+                got = synth.bf16_values(kk[(base * 16 + L % 16) * shape.head_dim:][:shape.head_dim])
+                ref = orc.K[l][b][L, g]
+                assert np.max(np.abs(got - ref)) <= BF16_TOL * np.max(np.abs(ref))
+
+
+# ----------------------------------------------------------------------------
+# one 8B-shape layer + LM head, batch 32, cache 4096: sampled rows at full size
+# ----------------------------------------------------------------------------
+
+@pytest.mark.slow
+def test_layer8b_full_size_sampled():
+    w = synth.workload("layer8b_bf16")
+    shape = w["shape"]
+    B, L = w["batch"], w["cache_len"]
+    W = synth.make_weights(shape, seed=0)
+    sess = make_session(shape, W, max_batch=B, max_pos=L + 16)
+    fill_cache(sess, None, shape, [L] * B)
+    h = synth.make_hidden(shape, B, step=0, seed=2)
+    t = sess.decode(h1=h[0], h2=h[1])
+    sample = [0, 17, 31]
+    orc = Oracle(shape, W.values)
+    for b in sample:
+        (kv_, _), (vv_, _) = synth.make_kv(shape, 0, b, L, seed=3)
+        orc.kv_fill(b, L, [kv_], [vv_])
+    outs = []
+    for b in sample:
+        outs.append(orc.step_one(b, h1=h[0, b], h2=h[1, b], readout=False))
+    orc._readout(outs)
+    sub = {k: v[sample] for k, v in t.items()}
+    _check_readout(sub, outs, BF16_TOL, "layer8b")
+    assert row_err(_np(sub["h1_out"]), np.stack([o["h1"] for o in outs])).max() <= BF16_TOL
+    assert row_err(_np(sub["h2_out"]), np.stack([o["h2"] for o in outs])).max() <= BF16_TOL
+    # properties at full size for every row: alpha in [0.5, 1]; tokens valid
+    a = _np(t["alpha"])
+    assert np.all((a >= 0.5) & (a <= 1.0))
+    nt = _np(t["next_token"])
+    assert np.all((nt >= 0) & (nt < shape.vocab))
