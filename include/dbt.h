@@ -220,6 +220,26 @@ dbt_status dbt_decode_step(dbt_model *m, dbt_kv *kv, const dbt_step_in *in, int3
 dbt_status dbt_decode_step_ungrouped(dbt_model *m, dbt_kv *kv, const dbt_step_in *in,
                                      dbt_step_out *out, dbt_stream stream);
 
+/* ---- stage timing -------------------------------------------------------
+ * While enabled for a stage, every later device call records a HIP event pair
+ * on its stream around the kernel(s) of that stage, once per launch.
+ * dbt_stage_time() waits for the recorded events, returns the summed elapsed
+ * milliseconds, stores the number of launches in *h_launches, and clears the
+ * record.  Events are created by the library on first use and destroyed by
+ * dbt_destroy.  Stages: */
+enum {
+  DBT_STAGE_QKV = 0,    /* stacked Q/K/V projection kernel */
+  DBT_STAGE_ATTN = 1,   /* grouped decode-attention kernel (without the split merge) */
+  DBT_STAGE_WO = 2,     /* attention output projection kernel */
+  DBT_STAGE_GATEUP = 3, /* gate/up projection kernel */
+  DBT_STAGE_DOWN = 4,   /* down projection kernel */
+  DBT_STAGE_LMHEAD = 5, /* output-matrix projection kernel */
+  DBT_STAGE_MIX = 6,    /* mixture readout kernels */
+  DBT_STAGE_COUNT = 7
+};
+dbt_status dbt_stage_timing(dbt_model *m, int32_t stage, int32_t enable);
+double dbt_stage_time(dbt_model *m, int32_t stage, int32_t *h_launches);
+
 #ifdef __cplusplus
 }
 #endif

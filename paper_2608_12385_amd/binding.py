@@ -75,7 +75,11 @@ _SIGS = {
     "dbt_boundary": (I32, [P, P, I32, ctypes.POINTER(dbt_step_out), P]),
     "dbt_decode_step": (I32, [P, P, ctypes.POINTER(dbt_step_in), I32, ctypes.POINTER(dbt_step_out), P]),
     "dbt_decode_step_ungrouped": (I32, [P, P, ctypes.POINTER(dbt_step_in), ctypes.POINTER(dbt_step_out), P]),
+    "dbt_stage_timing": (I32, [P, I32, I32]),
+    "dbt_stage_time": (ctypes.c_double, [P, I32, ctypes.POINTER(I32)]),
 }
+
+STAGES = dict(qkv=0, attn=1, wo=2, gateup=3, down=4, lmhead=5, mix=6)
 
 
 def lib():
@@ -179,6 +183,18 @@ def dbt_decode_step(m, kv, step_in, branch_on, out, stream):
 
 def dbt_decode_step_ungrouped(m, kv, step_in, out, stream):
     _check(lib().dbt_decode_step_ungrouped(m, kv, ctypes.byref(step_in), ctypes.byref(out), P(stream)))
+
+
+def dbt_stage_timing(m, stage, enable):
+    _check(lib().dbt_stage_timing(m, stage, int(enable)))
+
+
+def dbt_stage_time(m, stage):
+    n = I32(0)
+    ms = lib().dbt_stage_time(m, stage, ctypes.byref(n))
+    if ms < 0:
+        raise DbtError(6, "stage timing failed")
+    return ms, n.value
 
 
 # ----------------------------------------------------------------------------

@@ -129,7 +129,21 @@ Layout make_layout(const dbt_config *c) {
 
 }  // namespace
 
+struct StageTimer {
+  bool on = false;
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> ev;
+  size_t used = 0;
+};
+
 struct dbt_model {
+  StageTimer timers[DBT_STAGE_COUNT];
+  ~dbt_model() {
+    for (auto &t : timers)
+      for (auto &e : t.ev) {
+        (void)hipEventDestroy(e.first);
+        (void)hipEventDestroy(e.second);
+      }
+  }
   dbt_config cfg;
   dbt_weights w;
   std::vector<dbt_layer_weights> layers;
@@ -165,6 +179,31 @@ struct dbt_kv {
 namespace {
 
 size_t esize(const dbt_config &c) { return c.dtype == DBT_BF16 ? 2 : 4; }
+
+// Records an event pair around the launches made during its lifetime when
+// timing is enabled for the stage (a measurement aid; failures are ignored).
+class Timed {
+ public:
+  Timed(dbt_model *m, int stage, hipStream_t st) : st_(st) {
+    StageTimer &t = m->timers[stage];
+    if (!t.on) return;
+    if (t.used == t.ev.size()) {
+      hipEvent_t a, b;
+      if (hipEventCreate(&a) != hipSuccess) return;
+      if (hipEventCreate(&b) != hipSuccess) { (void)hipEventDestroy(a); return; }
+      t.ev.emplace_back(a, b);
+    }
+    pair_ = &t.ev[t.used++];
+    (void)hipEventRecord(pair_->first, st_);
+  }
+  ~Timed() {
+    if (pair_) (void)hipEventRecord(pair_->second, st_);
+  }
+
+ private:
+  hipStream_t st_;
+  std::pair<hipEvent_t, hipEvent_t> *pair_ = nullptr;
+};
 
 // K/V pages of one layer.
 KVRef kv_layer(const dbt_kv *kv, int l) {
@@ -255,8 +294,11 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
     nq = L.nqkv;
   }
   long long stride = (long long)c.rows_layout * nq;
-  HIPCHK(launch_gemm(qkv, nq, d, cf.dtype, Xn + (size_t)xrow0 * d * es, d, M, P + (size_t)xrow0 * nq, nq,
-                     stride, S_qkv, st));
+  {
+    Timed tm(m, DBT_STAGE_QKV, st);
+    HIPCHK(launch_gemm(qkv, nq, d, cf.dtype, Xn + (size_t)xrow0 * d * es, d, M, P + (size_t)xrow0 * nq, nq,
+                       stride, S_qkv, st));
+  }
   QKVFinish qf{};
   qf.part = P;
   qf.split_stride = stride;
@@ -293,30 +335,42 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
     aa.opart = m->at<float>(L.apart);
     aa.ostat = m->at<float>(L.astat);
     aa.dtype = cf.dtype;
-    HIPCHK(launch_attn_decode(aa, st));
+    {
+      Timed tm(m, DBT_STAGE_ATTN, st);
+      HIPCHK(launch_attn_decode(aa, st));
+    }
     HIPCHK(launch_attn_combine(aa, O, dq, st));
   }
 
   // 3. output projection + residual + MLP norm
   WSegs wo{{W.wo, nullptr, nullptr}, {d, 0, 0}};
   stride = (long long)c.rows_layout * d;
-  HIPCHK(launch_gemm(wo, d, dq, cf.dtype, O + (size_t)xrow0 * dq * es, dq, M, P + (size_t)xrow0 * d, d,
-                     stride, S_o, st));
+  {
+    Timed tm(m, DBT_STAGE_WO, st);
+    HIPCHK(launch_gemm(wo, d, dq, cf.dtype, O + (size_t)xrow0 * dq * es, dq, M, P + (size_t)xrow0 * d, d,
+                       stride, S_o, st));
+  }
   HIPCHK(launch_resid_norm(P, stride, S_o, d, S, W.mlp_norm, cf.rms_eps, d, cf.dtype, c.rows, Xn, d, st));
 
   // 4. gate/up + SwiGLU + b coupling
   WSegs gu{{W.w_gate, W.w_up, nullptr}, {f, f, 0}};
   stride = (long long)c.rows_layout * 2 * f;
-  HIPCHK(launch_gemm(gu, 2 * f, d, cf.dtype, Xn + (size_t)xrow0 * d * es, d, M, P + (size_t)xrow0 * 2 * f,
-                     2 * f, stride, S_gu, st));
+  {
+    Timed tm(m, DBT_STAGE_GATEUP, st);
+    HIPCHK(launch_gemm(gu, 2 * f, d, cf.dtype, Xn + (size_t)xrow0 * d * es, d, M, P + (size_t)xrow0 * 2 * f,
+                       2 * f, stride, S_gu, st));
+  }
   HIPCHK(launch_swiglu_finish(P, stride, S_gu, 2 * f, f, c.mode, c.rows, W.b, ret_h,
                               Retain{c.retain ? ret_h : nullptr, c.ret_src, c.ret_dst}, cf.dtype, Xh, f, st));
 
   // 5. down projection + c coupling + residual + next norm
   WSegs wd{{W.w_down, nullptr, nullptr}, {d, 0, 0}};
   stride = (long long)c.rows_layout * d;
-  HIPCHK(launch_gemm(wd, d, f, cf.dtype, Xh + (size_t)xrow0 * f * es, f, M, P + (size_t)xrow0 * d, d, stride,
-                     S_d, st));
+  {
+    Timed tm(m, DBT_STAGE_DOWN, st);
+    HIPCHK(launch_gemm(wd, d, f, cf.dtype, Xh + (size_t)xrow0 * f * es, f, M, P + (size_t)xrow0 * d, d, stride,
+                       S_d, st));
+  }
   const float *g_next = nullptr;
   if (l + 1 < cf.n_layers) g_next = m->layers[l + 1].attn_norm;
   else if (cf.vocab > 0 && c.last_norm) g_next = m->w.final_norm;
@@ -348,6 +402,7 @@ dbt_status lm_head(dbt_model *m, Rows rows, hipStream_t st) {
   const Layout &L = m->L;
   const int xrow0 = rows.p0 * rows.Bp;
   WSegs lm{{m->w.lm_head, nullptr, nullptr}, {cf.vocab, 0, 0}};
+  Timed tm(m, DBT_STAGE_LMHEAD, st);
   HIPCHK(launch_gemm(lm, cf.vocab, cf.d_model, cf.dtype, m->ws + L.Xn + (size_t)xrow0 * cf.d_model * esize(cf),
                      cf.d_model, rows.np * rows.Bp, m->at<float>(L.logits) + (size_t)xrow0 * cf.vocab, cf.vocab,
                      0, 1, st));
@@ -367,7 +422,10 @@ dbt_status readout(dbt_model *m, int B, int Bp, bool branch, dbt_step_out *out, 
   mx.cand = m->at<float>(L.mcand);
   mx.alpha = out ? out->alpha : nullptr;
   mx.next = out ? out->next_token : nullptr;
-  if (mx.alpha || mx.next) HIPCHK(launch_mixture(mx, st));
+  if (mx.alpha || mx.next) {
+    Timed tm(m, DBT_STAGE_MIX, st);
+    HIPCHK(launch_mixture(mx, st));
+  }
   if (out && out->logits1)
     HIPCHK(hipMemcpyAsync(out->logits1, m->at<float>(L.logits), (size_t)B * cf.vocab * 4, hipMemcpyDeviceToDevice, st));
   if (out && out->logits2 && branch)
@@ -765,6 +823,29 @@ dbt_status dbt_boundary(dbt_model *m, dbt_kv *kv, int32_t batch, dbt_step_out *o
     if ((s = copy_rows(out->h2_out, m->at<float>(L.S) + (size_t)Bp * cf.d_model, B, cf.d_model, st))) return s;
   }
   return DBT_OK;
+}
+
+dbt_status dbt_stage_timing(dbt_model *m, int32_t stage, int32_t enable) {
+  if (!m) return fail(DBT_ERR_ARG, "model is NULL");
+  if (stage < 0 || stage >= DBT_STAGE_COUNT) return fail(DBT_ERR_ARG, "stage %d out of range", stage);
+  m->timers[stage].on = enable != 0;
+  m->timers[stage].used = 0;
+  return DBT_OK;
+}
+
+double dbt_stage_time(dbt_model *m, int32_t stage, int32_t *h_launches) {
+  if (!m || stage < 0 || stage >= DBT_STAGE_COUNT) return -1.0;
+  StageTimer &t = m->timers[stage];
+  double total = 0.0;
+  for (size_t i = 0; i < t.used; ++i) {
+    float ms = 0.f;
+    if (hipEventSynchronize(t.ev[i].second) != hipSuccess) return -1.0;
+    if (hipEventElapsedTime(&ms, t.ev[i].first, t.ev[i].second) != hipSuccess) return -1.0;
+    total += ms;
+  }
+  if (h_launches) *h_launches = (int32_t)t.used;
+  t.used = 0;
+  return total;
 }
 
 }  // extern "C"
