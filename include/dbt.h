@@ -18,7 +18,7 @@
  *
  * Conventions
  *   - Every pointer argument is DEVICE memory unless its name starts with h_
- *     (host memory).  The caller owns all device memory: weights, KV pages,
+ *     (host memory).  Device pointers must be 16-byte aligned.  The caller owns all device memory: weights, KV pages,
  *     page table, workspace, inputs and outputs.  The library keeps borrowed
  *     pointers, which must stay valid until the handle is destroyed.  The
  *     library itself never allocates device memory.

@@ -250,30 +250,40 @@ __global__ __launch_bounds__(256) void k_attn_decode_f32(AttnArgs a) {
 
 // Merge the splits of one (sequence, KV head) in split order and write the
 // normalised head outputs to O (row path*Bp + b, column head*d_h + dh).
+// One thread per (query row, 4 consecutive dims).
 template <typename T>
 __global__ void k_attn_combine(AttnArgs a, T *O, int ldo) {
   const int g = blockIdx.x, b = blockIdx.y;
   const int len = a.pos_arr[b] + 1;
   const int npages = (len + 15) >> 4;
   const int nsplit = (npages + a.pages_per_split - 1) / a.pages_per_split;
-  const int n_kv = a.kv.n_kv, DH = a.kv.d_h;
+  const int n_kv = a.kv.n_kv, DH = a.kv.d_h, Q4 = DH / 4;
   const int G = a.n_q / n_kv;
   const int nrows = a.rows.np * G;
+  const int e = threadIdx.x;
+  if (e >= nrows * Q4) return;
+  const int qr = e / Q4, d4 = e % Q4;
   const size_t base = ((size_t)b * n_kv + g) * a.max_splits;
-  for (int e = threadIdx.x; e < nrows * DH; e += blockDim.x) {
-    const int qr = e / DH, dh = e % DH;
-    float mx = -INFINITY;
-    for (int s = 0; s < nsplit; ++s) mx = fmaxf(mx, a.ostat[((base + s) * 16 + qr) * 2]);
-    float o = 0.f, l = 0.f;
-    for (int s = 0; s < nsplit; ++s) {
-      const size_t ix = (base + s) * 16 + qr;
-      const float f = exp2f(a.ostat[ix * 2] - mx);
-      o += a.opart[ix * DH + dh] * f;
-      l += a.ostat[ix * 2 + 1] * f;
-    }
-    const int path = a.rows.p0 + qr / G, head = g * G + qr % G;
-    st<T>(O, (size_t)(path * a.rows.Bp + b) * ldo + head * DH + dh, o / l);
+  float mx = -INFINITY;
+  for (int s = 0; s < nsplit; ++s) mx = fmaxf(mx, a.ostat[((base + s) * 16 + qr) * 2]);
+  float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+  float l = 0.f;
+  for (int s = 0; s < nsplit; ++s) {
+    const size_t ix = (base + s) * 16 + qr;
+    const float f = exp2f(a.ostat[ix * 2] - mx);
+    const float4 v = ((const float4 *)(a.opart + ix * DH))[d4];
+    o.x += v.x * f;
+    o.y += v.y * f;
+    o.z += v.z * f;
+    o.w += v.w * f;
+    l += a.ostat[ix * 2 + 1] * f;
   }
+  const int path = a.rows.p0 + qr / G, head = g * G + qr % G;
+  const size_t out = (size_t)(path * a.rows.Bp + b) * ldo + head * DH + d4 * 4;
+  st<T>(O, out + 0, o.x / l);
+  st<T>(O, out + 1, o.y / l);
+  st<T>(O, out + 2, o.z / l);
+  st<T>(O, out + 3, o.w / l);
 }
 
 // Causal attention over the prompt of one sequence: workgroup per
@@ -363,10 +373,12 @@ hipError_t launch_attn_decode(const AttnArgs &a, hipStream_t st) {
 
 hipError_t launch_attn_combine(const AttnArgs &a, void *O, int ldo, hipStream_t st) {
   dim3 grid(a.kv.n_kv, a.rows.B);
+  const int G = a.n_q / a.kv.n_kv;
+  const int threads = (a.rows.np * G * (a.kv.d_h / 4) + 63) / 64 * 64;
   if (a.dtype == 1)
-    hipLaunchKernelGGL(k_attn_combine<uint16_t>, grid, dim3(256), 0, st, a, (uint16_t *)O, ldo);
+    hipLaunchKernelGGL(k_attn_combine<uint16_t>, grid, dim3(threads), 0, st, a, (uint16_t *)O, ldo);
   else
-    hipLaunchKernelGGL(k_attn_combine<float>, grid, dim3(256), 0, st, a, (float *)O, ldo);
+    hipLaunchKernelGGL(k_attn_combine<float>, grid, dim3(threads), 0, st, a, (float *)O, ldo);
   return hipGetLastError();
 }
 

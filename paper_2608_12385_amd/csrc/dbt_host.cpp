@@ -10,6 +10,7 @@
 #include <cstdio>
 #include <cstring>
 #include <functional>
+#include <numeric>
 #include <new>
 #include <queue>
 #include <string>
@@ -50,7 +51,7 @@ int round16(int x) { return (x + 15) / 16 * 16; }
 // Offsets (bytes) of every workspace buffer.
 struct Layout {
   int Bp_max = 0, R_max = 0, rows_max = 0, max_in = 0, nqkv = 0, f = 0;
-  int S_qkv = 1, S_o = 1, S_gu = 1, S_d = 1;
+  GemmConfig g_qkv{1, 1, 1}, g_o{1, 1, 1}, g_gu{1, 1, 1}, g_d{1, 1, 1}, g_lm{1, 1, 1};
   int max_splits = 0, nch = 0;
   size_t rope = 0, pos = 0, S = 0, Xn = 0, Xh = 0, Q = 0, O = 0, P = 0, apart = 0, astat = 0,
          logits = 0, mstats = 0, mcand = 0, ret_q = 0, ret_h = 0, ret_m = 0, btok = 0, slast = 0,
@@ -64,7 +65,8 @@ dbt_status check_config(const dbt_config *c) {
     return fail(DBT_ERR_ARG, "sizes must be positive");
   if (c->dtype != DBT_F32 && c->dtype != DBT_BF16) return fail(DBT_ERR_ARG, "dtype must be DBT_F32 or DBT_BF16");
   if (c->n_q_heads % c->n_kv_heads) return fail(DBT_ERR_SHAPE, "n_q_heads %% n_kv_heads != 0");
-  if (c->head_dim % 2) return fail(DBT_ERR_SHAPE, "head_dim must be even");
+  if (c->head_dim % 4) return fail(DBT_ERR_SHAPE, "head_dim must be a multiple of 4");
+  if (c->d_model % 4) return fail(DBT_ERR_SHAPE, "d_model must be a multiple of 4");
   if (c->max_prompt > c->max_pos) return fail(DBT_ERR_SHAPE, "max_prompt > max_pos");
   if (c->n_experts > 0) return fail(DBT_ERR_UNSUPPORTED, "MoE layers are not built in this library version");
   if (c->d_ff <= 0) return fail(DBT_ERR_ARG, "d_ff must be positive");
@@ -93,15 +95,16 @@ Layout make_layout(const dbt_config *c) {
   L.rows_max = std::max(L.R_max, c->max_prompt);
   L.max_in = std::max(std::max(d, dq), L.f);
   L.nqkv = dq + 2 * dkv;
-  L.S_qkv = gemm_splits(L.nqkv, d, c->dtype);
-  L.S_o = gemm_splits(d, dq, c->dtype);
-  L.S_gu = gemm_splits(2 * L.f, d, c->dtype);
-  L.S_d = gemm_splits(d, L.f, c->dtype);
+  L.g_qkv = gemm_config(L.nqkv, d, c->dtype, std::gcd(dq, dkv));
+  L.g_o = gemm_config(d, dq, c->dtype, d);
+  L.g_gu = gemm_config(2 * L.f, d, c->dtype, L.f);
+  L.g_d = gemm_config(d, L.f, c->dtype, d);
+  L.g_lm = gemm_config(std::max(c->vocab, 1), d, c->dtype, std::max(c->vocab, 1));
   const int maxpages = (c->max_pos + kPage - 1) / kPage;
   L.max_splits = (maxpages + kPagesPerSplit - 1) / kPagesPerSplit;
   L.nch = c->vocab > 0 ? (c->vocab + kMixChunk - 1) / kMixChunk : 0;
-  size_t part = std::max({(size_t)L.S_qkv * L.R_max * L.nqkv, (size_t)L.S_o * L.R_max * d,
-                          (size_t)L.S_gu * L.R_max * 2 * L.f, (size_t)L.S_d * L.R_max * d});
+  size_t part = std::max({(size_t)L.g_qkv.S * L.R_max * L.nqkv, (size_t)L.g_o.S * L.R_max * d,
+                          (size_t)L.g_gu.S * L.R_max * 2 * L.f, (size_t)L.g_d.S * L.R_max * d});
   part = std::max(part, (size_t)c->max_prompt * std::max({L.nqkv, d, 2 * L.f}));
   size_t o = 0;
   auto take = [&](size_t bytes) { size_t at = o; o += align256(bytes); return at; };
@@ -275,8 +278,10 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
   const int M = c.rows.np * c.rows.Bp;
   char *Xn = m->ws + L.Xn, *Xh = m->ws + L.Xh, *O = m->ws + L.O;
   float *P = m->at<float>(L.P), *S = m->at<float>(L.S), *Q = m->at<float>(L.Q);
-  const int S_qkv = c.prefill ? 1 : L.S_qkv, S_o = c.prefill ? 1 : L.S_o, S_gu = c.prefill ? 1 : L.S_gu,
-            S_d = c.prefill ? 1 : L.S_d;
+  // prompt-wide rows: no reduction split (plenty of row tiles)
+  auto cfg = [&](GemmConfig g) { if (c.prefill) g.S = 1; return g; };
+  const GemmConfig g_qkv = cfg(L.g_qkv), g_o = cfg(L.g_o), g_gu = cfg(L.g_gu), g_d = cfg(L.g_d);
+  const int S_qkv = g_qkv.S, S_o = g_o.S, S_gu = g_gu.S, S_d = g_d.S;
   KVRef kvl = kv_layer(kv, l);
   const size_t rq = (size_t)l * L.Bp_max;
   float *ret_q = m->at<float>(L.ret_q) + rq * dq;
@@ -297,7 +302,7 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
   {
     Timed tm(m, DBT_STAGE_QKV, st);
     HIPCHK(launch_gemm(qkv, nq, d, cf.dtype, Xn + (size_t)xrow0 * d * es, d, M, P + (size_t)xrow0 * nq, nq,
-                       stride, S_qkv, st));
+                       stride, g_qkv, st));
   }
   QKVFinish qf{};
   qf.part = P;
@@ -348,7 +353,7 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
   {
     Timed tm(m, DBT_STAGE_WO, st);
     HIPCHK(launch_gemm(wo, d, dq, cf.dtype, O + (size_t)xrow0 * dq * es, dq, M, P + (size_t)xrow0 * d, d,
-                       stride, S_o, st));
+                       stride, g_o, st));
   }
   HIPCHK(launch_resid_norm(P, stride, S_o, d, S, W.mlp_norm, cf.rms_eps, d, cf.dtype, c.rows, Xn, d, st));
 
@@ -358,7 +363,7 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
   {
     Timed tm(m, DBT_STAGE_GATEUP, st);
     HIPCHK(launch_gemm(gu, 2 * f, d, cf.dtype, Xn + (size_t)xrow0 * d * es, d, M, P + (size_t)xrow0 * 2 * f,
-                       2 * f, stride, S_gu, st));
+                       2 * f, stride, g_gu, st));
   }
   HIPCHK(launch_swiglu_finish(P, stride, S_gu, 2 * f, f, c.mode, c.rows, W.b, ret_h,
                               Retain{c.retain ? ret_h : nullptr, c.ret_src, c.ret_dst}, cf.dtype, Xh, f, st));
@@ -369,7 +374,7 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
   {
     Timed tm(m, DBT_STAGE_DOWN, st);
     HIPCHK(launch_gemm(wd, d, f, cf.dtype, Xh + (size_t)xrow0 * f * es, f, M, P + (size_t)xrow0 * d, d, stride,
-                       S_d, st));
+                       g_d, st));
   }
   const float *g_next = nullptr;
   if (l + 1 < cf.n_layers) g_next = m->layers[l + 1].attn_norm;
@@ -405,7 +410,7 @@ dbt_status lm_head(dbt_model *m, Rows rows, hipStream_t st) {
   Timed tm(m, DBT_STAGE_LMHEAD, st);
   HIPCHK(launch_gemm(lm, cf.vocab, cf.d_model, cf.dtype, m->ws + L.Xn + (size_t)xrow0 * cf.d_model * esize(cf),
                      cf.d_model, rows.np * rows.Bp, m->at<float>(L.logits) + (size_t)xrow0 * cf.vocab, cf.vocab,
-                     0, 1, st));
+                     0, L.g_lm, st));
   return DBT_OK;
 }
 

@@ -30,14 +30,43 @@ __global__ void k_step_begin(StepBegin sb, int *pos_arr, int *page_table, int mp
   if (t < sb.n_pt) page_table[(size_t)sb.pt_b[t] * mpps + sb.pt_slot[t]] = sb.pt_page[t];
 }
 
-// y = x / sqrt(mean(x^2) + eps) * g written to out (dtype T); x read from src.
+// Row kernels use one workgroup per row (or row pair) with float4 accesses;
+// d is a multiple of 4.  st4 writes four consecutive values in dtype T.
+template <typename T> __device__ __forceinline__ void st4(T *p, size_t i4, float4 v);
+template <> __device__ __forceinline__ void st4<float>(float *p, size_t i4, float4 v) { ((float4 *)p)[i4] = v; }
+template <> __device__ __forceinline__ void st4<uint16_t>(uint16_t *p, size_t i4, float4 v) {
+  uint2 u;
+  u.x = (uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16);
+  u.y = (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16);
+  ((uint2 *)p)[i4] = u;
+}
+template <typename T> __device__ __forceinline__ float4 ld4(const T *p, size_t i4);
+template <> __device__ __forceinline__ float4 ld4<float>(const float *p, size_t i4) { return ((const float4 *)p)[i4]; }
+template <> __device__ __forceinline__ float4 ld4<uint16_t>(const uint16_t *p, size_t i4) {
+  const uint2 u = ((const uint2 *)p)[i4];
+  return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u), __uint_as_float(u.y << 16),
+                     __uint_as_float(u.y & 0xffff0000u));
+}
+__device__ __forceinline__ float dot4(float4 a) { return a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w; }
+__device__ __forceinline__ float4 add4(float4 a, float4 b) { return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w); }
+__device__ __forceinline__ float4 mul4(float4 a, float s, float4 g) {
+  return make_float4(a.x * s * g.x, a.y * s * g.y, a.z * s * g.z, a.w * s * g.w);
+}
+__device__ __forceinline__ float4 psum4(const float *part, long long stride, int S, size_t idx4) {
+  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int k = 0; k < S; ++k) s = add4(s, ((const float4 *)(part + k * stride))[idx4]);
+  return s;
+}
+
+// out = x / sqrt(mean(x^2) + eps) * g (x read from global, fp32)
 template <typename T>
 __device__ void norm_row(const float *x, const float *g, float eps, int d, T *out, float *red) {
   float ss = 0.f;
-  for (int i = threadIdx.x; i < d; i += blockDim.x) ss += x[i] * x[i];
+  for (int i = threadIdx.x; i < d / 4; i += blockDim.x) ss += dot4(((const float4 *)x)[i]);
   ss = block_sum(ss, red);
   const float inv = 1.0f / sqrtf(ss / (float)d + eps);
-  for (int i = threadIdx.x; i < d; i += blockDim.x) st<T>(out, i, x[i] * inv * g[i]);
+  for (int i = threadIdx.x; i < d / 4; i += blockDim.x)
+    st4<T>(out, i, mul4(((const float4 *)x)[i], inv, ((const float4 *)g)[i]));
 }
 
 // Tokens outside [0, vocab) read as a zero embedding row (no out-of-bounds read).
@@ -52,14 +81,14 @@ __global__ void k_embed(const int *tokens, int vocab, const T *e1, const T *e2, 
   const T *e = (path == 0 ? e1 : e2) + (size_t)(valid ? tok : 0) * d;
   float *s = S + (size_t)row * d;
   float ss = 0.f;
-  for (int i = threadIdx.x; i < d; i += blockDim.x) {
-    const float v = valid ? ld<T>(e, i) : 0.f;
-    s[i] = v;
-    ss += v * v;
+  for (int i = threadIdx.x; i < d / 4; i += blockDim.x) {
+    const float4 v = valid ? ld4<T>(e, i) : make_float4(0.f, 0.f, 0.f, 0.f);
+    ((float4 *)s)[i] = v;
+    ss += dot4(v);
   }
   ss = block_sum(ss, red);
   const float inv = 1.0f / sqrtf(ss / (float)d + eps);
-  for (int i = threadIdx.x; i < d; i += blockDim.x) s[i] = s[i] * inv * g_emb[i];
+  for (int i = threadIdx.x; i < d / 4; i += blockDim.x) ((float4 *)s)[i] = mul4(((float4 *)s)[i], inv, ((const float4 *)g_emb)[i]);
   __syncthreads();
   norm_row<T>(s, g_next, eps, d, Xn + (size_t)row * ldx, red);
 }
@@ -72,7 +101,7 @@ __global__ void k_load_hidden(const float *h1, const float *h2, const float *g_n
   const int row = phys_row(rows, path, b);
   const float *h = (path == 0 ? h1 : h2) + (size_t)b * d;
   float *s = S + (size_t)row * d;
-  for (int i = threadIdx.x; i < d; i += blockDim.x) s[i] = h[i];
+  for (int i = threadIdx.x; i < d / 4; i += blockDim.x) ((float4 *)s)[i] = ((const float4 *)h)[i];
   __syncthreads();
   norm_row<T>(s, g_next, eps, d, Xn + (size_t)row * ldx, red);
 }
@@ -166,7 +195,8 @@ __global__ void k_resid_norm(const float *part, long long stride, int S, int ldp
   __shared__ float red[16];
   const int row = phys_row(rows, rows.p0 + blockIdx.y, blockIdx.x);
   float *s = Sres + (size_t)row * d;
-  for (int i = threadIdx.x; i < d; i += blockDim.x) s[i] += psum(part, stride, S, (size_t)row * ldp + i);
+  for (int i = threadIdx.x; i < d / 4; i += blockDim.x)
+    ((float4 *)s)[i] = add4(((float4 *)s)[i], psum4(part, stride, S, ((size_t)row * ldp) / 4 + i));
   __syncthreads();
   norm_row<T>(s, g, eps, d, Xn + (size_t)row * ldx, red);
 }
@@ -212,27 +242,32 @@ __global__ void k_down_finish(const float *part, long long stride, int S, int ld
   const int b = blockIdx.x;
   const bool prim = mode != MODE_BRANCH, br = mode != MODE_PRIMARY;
   const int r1 = phys_row(rows, 0, b), r2 = phys_row(rows, 1, b);
-  float *s1 = Sres + (size_t)r1 * d;
-  float *s2 = Sres + (size_t)r2 * d;
+  float4 *s1 = (float4 *)(Sres + (size_t)r1 * d);
+  float4 *s2 = (float4 *)(Sres + (size_t)r2 * d);
   const bool keep = ret.ptr && (ret.src_row < 0 || ret.src_row == b);
-  float *kept = keep ? ret.ptr + (size_t)(ret.src_row < 0 ? b : ret.dst_row) * d : nullptr;
-  for (int i = threadIdx.x; i < d; i += blockDim.x) {
-    float m1;
+  float4 *kept = keep ? (float4 *)(ret.ptr + (size_t)(ret.src_row < 0 ? b : ret.dst_row) * d) : nullptr;
+  for (int i = threadIdx.x; i < d / 4; i += blockDim.x) {
+    float4 m1;
     if (prim) {
-      m1 = psum(part, stride, S, (size_t)r1 * ldp + i);
-      s1[i] += m1;
+      m1 = psum4(part, stride, S, ((size_t)r1 * ldp) / 4 + i);
+      s1[i] = add4(s1[i], m1);
       if (keep) kept[i] = m1;
     } else {
-      m1 = M1_in[(size_t)b * d + i];
+      m1 = ((const float4 *)(M1_in + (size_t)b * d))[i];
     }
-    if (br) s2[i] += psum(part, stride, S, (size_t)r2 * ldp + i) + cvec[i] * m1;
+    if (br) {
+      const float4 m2 = psum4(part, stride, S, ((size_t)r2 * ldp) / 4 + i);
+      const float4 c = ((const float4 *)cvec)[i];
+      const float4 t = make_float4(m2.x + c.x * m1.x, m2.y + c.y * m1.y, m2.z + c.z * m1.z, m2.w + c.w * m1.w);
+      s2[i] = add4(s2[i], t);
+    }
   }
   if (!g_next) return;
   __syncthreads();
-  if (prim) norm_row<T>(s1, g_next, eps, d, Xn + (size_t)r1 * ldx, red);
+  if (prim) norm_row<T>((const float *)s1, g_next, eps, d, Xn + (size_t)r1 * ldx, red);
   if (br) {
     __syncthreads();
-    norm_row<T>(s2, g_next, eps, d, Xn + (size_t)r2 * ldx, red);
+    norm_row<T>((const float *)s2, g_next, eps, d, Xn + (size_t)r2 * ldx, red);
   }
 }
 
@@ -268,12 +303,27 @@ __global__ void k_mix_stats(MixArgs m) {
   const int nch = (m.V + m.chunk - 1) / m.chunk;
   const int lo = c * m.chunk, hi = min(m.V, lo + m.chunk);
   const float *z = m.logits + (size_t)row * m.V;
+  // each thread keeps its values in registers between the two passes
+  constexpr int PER = 16;
+  float v[PER];
   float mx = -INFINITY;
-  for (int v = lo + threadIdx.x; v < hi; v += blockDim.x) mx = fmaxf(mx, z[v]);
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int idx = lo + threadIdx.x + k * blockDim.x;
+    v[k] = idx < hi ? z[idx] : -INFINITY;
+    mx = fmaxf(mx, v[k]);
+  }
+  for (int idx = lo + threadIdx.x + PER * blockDim.x; idx < hi; idx += blockDim.x) mx = fmaxf(mx, z[idx]);
   mx = block_max(mx, red);
   float s1 = 0.f, s2 = 0.f;
-  for (int v = lo + threadIdx.x; v < hi; v += blockDim.x) {
-    const float e = expf(z[v] - mx);
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const float e = expf(v[k] - mx);
+    s1 += e;
+    s2 += e * e;
+  }
+  for (int idx = lo + threadIdx.x + PER * blockDim.x; idx < hi; idx += blockDim.x) {
+    const float e = expf(z[idx] - mx);
     s1 += e;
     s2 += e * e;
   }
@@ -366,15 +416,20 @@ hipError_t launch_step_begin(const StepBegin &sb, int *pos_arr, int *page_table,
   return hipGetLastError();
 }
 
+static int row_threads(int d) {
+  int t = (d / 4 + 63) / 64 * 64;
+  return t < 64 ? 64 : t > 1024 ? 1024 : t;
+}
+
 hipError_t launch_embed(const int *tokens, int vocab, const void *e1, const void *e2, const float *g_emb,
                         const float *g_next, float eps, int d, int dtype, Rows rows, float *S,
                         void *Xn, int ldx, hipStream_t st) {
   dim3 grid(rows.B, rows.np);
   if (dtype == 1)
-    hipLaunchKernelGGL(k_embed<uint16_t>, grid, dim3(256), 0, st, tokens, vocab, (const uint16_t *)e1,
+    hipLaunchKernelGGL(k_embed<uint16_t>, grid, dim3(row_threads(d)), 0, st, tokens, vocab, (const uint16_t *)e1,
                        (const uint16_t *)e2, g_emb, g_next, eps, d, rows, S, (uint16_t *)Xn, ldx);
   else
-    hipLaunchKernelGGL(k_embed<float>, grid, dim3(256), 0, st, tokens, vocab, (const float *)e1,
+    hipLaunchKernelGGL(k_embed<float>, grid, dim3(row_threads(d)), 0, st, tokens, vocab, (const float *)e1,
                        (const float *)e2, g_emb, g_next, eps, d, rows, S, (float *)Xn, ldx);
   return hipGetLastError();
 }
@@ -383,10 +438,10 @@ hipError_t launch_load_hidden(const float *h1, const float *h2, const float *g_n
                               int d, int dtype, Rows rows, float *S, void *Xn, int ldx, hipStream_t st) {
   dim3 grid(rows.B, rows.np);
   if (dtype == 1)
-    hipLaunchKernelGGL(k_load_hidden<uint16_t>, grid, dim3(256), 0, st, h1, h2, g_next, eps, d, rows, S,
+    hipLaunchKernelGGL(k_load_hidden<uint16_t>, grid, dim3(row_threads(d)), 0, st, h1, h2, g_next, eps, d, rows, S,
                        (uint16_t *)Xn, ldx);
   else
-    hipLaunchKernelGGL(k_load_hidden<float>, grid, dim3(256), 0, st, h1, h2, g_next, eps, d, rows, S,
+    hipLaunchKernelGGL(k_load_hidden<float>, grid, dim3(row_threads(d)), 0, st, h1, h2, g_next, eps, d, rows, S,
                        (float *)Xn, ldx);
   return hipGetLastError();
 }
@@ -395,9 +450,9 @@ hipError_t launch_rmsnorm_rows(const float *S, const float *g, float eps, int d,
                                void *Xn, int ldx, hipStream_t st) {
   dim3 grid(rows.B, rows.np);
   if (dtype == 1)
-    hipLaunchKernelGGL(k_rmsnorm_rows<uint16_t>, grid, dim3(256), 0, st, S, g, eps, d, rows, (uint16_t *)Xn, ldx);
+    hipLaunchKernelGGL(k_rmsnorm_rows<uint16_t>, grid, dim3(row_threads(d)), 0, st, S, g, eps, d, rows, (uint16_t *)Xn, ldx);
   else
-    hipLaunchKernelGGL(k_rmsnorm_rows<float>, grid, dim3(256), 0, st, S, g, eps, d, rows, (float *)Xn, ldx);
+    hipLaunchKernelGGL(k_rmsnorm_rows<float>, grid, dim3(row_threads(d)), 0, st, S, g, eps, d, rows, (float *)Xn, ldx);
   return hipGetLastError();
 }
 
@@ -417,10 +472,10 @@ hipError_t launch_resid_norm(const float *part, long long stride, int S, int ldp
                              hipStream_t st) {
   dim3 grid(rows.B, rows.np);
   if (dtype == 1)
-    hipLaunchKernelGGL(k_resid_norm<uint16_t>, grid, dim3(256), 0, st, part, stride, S, ldp, Sres, g, eps, d,
+    hipLaunchKernelGGL(k_resid_norm<uint16_t>, grid, dim3(row_threads(d)), 0, st, part, stride, S, ldp, Sres, g, eps, d,
                        rows, (uint16_t *)Xn, ldx);
   else
-    hipLaunchKernelGGL(k_resid_norm<float>, grid, dim3(256), 0, st, part, stride, S, ldp, Sres, g, eps, d,
+    hipLaunchKernelGGL(k_resid_norm<float>, grid, dim3(row_threads(d)), 0, st, part, stride, S, ldp, Sres, g, eps, d,
                        rows, (float *)Xn, ldx);
   return hipGetLastError();
 }
@@ -443,10 +498,10 @@ hipError_t launch_down_finish(const float *part, long long stride, int S, int ld
                               const float *g_next, float eps, int dtype, void *Xn, int ldx, hipStream_t st) {
   dim3 grid(rows.B);
   if (dtype == 1)
-    hipLaunchKernelGGL(k_down_finish<uint16_t>, grid, dim3(256), 0, st, part, stride, S, ldp, d, mode, rows,
+    hipLaunchKernelGGL(k_down_finish<uint16_t>, grid, dim3(row_threads(d)), 0, st, part, stride, S, ldp, d, mode, rows,
                        cvec, M1_in, ret, Sres, g_next, eps, (uint16_t *)Xn, ldx);
   else
-    hipLaunchKernelGGL(k_down_finish<float>, grid, dim3(256), 0, st, part, stride, S, ldp, d, mode, rows,
+    hipLaunchKernelGGL(k_down_finish<float>, grid, dim3(row_threads(d)), 0, st, part, stride, S, ldp, d, mode, rows,
                        cvec, M1_in, ret, Sres, g_next, eps, (float *)Xn, ldx);
   return hipGetLastError();
 }

@@ -18,101 +18,121 @@ namespace dbt {
 
 namespace {
 
-constexpr int kRowsPerWG = 64;   // weight rows per workgroup
-constexpr int kChunk = 128;      // reduction elements per wave iteration
+constexpr int kChunk = 128;  // reduction elements per pipeline stage
+constexpr int kLdsRow = kChunk + 8;  // padded LDS row of a staged activation chunk (elements)
 
-__device__ __forceinline__ const uint16_t *seg_base(const WSegs &s, int n0, int &nloc) {
-  nloc = n0;
-  if (nloc < s.rows[0]) return (const uint16_t *)s.w[0];
-  nloc -= s.rows[0];
-  if (nloc < s.rows[1]) return (const uint16_t *)s.w[1];
-  nloc -= s.rows[1];
-  return (const uint16_t *)s.w[2];
-}
-
-template <int MB>
-__global__ __launch_bounds__(256) void k_gemm_bf16(WSegs segs, int K, const uint16_t *__restrict__ X,
-                                                   int ldx, int M, float *__restrict__ Y, int ldy,
-                                                   long long y_split_stride, int k_per_split) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+// A workgroup owns 64*RB consecutive weight rows (all in one segment); wave w
+// owns rows w*16*RB .. +16*RB and runs the whole reduction range of its split.
+// The activation chunk [16*MB rows][128] is staged once per workgroup in LDS
+// (contiguous loads) and read by the four waves in MFMA operand layout.
+// Weight loads are issued PD chunks ahead into a register ring; the
+// activation chunks use an LDS ring of the same depth.
+template <int MB, int RB, int PD>
+__global__ __launch_bounds__(256) void k_gemm_bf16(WSegs segs, int K, const uint16_t *__restrict__ X, int ldx,
+                                                   int M, float *__restrict__ Y, int ldy, long long y_split_stride,
+                                                   int k_per_split) {
+  constexpr int XR = 16 * MB;
+  constexpr int PIECES = XR * (kChunk / 8);  // 16-byte pieces of one activation chunk
+  constexpr int PPT = (PIECES + 255) / 256;
+  __shared__ uint16_t xs[PD][XR * kLdsRow];
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int r = lane & 15, gq = lane >> 4;
-  const int n0 = blockIdx.x * kRowsPerWG;
   const int split = blockIdx.y;
-  const int m0 = blockIdx.z * (16 * MB);
-  int nloc;
-  const uint16_t *W = seg_base(segs, n0, nloc);
+  const int m0 = blockIdx.z * XR;
   const int kbeg = split * k_per_split;
-  const int nchunks = k_per_split / kChunk;
-
-  const uint16_t *wrow[4];
-#pragma unroll
-  for (int rb = 0; rb < 4; ++rb) wrow[rb] = W + (size_t)(nloc + rb * 16 + r) * K + kbeg + gq * 8;
-  const uint16_t *xrow[MB];
-  bool xval[MB];
-#pragma unroll
-  for (int cb = 0; cb < MB; ++cb) {
-    const int m = m0 + cb * 16 + r;
-    xval[cb] = m < M;
-    xrow[cb] = X + (size_t)(xval[cb] ? m : 0) * ldx + kbeg + gq * 8;
+  const int nch = k_per_split / kChunk;
+  // segment of this workgroup's rows (segment sizes are multiples of 64*RB)
+  int nloc = blockIdx.x * 64 * RB;
+  const uint16_t *Wseg = (const uint16_t *)segs.w[0];
+  if (nloc >= segs.rows[0]) {
+    nloc -= segs.rows[0];
+    Wseg = (const uint16_t *)segs.w[1];
+    if (nloc >= segs.rows[1]) {
+      nloc -= segs.rows[1];
+      Wseg = (const uint16_t *)segs.w[2];
+    }
   }
-
-  floatx4 acc[4][MB];
+  const int nw = nloc + wave * 16 * RB;             // first row of this wave within the segment
+  const int ny = blockIdx.x * 64 * RB + wave * 16 * RB;  // first output column of this wave
+  const uint16_t *wrow[RB];
 #pragma unroll
-  for (int rb = 0; rb < 4; ++rb)
+  for (int rb = 0; rb < RB; ++rb) wrow[rb] = Wseg + (size_t)(nw + rb * 16 + r) * K + kbeg + gq * 8;
+
+  floatx4 acc[RB][MB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
     for (int cb = 0; cb < MB; ++cb) acc[rb][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  for (int c = wave; c < nchunks; c += 4) {
-    const int koff = c * kChunk;
-    u32x4 a[4][4];
+  u32x4 a[PD][RB][4];
+  u32x4 stage[PPT];
+  auto wload = [&](int slot, int c) {
 #pragma unroll
-    for (int rb = 0; rb < 4; ++rb)
+    for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-      for (int s = 0; s < 4; ++s) a[rb][s] = *(const u32x4 *)(wrow[rb] + koff + s * 32);
-    u32x4 bx[MB][4];
+      for (int s = 0; s < 4; ++s) a[slot][rb][s] = *(const u32x4 *)(wrow[rb] + c * kChunk + s * 32);
+  };
+  auto xload = [&](int c) {
 #pragma unroll
-    for (int cb = 0; cb < MB; ++cb)
+    for (int j = 0; j < PPT; ++j) {
+      const int p = t + 256 * j;
+      const int row = p >> 4, col = (p & 15) * 8;
+      const bool ok = p < PIECES && m0 + row < M;
+      stage[j] = ok ? *(const u32x4 *)(X + (size_t)(m0 + row) * ldx + kbeg + c * kChunk + col)
+                    : u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+  auto xstore = [&](int slot) {
 #pragma unroll
-      for (int s = 0; s < 4; ++s)
-        bx[cb][s] = xval[cb] ? *(const u32x4 *)(xrow[cb] + koff + s * 32) : u32x4{0u, 0u, 0u, 0u};
-#pragma unroll
-    for (int s = 0; s < 4; ++s)
-#pragma unroll
-      for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-        for (int cb = 0; cb < MB; ++cb)
-          acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              __builtin_bit_cast(bf16x8, a[rb][s]), __builtin_bit_cast(bf16x8, bx[cb][s]),
-              acc[rb][cb], 0, 0, 0);
-  }
+    for (int j = 0; j < PPT; ++j) {
+      const int p = t + 256 * j;
+      if (p < PIECES) *(u32x4 *)(&xs[slot][(p >> 4) * kLdsRow + (p & 15) * 8]) = stage[j];
+    }
+  };
 
-  // Fixed-order sum of the four waves' partial results, 64 activation rows at a time.
-  __shared__ float red[4][64][kRowsPerWG + 1];
+#pragma unroll
+  for (int u = 0; u < PD; ++u)
+    if (u < nch) {
+      xload(u);
+      xstore(u);
+      wload(u, u);
+    }
+  __syncthreads();
+  for (int c0 = 0; c0 < nch; c0 += PD) {
+#pragma unroll
+    for (int u = 0; u < PD; ++u) {
+      const int c = c0 + u;
+      if (c < nch) {
+        const bool more = c + PD < nch;
+        if (more) xload(c + PD);
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+          u32x4 bx[MB];
+#pragma unroll
+          for (int cb = 0; cb < MB; ++cb) bx[cb] = *(const u32x4 *)(&xs[u][(cb * 16 + r) * kLdsRow + s * 32 + gq * 8]);
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+            for (int cb = 0; cb < MB; ++cb)
+              acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a[u][rb][s]),
+                                                                    __builtin_bit_cast(bf16x8, bx[cb]), acc[rb][cb], 0,
+                                                                    0, 0);
+        }
+        if (more) wload(u, c + PD);
+        __syncthreads();
+        if (more) xstore(u);
+      }
+    }
+  }
+  // lane holds D[n = rb*16 + 4*gq + i][m = cb*16 + r]: Y[m][n .. n+3]
   float *Ys = Y + (long long)split * y_split_stride;
 #pragma unroll
-  for (int half = 0; half < (MB + 3) / 4; ++half) {
-    __syncthreads();
+  for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-    for (int cbh = 0; cbh < 4; ++cbh) {
-      const int cb = half * 4 + cbh;
-      if (cb < MB) {
-#pragma unroll
-        for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) red[wave][cbh * 16 + r][rb * 16 + gq * 4 + i] = acc[rb][cb][i];
-      }
+    for (int cb = 0; cb < MB; ++cb) {
+      const int m = m0 + cb * 16 + r;
+      if (m < M) *(floatx4 *)(Ys + (size_t)m * ldy + ny + rb * 16 + gq * 4) = acc[rb][cb];
     }
-    __syncthreads();
-    const int rows_here = min(64, 16 * MB - half * 64);
-    for (int e = threadIdx.x; e < rows_here * kRowsPerWG; e += 256) {
-      const int m = e / kRowsPerWG, n = e % kRowsPerWG;
-      const int mg = m0 + half * 64 + m;
-      if (mg < M) {
-        const float v = ((red[0][m][n] + red[1][m][n]) + red[2][m][n]) + red[3][m][n];
-        Ys[(size_t)mg * ldy + n0 + n] = v;
-      }
-    }
-  }
 }
 
 // fp32: 64 output columns x 16 rows per workgroup, reduction staged through LDS.
@@ -162,39 +182,62 @@ __global__ __launch_bounds__(256) void k_gemm_f32(WSegs segs, int N, int K, cons
 
 }  // namespace
 
-// Reduction splits for a weight matrix of n_full rows and K columns.  Depends
-// on the matrix shape only (never on the number of stacked rows), so every
-// output element is summed in the same order whichever paths are active.
-int gemm_splits(int n_full, int K, int dtype) {
-  if (dtype != 1) return 1;
-  const int tiles = n_full / kRowsPerWG;
-  int best = 1;
-  for (int S = 1; S <= 8; ++S) {
-    if (K % (kChunk * S) != 0 || K / S < 4 * kChunk) continue;
-    best = S;
-    if (tiles * S >= 256) break;
+// Launch configuration of a weight matrix of n_full rows and K columns:
+// row blocks per wave (RB), weight prefetch depth (PD) and reduction splits
+// (S).  It depends on the matrix shape only (never on the number of stacked
+// rows), so every output element is summed in the same order whichever paths
+// are active.
+// seg_gran: every segment boundary of the stacked matrices is a multiple of it.
+GemmConfig gemm_config(int n_full, int K, int dtype, int seg_gran) {
+  GemmConfig g{1, 1, 1};
+  if (dtype != 1) return g;
+  if (n_full >= 65536 && seg_gran % 256 == 0) {
+    g = GemmConfig{4, 1, 1};       // output-matrix shapes: 256 rows per workgroup
+  } else if (n_full >= 16384 && seg_gran % 128 == 0) {
+    g = GemmConfig{2, 3, 1};       // MLP up projections
+  } else {
+    g = GemmConfig{1, 2, 1};       // thin matrices: split the reduction
+    const int tiles = n_full / 64;
+    for (int S = 1; S <= 8; ++S) {
+      if (K % (kChunk * S) != 0 || K / S < 4 * kChunk) continue;
+      g.S = S;
+      if (tiles * S >= 448) break;
+    }
   }
-  return best;
+  return g;
 }
 
-hipError_t launch_gemm(const WSegs &segs, int N, int K, int dtype, const void *X, int ldx, int M,
-                       float *Y, int ldy, long long y_split_stride, int S, hipStream_t st) {
+namespace {
+template <int MB>
+void launch_mb(const GemmConfig &g, dim3 grid, hipStream_t st, const WSegs &segs, int K, const uint16_t *X, int ldx,
+               int M, float *Y, int ldy, long long yss, int kps) {
+  if (g.RB == 4)
+    hipLaunchKernelGGL((k_gemm_bf16<MB, 4, 1>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, kps);
+  else if (g.RB == 2)
+    hipLaunchKernelGGL((k_gemm_bf16<MB, 2, (MB > 4 ? 2 : 3)>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, kps);
+  else
+    hipLaunchKernelGGL((k_gemm_bf16<MB, 1, 2>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, kps);
+}
+}  // namespace
+
+hipError_t launch_gemm(const WSegs &segs, int N, int K, int dtype, const void *X, int ldx, int M, float *Y,
+                       int ldy, long long y_split_stride, const GemmConfig &g, hipStream_t st) {
   if (M <= 0 || N <= 0) return hipSuccess;
   if (dtype == 1) {
     const int mb_total = (M + 15) / 16;
     const int MB = mb_total >= 8 ? 8 : mb_total;
-    dim3 grid(N / kRowsPerWG, S, (mb_total + MB - 1) / MB);
-    const int kps = K / S;
+    dim3 grid(N / (64 * g.RB), g.S, (mb_total + MB - 1) / MB);
+    const int kps = K / g.S;
     const uint16_t *Xb = (const uint16_t *)X;
     switch (MB) {
-      case 1: hipLaunchKernelGGL(k_gemm_bf16<1>, grid, dim3(256), 0, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps); break;
-      case 2: hipLaunchKernelGGL(k_gemm_bf16<2>, grid, dim3(256), 0, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps); break;
-      case 3: hipLaunchKernelGGL(k_gemm_bf16<3>, grid, dim3(256), 0, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps); break;
-      case 4: hipLaunchKernelGGL(k_gemm_bf16<4>, grid, dim3(256), 0, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps); break;
-      case 5: hipLaunchKernelGGL(k_gemm_bf16<5>, grid, dim3(256), 0, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps); break;
-      case 6: hipLaunchKernelGGL(k_gemm_bf16<6>, grid, dim3(256), 0, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps); break;
-      case 7: hipLaunchKernelGGL(k_gemm_bf16<7>, grid, dim3(256), 0, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps); break;
-      default: hipLaunchKernelGGL(k_gemm_bf16<8>, grid, dim3(256), 0, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps); break;
+      case 1: launch_mb<1>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps); break;
+      case 2: launch_mb<2>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps); break;
+      case 3: launch_mb<3>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps); break;
+      case 4: launch_mb<4>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps); break;
+      case 5: launch_mb<5>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps); break;
+      case 6: launch_mb<6>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps); break;
+      case 7: launch_mb<7>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps); break;
+      default: launch_mb<8>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps); break;
     }
   } else {
     dim3 grid((N + 63) / 64, (M + 15) / 16);

@@ -42,9 +42,14 @@ struct KVRef {
 };
 
 // ---- projections ----
-int gemm_splits(int n_full, int K, int dtype);
+struct GemmConfig {
+  int RB;  // 16-row blocks per wave (a workgroup owns 64*RB weight rows)
+  int PD;  // weight prefetch depth in 128-element chunks
+  int S;   // reduction splits (one fp32 output slab per split)
+};
+GemmConfig gemm_config(int n_full, int K, int dtype, int seg_gran);
 hipError_t launch_gemm(const WSegs &segs, int N, int K, int dtype, const void *X, int ldx, int M,
-                       float *Y, int ldy, long long y_split_stride, int S, hipStream_t st);
+                       float *Y, int ldy, long long y_split_stride, const GemmConfig &g, hipStream_t st);
 
 // ---- row-wise and elementwise stages ----
 struct StepBegin {
