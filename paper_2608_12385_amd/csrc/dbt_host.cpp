@@ -52,7 +52,7 @@ int round16(int x) { return (x + 15) / 16 * 16; }
 struct Layout {
   int Bp_max = 0, R_max = 0, rows_max = 0, max_in = 0, nqkv = 0, f = 0;
   GemmConfig g_qkv{1, 1, 1}, g_o{1, 1, 1}, g_gu{1, 1, 1}, g_d{1, 1, 1}, g_lm{1, 1, 1};
-  int max_splits = 0, nch = 0;
+  int max_splits = 0, nch = 0, nstat = 0;
   size_t rope = 0, pos = 0, S = 0, Xn = 0, Xh = 0, Q = 0, O = 0, P = 0, apart = 0, astat = 0,
          logits = 0, mstats = 0, mcand = 0, ret_q = 0, ret_h = 0, ret_m = 0, btok = 0, slast = 0,
          total = 0;
@@ -100,6 +100,7 @@ Layout make_layout(const dbt_config *c) {
   L.g_gu = gemm_config(2 * L.f, d, c->dtype, L.f);
   L.g_d = gemm_config(d, L.f, c->dtype, d);
   L.g_lm = gemm_config(std::max(c->vocab, 1), d, c->dtype, std::max(c->vocab, 1));
+  L.g_lm.S = 1;  // the logits are written in place (one slab)
   const int maxpages = (c->max_pos + kPage - 1) / kPage;
   L.max_splits = (maxpages + kPagesPerSplit - 1) / kPagesPerSplit;
   L.nch = c->vocab > 0 ? (c->vocab + kMixChunk - 1) / kMixChunk : 0;
@@ -119,7 +120,9 @@ Layout make_layout(const dbt_config *c) {
   L.apart = take((size_t)c->max_batch * c->n_kv_heads * L.max_splits * 16 * c->head_dim * 4);
   L.astat = take((size_t)c->max_batch * c->n_kv_heads * L.max_splits * 16 * 2 * 4);
   L.logits = take((size_t)L.R_max * std::max(c->vocab, 1) * 4);
-  L.mstats = take((size_t)L.R_max * std::max(L.nch, 1) * 3 * 4);
+  L.nstat = gemm_stats_tiles(std::max(c->vocab, 1), L.g_lm, c->dtype);
+  if (L.nstat == 0) L.nstat = std::max(L.nch, 1);
+  L.mstats = take((size_t)L.R_max * L.nstat * 3 * 4);
   L.mcand = take((size_t)c->max_batch * std::max(L.nch, 1) * 2 * 4);
   L.ret_q = take((size_t)c->n_layers * L.Bp_max * dq * 4);
   L.ret_h = take((size_t)c->n_layers * L.Bp_max * L.f * 4);
@@ -408,9 +411,10 @@ dbt_status lm_head(dbt_model *m, Rows rows, hipStream_t st) {
   const int xrow0 = rows.p0 * rows.Bp;
   WSegs lm{{m->w.lm_head, nullptr, nullptr}, {cf.vocab, 0, 0}};
   Timed tm(m, DBT_STAGE_LMHEAD, st);
+  const bool fused = gemm_stats_tiles(cf.vocab, L.g_lm, cf.dtype) > 0;
   HIPCHK(launch_gemm(lm, cf.vocab, cf.d_model, cf.dtype, m->ws + L.Xn + (size_t)xrow0 * cf.d_model * esize(cf),
                      cf.d_model, rows.np * rows.Bp, m->at<float>(L.logits) + (size_t)xrow0 * cf.vocab, cf.vocab,
-                     0, L.g_lm, st));
+                     0, L.g_lm, st, fused ? m->at<float>(L.mstats) + (size_t)xrow0 * L.nstat * 3 : nullptr));
   return DBT_OK;
 }
 
@@ -424,6 +428,8 @@ dbt_status readout(dbt_model *m, int B, int Bp, bool branch, dbt_step_out *out, 
   mx.rows = Rows{B, Bp, 0, branch ? 2 : 1};
   mx.chunk = kMixChunk;
   mx.stats = m->at<float>(L.mstats);
+  mx.stats_ready = gemm_stats_tiles(cf.vocab, L.g_lm, cf.dtype) > 0;
+  mx.nstat = L.nstat;
   mx.cand = m->at<float>(L.mcand);
   mx.alpha = out ? out->alpha : nullptr;
   mx.next = out ? out->next_token : nullptr;

@@ -300,7 +300,7 @@ __global__ void k_mix_stats(MixArgs m) {
   const int y = blockIdx.y;
   const int path = m.rows.p0 + y / m.rows.B, b = y % m.rows.B;
   const int row = phys_row(m.rows, path, b);
-  const int nch = (m.V + m.chunk - 1) / m.chunk;
+  const int nch = m.nstat;
   const int lo = c * m.chunk, hi = min(m.V, lo + m.chunk);
   const float *z = m.logits + (size_t)row * m.V;
   // each thread keeps its values in registers between the two passes
@@ -337,17 +337,21 @@ __global__ void k_mix_stats(MixArgs m) {
   }
 }
 
+// Merge the per-tile statistics of one row with one wave (fixed-order tree).
 __device__ void merged_stats(const MixArgs &m, int row, float &lse, float &p2) {
-  const int nch = (m.V + m.chunk - 1) / m.chunk;
-  const float *st = m.stats + (size_t)row * nch * 3;
+  const int lane = threadIdx.x & 63;
+  const float *st = m.stats + (size_t)row * m.nstat * 3;
   float mx = -INFINITY;
-  for (int c = 0; c < nch; ++c) mx = fmaxf(mx, st[c * 3]);
+  for (int c = lane; c < m.nstat; c += 64) mx = fmaxf(mx, st[c * 3]);
+  mx = wave_max(mx);
   float z = 0.f, y = 0.f;
-  for (int c = 0; c < nch; ++c) {
+  for (int c = lane; c < m.nstat; c += 64) {
     const float e = expf(st[c * 3] - mx);
     z += st[c * 3 + 1] * e;
     y += st[c * 3 + 2] * e * e;
   }
+  z = wave_sum(z);
+  y = wave_sum(y);
   lse = mx + logf(z);
   p2 = y / (z * z);
 }
@@ -355,17 +359,23 @@ __device__ void merged_stats(const MixArgs &m, int row, float &lse, float &p2) {
 __global__ void k_mix_argmax(MixArgs m) {
   __shared__ float rv[16];
   __shared__ int ri[16];
+  __shared__ float sh[3];
   const int c = blockIdx.x, b = blockIdx.y;
   const bool on = m.rows.np == 2;
   const int nch = (m.V + m.chunk - 1) / m.chunk;
   const int r1 = phys_row(m.rows, 0, b), r2 = phys_row(m.rows, 1, b);
-  float lse1 = 0.f, p2 = 0.f, lse2 = 0.f, alpha = 1.f;
-  if (on) {
+  if (on && threadIdx.x < 64) {
+    float lse1, p2, lse2, dummy;
     merged_stats(m, r1, lse1, p2);
-    float dummy;
     merged_stats(m, r2, lse2, dummy);
-    alpha = fminf(1.f, fmaxf(0.5f, p2));
+    if (threadIdx.x == 0) {
+      sh[0] = lse1;
+      sh[1] = fminf(1.f, fmaxf(0.5f, p2));
+      sh[2] = lse2;
+    }
   }
+  __syncthreads();
+  const float lse1 = on ? sh[0] : 0.f, alpha = on ? sh[1] : 1.f, lse2 = on ? sh[2] : 0.f;
   const int lo = c * m.chunk, hi = min(m.V, lo + m.chunk);
   const float *z1 = m.logits + (size_t)r1 * m.V;
   const float *z2 = m.logits + (size_t)r2 * m.V;
@@ -521,7 +531,7 @@ hipError_t launch_kv_fill(KVRef kv, int seq, int start, int count, const void *k
 
 hipError_t launch_mixture(const MixArgs &m, hipStream_t st) {
   const int nch = (m.V + m.chunk - 1) / m.chunk;
-  hipLaunchKernelGGL(k_mix_stats, dim3(nch, m.rows.np * m.rows.B), dim3(256), 0, st, m);
+  if (!m.stats_ready) hipLaunchKernelGGL(k_mix_stats, dim3(nch, m.rows.np * m.rows.B), dim3(256), 0, st, m);
   hipLaunchKernelGGL(k_mix_argmax, dim3(nch, m.rows.B), dim3(256), 0, st, m);
   hipLaunchKernelGGL(k_mix_final, dim3(m.rows.B), dim3(64), 0, st, m);
   return hipGetLastError();

@@ -30,7 +30,7 @@ constexpr int kLdsRow = kChunk + 8;  // padded LDS row of a staged activation ch
 template <int MB, int RB, int PD>
 __global__ __launch_bounds__(256) void k_gemm_bf16(WSegs segs, int K, const uint16_t *__restrict__ X, int ldx,
                                                    int M, float *__restrict__ Y, int ldy, long long y_split_stride,
-                                                   int k_per_split) {
+                                                   int k_per_split, float *__restrict__ row_stats) {
   constexpr int XR = 16 * MB;
   constexpr int PIECES = XR * (kChunk / 8);  // 16-byte pieces of one activation chunk
   constexpr int PPT = (PIECES + 255) / 256;
@@ -125,6 +125,54 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(WSegs segs, int K, const uint
     }
   }
   // lane holds D[n = rb*16 + 4*gq + i][m = cb*16 + r]: Y[m][n .. n+3]
+  if (row_stats) {
+    // Softmax statistics of each activation row over this workgroup's 64*RB
+    // outputs (one tile): max, sum e^(y - max), sum e^(2(y - max)); waves are
+    // merged in wave order.  Used by the mixture readout (no split here).
+    __shared__ float smx[4][XR], s1[4][XR], s2[4][XR];
+#pragma unroll
+    for (int cb = 0; cb < MB; ++cb) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) mx = fmaxf(mx, acc[rb][cb][i]);
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      if (gq == 0) smx[wave][cb * 16 + r] = mx;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int cb = 0; cb < MB; ++cb) {
+      const int mm = cb * 16 + r;
+      const float mx = fmaxf(fmaxf(smx[0][mm], smx[1][mm]), fmaxf(smx[2][mm], smx[3][mm]));
+      float e1 = 0.f, e2 = 0.f;
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float e = expf(acc[rb][cb][i] - mx);
+          e1 += e;
+          e2 += e * e;
+        }
+      e1 += __shfl_xor(e1, 16, 64);
+      e1 += __shfl_xor(e1, 32, 64);
+      e2 += __shfl_xor(e2, 16, 64);
+      e2 += __shfl_xor(e2, 32, 64);
+      if (gq == 0) {
+        s1[wave][mm] = e1;
+        s2[wave][mm] = e2;
+      }
+    }
+    __syncthreads();
+    if (t < XR && m0 + t < M) {
+      const float mx = fmaxf(fmaxf(smx[0][t], smx[1][t]), fmaxf(smx[2][t], smx[3][t]));
+      float *o = row_stats + ((size_t)(m0 + t) * gridDim.x + blockIdx.x) * 3;
+      o[0] = mx;
+      o[1] = ((s1[0][t] + s1[1][t]) + s1[2][t]) + s1[3][t];
+      o[2] = ((s2[0][t] + s2[1][t]) + s2[2][t]) + s2[3][t];
+    }
+  }
   float *Ys = Y + (long long)split * y_split_stride;
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb)
@@ -210,18 +258,23 @@ GemmConfig gemm_config(int n_full, int K, int dtype, int seg_gran) {
 namespace {
 template <int MB>
 void launch_mb(const GemmConfig &g, dim3 grid, hipStream_t st, const WSegs &segs, int K, const uint16_t *X, int ldx,
-               int M, float *Y, int ldy, long long yss, int kps) {
+               int M, float *Y, int ldy, long long yss, int kps, float *rs) {
   if (g.RB == 4)
-    hipLaunchKernelGGL((k_gemm_bf16<MB, 4, 1>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, kps);
+    hipLaunchKernelGGL((k_gemm_bf16<MB, 4, 1>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, kps, rs);
   else if (g.RB == 2)
-    hipLaunchKernelGGL((k_gemm_bf16<MB, 2, (MB > 4 ? 2 : 3)>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, kps);
+    hipLaunchKernelGGL((k_gemm_bf16<MB, 2, (MB > 4 ? 2 : 3)>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss,
+                       kps, rs);
   else
-    hipLaunchKernelGGL((k_gemm_bf16<MB, 1, 2>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, kps);
+    hipLaunchKernelGGL((k_gemm_bf16<MB, 1, 2>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, kps, rs);
 }
 }  // namespace
 
+int gemm_stats_tiles(int N, const GemmConfig &g, int dtype) {
+  return (dtype == 1 && g.S == 1) ? N / (64 * g.RB) : 0;
+}
+
 hipError_t launch_gemm(const WSegs &segs, int N, int K, int dtype, const void *X, int ldx, int M, float *Y,
-                       int ldy, long long y_split_stride, const GemmConfig &g, hipStream_t st) {
+                       int ldy, long long y_split_stride, const GemmConfig &g, hipStream_t st, float *row_stats) {
   if (M <= 0 || N <= 0) return hipSuccess;
   if (dtype == 1) {
     const int mb_total = (M + 15) / 16;
@@ -229,15 +282,16 @@ hipError_t launch_gemm(const WSegs &segs, int N, int K, int dtype, const void *X
     dim3 grid(N / (64 * g.RB), g.S, (mb_total + MB - 1) / MB);
     const int kps = K / g.S;
     const uint16_t *Xb = (const uint16_t *)X;
+    float *rs = g.S == 1 ? row_stats : nullptr;
     switch (MB) {
-      case 1: launch_mb<1>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps); break;
-      case 2: launch_mb<2>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps); break;
-      case 3: launch_mb<3>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps); break;
-      case 4: launch_mb<4>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps); break;
-      case 5: launch_mb<5>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps); break;
-      case 6: launch_mb<6>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps); break;
-      case 7: launch_mb<7>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps); break;
-      default: launch_mb<8>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps); break;
+      case 1: launch_mb<1>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps, rs); break;
+      case 2: launch_mb<2>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps, rs); break;
+      case 3: launch_mb<3>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps, rs); break;
+      case 4: launch_mb<4>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps, rs); break;
+      case 5: launch_mb<5>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps, rs); break;
+      case 6: launch_mb<6>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps, rs); break;
+      case 7: launch_mb<7>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps, rs); break;
+      default: launch_mb<8>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps, rs); break;
     }
   } else {
     dim3 grid((N + 63) / 64, (M + 15) / 16);

@@ -49,7 +49,11 @@ struct GemmConfig {
 };
 GemmConfig gemm_config(int n_full, int K, int dtype, int seg_gran);
 hipError_t launch_gemm(const WSegs &segs, int N, int K, int dtype, const void *X, int ldx, int M,
-                       float *Y, int ldy, long long y_split_stride, const GemmConfig &g, hipStream_t st);
+                       float *Y, int ldy, long long y_split_stride, const GemmConfig &g, hipStream_t st,
+                       float *row_stats = nullptr);
+// Tiles per row of the statistics the output projection writes when given
+// row_stats (0: this shape does not produce them).
+int gemm_stats_tiles(int N, const GemmConfig &g, int dtype);
 
 // ---- row-wise and elementwise stages ----
 struct StepBegin {
@@ -131,8 +135,10 @@ struct MixArgs {
   const float *logits;  // [2Bp][V]
   int V;
   Rows rows;            // np = 2 with the branch on, 1 (primary) otherwise
-  int chunk;            // vocabulary entries per chunk
-  float *stats;         // [2Bp][nchunks][3]
+  int chunk;            // vocabulary entries per argmax chunk
+  float *stats;         // [2Bp][nstat][3] per-tile (max, sum e^(z-max), sum e^(2(z-max)))
+  int nstat;            // tiles per row in stats
+  int stats_ready;      // 1: the output projection already wrote stats (tiles of 256)
   float *cand;          // [B][nchunks][2] (value, index as float bits)
   float *alpha;         // [B] or NULL
   int *next;            // [B] or NULL
