@@ -235,10 +235,16 @@ dbt_status ensure_device(dbt_model *m, hipStream_t st) {
 }
 
 // Enqueue pending page-table entries and (optionally) per-sequence positions.
-dbt_status flush(dbt_kv *kv, const int *h_pos, int npos, hipStream_t st) {
+// With `fold` the last block is returned there instead of launched, for the
+// caller to pass to the step's first kernel.
+dbt_status flush(dbt_kv *kv, const int *h_pos, int npos, hipStream_t st, StepBegin *fold = nullptr) {
   dbt_model *m = kv->m;
   size_t ip = 0;
   int ipos = 0;
+  if (fold) {
+    fold->n_pos = fold->n_pt = 0;
+    fold->b0 = 0;
+  }
   while (ip < kv->pending.size() || ipos < npos) {
     StepBegin sb;
     std::memset(&sb, 0, sizeof sb);
@@ -253,6 +259,10 @@ dbt_status flush(dbt_kv *kv, const int *h_pos, int npos, hipStream_t st) {
       sb.pt_page[i] = kv->pending[ip + i].page;
     }
     ip += sb.n_pt;
+    if (fold && ip >= kv->pending.size() && ipos >= npos) {
+      *fold = sb;
+      break;
+    }
     HIPCHK(launch_step_begin(sb, m->at<int>(m->L.pos), kv->page_table, kv->mpps, st));
   }
   kv->pending.clear();
@@ -390,16 +400,18 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
 
 // Step inputs for the active rows: embeddings (Eq. (7)) or given residuals,
 // then the first layer's attention norm.
-dbt_status load_inputs(dbt_model *m, const dbt_step_in *in, const int *tokens, Rows rows, hipStream_t st) {
+dbt_status load_inputs(dbt_model *m, dbt_kv *kv, const dbt_step_in *in, const int *tokens, Rows rows,
+                       hipStream_t st, const StepBegin *sb = nullptr) {
   const dbt_config &cf = m->cfg;
   const Layout &L = m->L;
   const float *g0 = m->layers[0].attn_norm;
   if (cf.has_embeddings) {
     HIPCHK(launch_embed(tokens, cf.vocab, m->w.emb1, m->w.emb2, m->w.emb_norm, g0, cf.rms_eps, cf.d_model, cf.dtype, rows,
-                        m->at<float>(L.S), m->ws + L.Xn, cf.d_model, st));
+                        m->at<float>(L.S), m->ws + L.Xn, cf.d_model, st, sb, m->at<int>(L.pos), kv->page_table,
+                        kv->mpps));
   } else {
     HIPCHK(launch_load_hidden(in->h1_in, in->h2_in, g0, cf.rms_eps, cf.d_model, cf.dtype, rows, m->at<float>(L.S),
-                              m->ws + L.Xn, cf.d_model, st));
+                              m->ws + L.Xn, cf.d_model, st, sb, m->at<int>(L.pos), kv->page_table, kv->mpps));
   }
   return DBT_OK;
 }
@@ -677,10 +689,11 @@ dbt_status dbt_decode_step(dbt_model *m, dbt_kv *kv, const dbt_step_in *in, int3
   m->bnd_kv = nullptr;
   std::vector<int> pos = begin_step(kv, B);
   if ((s = ensure_device(m, st))) return s;
-  if ((s = flush(kv, pos.data(), B, st))) return s;
+  StepBegin sb;
+  if ((s = flush(kv, pos.data(), B, st, &sb))) return s;
   const bool on = branch_on != 0;
   const Rows rows{B, Bp, 0, on ? 2 : 1};
-  if ((s = load_inputs(m, in, in->tokens, rows, st))) return s;
+  if ((s = load_inputs(m, kv, in, in->tokens, rows, st, &sb))) return s;
   LayerCall lc{};
   lc.rows = rows;
   lc.mode = on ? MODE_GROUPED : MODE_PRIMARY;
@@ -713,10 +726,11 @@ dbt_status dbt_decode_step_ungrouped(dbt_model *m, dbt_kv *kv, const dbt_step_in
   m->bnd_kv = nullptr;
   std::vector<int> pos = begin_step(kv, B);
   if ((s = ensure_device(m, st))) return s;
-  if ((s = flush(kv, pos.data(), B, st))) return s;
+  StepBegin sb;
+  if ((s = flush(kv, pos.data(), B, st, &sb))) return s;
   // pass 1: every primary layer, keeping Q1, H1, M1
   const Rows prim{B, Bp, 0, 1};
-  if ((s = load_inputs(m, in, in->tokens, prim, st))) return s;
+  if ((s = load_inputs(m, kv, in, in->tokens, prim, st, &sb))) return s;
   LayerCall lc{};
   lc.rows = prim;
   lc.mode = MODE_PRIMARY;
@@ -730,7 +744,7 @@ dbt_status dbt_decode_step_ungrouped(dbt_model *m, dbt_kv *kv, const dbt_step_in
   if (cf.vocab > 0 && (s = lm_head(m, prim, st))) return s;
   // pass 2: every branch layer
   const Rows br{B, Bp, 1, 1};
-  if ((s = load_inputs(m, in, in->tokens, br, st))) return s;
+  if ((s = load_inputs(m, kv, in, in->tokens, br, st))) return s;
   if ((s = branch_pass(m, kv, B, Bp, st))) return s;
   for (int b = 0; b < B; ++b) kv->len[b] += 1;
   if (out) {

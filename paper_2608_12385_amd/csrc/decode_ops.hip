@@ -10,21 +10,38 @@
 #include "common.h"
 #include "kernels.h"
 
+#include <algorithm>
+
 namespace dbt {
 
 namespace {
 
 __device__ __forceinline__ int phys_row(const Rows &r, int path, int b) { return path * r.Bp + b; }
 
+// Sum of the split-K partial slabs in split order (S <= 8).
 __device__ __forceinline__ float psum(const float *part, long long stride, int S, size_t idx) {
+  float v[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) v[k] = k < S ? part[k * stride + idx] : 0.f;
   float s = 0.f;
-  for (int k = 0; k < S; ++k) s += part[k * stride + idx];
+#pragma unroll
+  for (int k = 0; k < 8; ++k)
+    if (k < S) s += v[k];
   return s;
 }
 
 // ---------------------------------------------------------------------------
 
 __global__ void k_step_begin(StepBegin sb, int *pos_arr, int *page_table, int mpps) {
+  const int t = threadIdx.x;
+  if (t < sb.n_pos) pos_arr[sb.b0 + t] = sb.pos[t];
+  if (t < sb.n_pt) page_table[(size_t)sb.pt_b[t] * mpps + sb.pt_slot[t]] = sb.pt_page[t];
+}
+
+// Per-step positions and page-table entries travel as kernel arguments of
+// the step's first kernel (no host-to-device copy); block (0,0) writes them.
+__device__ __forceinline__ void apply_step_begin(const StepBegin &sb, int *pos_arr, int *page_table, int mpps) {
+  if (blockIdx.x != 0 || blockIdx.y != 0 || !pos_arr) return;
   const int t = threadIdx.x;
   if (t < sb.n_pos) pos_arr[sb.b0 + t] = sb.pos[t];
   if (t < sb.n_pt) page_table[(size_t)sb.pt_b[t] * mpps + sb.pt_slot[t]] = sb.pt_page[t];
@@ -53,8 +70,13 @@ __device__ __forceinline__ float4 mul4(float4 a, float s, float4 g) {
   return make_float4(a.x * s * g.x, a.y * s * g.y, a.z * s * g.z, a.w * s * g.w);
 }
 __device__ __forceinline__ float4 psum4(const float *part, long long stride, int S, size_t idx4) {
+  float4 v[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) v[k] = k < S ? ((const float4 *)(part + k * stride))[idx4] : make_float4(0.f, 0.f, 0.f, 0.f);
   float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int k = 0; k < S; ++k) s = add4(s, ((const float4 *)(part + k * stride))[idx4]);
+#pragma unroll
+  for (int k = 0; k < 8; ++k)
+    if (k < S) s = add4(s, v[k]);
   return s;
 }
 
@@ -72,8 +94,10 @@ __device__ void norm_row(const float *x, const float *g, float eps, int d, T *ou
 // Tokens outside [0, vocab) read as a zero embedding row (no out-of-bounds read).
 template <typename T>
 __global__ void k_embed(const int *tokens, int vocab, const T *e1, const T *e2, const float *g_emb,
-                        const float *g_next, float eps, int d, Rows rows, float *S, T *Xn, int ldx) {
+                        const float *g_next, float eps, int d, Rows rows, float *S, T *Xn, int ldx, StepBegin sb,
+                        int *pos_arr, int *page_table, int mpps) {
   __shared__ float red[16];
+  apply_step_begin(sb, pos_arr, page_table, mpps);
   const int b = blockIdx.x, path = rows.p0 + blockIdx.y;
   const int row = phys_row(rows, path, b);
   const int tok = tokens[b];
@@ -95,8 +119,10 @@ __global__ void k_embed(const int *tokens, int vocab, const T *e1, const T *e2, 
 
 template <typename T>
 __global__ void k_load_hidden(const float *h1, const float *h2, const float *g_next, float eps, int d,
-                              Rows rows, float *S, T *Xn, int ldx) {
+                              Rows rows, float *S, T *Xn, int ldx, StepBegin sb, int *pos_arr, int *page_table,
+                              int mpps) {
   __shared__ float red[16];
+  apply_step_begin(sb, pos_arr, page_table, mpps);
   const int b = blockIdx.x, path = rows.p0 + blockIdx.y;
   const int row = phys_row(rows, path, b);
   const float *h = (path == 0 ? h1 : h2) + (size_t)b * d;
@@ -338,14 +364,33 @@ __global__ void k_mix_stats(MixArgs m) {
 }
 
 // Merge the per-tile statistics of one row with one wave (fixed-order tree).
+// Up to 16 tiles per lane are loaded at once (one memory round trip).
 __device__ void merged_stats(const MixArgs &m, int row, float &lse, float &p2) {
   const int lane = threadIdx.x & 63;
   const float *st = m.stats + (size_t)row * m.nstat * 3;
+  constexpr int PER = 16;
+  float tm[PER], t1[PER], t2[PER];
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int c = lane + 64 * k;
+    const bool ok = c < m.nstat;
+    tm[k] = ok ? st[c * 3] : -INFINITY;
+    t1[k] = ok ? st[c * 3 + 1] : 0.f;
+    t2[k] = ok ? st[c * 3 + 2] : 0.f;
+  }
   float mx = -INFINITY;
-  for (int c = lane; c < m.nstat; c += 64) mx = fmaxf(mx, st[c * 3]);
+#pragma unroll
+  for (int k = 0; k < PER; ++k) mx = fmaxf(mx, tm[k]);
+  for (int c = lane + 64 * PER; c < m.nstat; c += 64) mx = fmaxf(mx, st[c * 3]);
   mx = wave_max(mx);
   float z = 0.f, y = 0.f;
-  for (int c = lane; c < m.nstat; c += 64) {
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const float e = expf(tm[k] - mx);
+    z += t1[k] * e;
+    y += t2[k] * e * e;
+  }
+  for (int c = lane + 64 * PER; c < m.nstat; c += 64) {
     const float e = expf(st[c * 3] - mx);
     z += st[c * 3 + 1] * e;
     y += st[c * 3 + 2] * e * e;
@@ -381,9 +426,21 @@ __global__ void k_mix_argmax(MixArgs m) {
   const float *z2 = m.logits + (size_t)r2 * m.V;
   float best = -INFINITY;
   int bi = 0x7fffffff;
-  for (int v = lo + threadIdx.x; v < hi; v += blockDim.x) {
-    const float val = on ? alpha * expf(z1[v] - lse1) + (1.f - alpha) * expf(z2[v] - lse2) : z1[v];
-    argmax_merge(best, bi, val, v);
+  constexpr int PER = 16;  // chunk = PER * blockDim.x
+  float a1[PER], a2[PER];
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int v = lo + threadIdx.x + k * blockDim.x;
+    a1[k] = v < hi ? z1[v] : -INFINITY;
+    a2[k] = (on && v < hi) ? z2[v] : -INFINITY;
+  }
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int v = lo + threadIdx.x + k * blockDim.x;
+    if (v < hi) {
+      const float val = on ? alpha * expf(a1[k] - lse1) + (1.f - alpha) * expf(a2[k] - lse2) : a1[k];
+      argmax_merge(best, bi, val, v);
+    }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
@@ -403,9 +460,10 @@ __global__ void k_mix_argmax(MixArgs m) {
   }
 }
 
+// Merge the chunk candidates of each sequence in chunk order.
 __global__ void k_mix_final(MixArgs m) {
-  const int b = blockIdx.x;
-  if (threadIdx.x != 0) return;
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= m.rows.B) return;
   const int nch = (m.V + m.chunk - 1) / m.chunk;
   float best = -INFINITY;
   int bi = 0x7fffffff;
@@ -433,26 +491,40 @@ static int row_threads(int d) {
 
 hipError_t launch_embed(const int *tokens, int vocab, const void *e1, const void *e2, const float *g_emb,
                         const float *g_next, float eps, int d, int dtype, Rows rows, float *S,
-                        void *Xn, int ldx, hipStream_t st) {
+                        void *Xn, int ldx, hipStream_t st, const StepBegin *sb, int *pos_arr, int *page_table,
+                        int mpps) {
   dim3 grid(rows.B, rows.np);
+  StepBegin none;
+  none.n_pos = none.n_pt = 0;
+  none.b0 = 0;
+  const StepBegin &s = sb ? *sb : none;
+  const int threads = std::max(row_threads(d), 64);
   if (dtype == 1)
-    hipLaunchKernelGGL(k_embed<uint16_t>, grid, dim3(row_threads(d)), 0, st, tokens, vocab, (const uint16_t *)e1,
-                       (const uint16_t *)e2, g_emb, g_next, eps, d, rows, S, (uint16_t *)Xn, ldx);
+    hipLaunchKernelGGL(k_embed<uint16_t>, grid, dim3(threads), 0, st, tokens, vocab, (const uint16_t *)e1,
+                       (const uint16_t *)e2, g_emb, g_next, eps, d, rows, S, (uint16_t *)Xn, ldx, s, pos_arr,
+                       page_table, mpps);
   else
-    hipLaunchKernelGGL(k_embed<float>, grid, dim3(row_threads(d)), 0, st, tokens, vocab, (const float *)e1,
-                       (const float *)e2, g_emb, g_next, eps, d, rows, S, (float *)Xn, ldx);
+    hipLaunchKernelGGL(k_embed<float>, grid, dim3(threads), 0, st, tokens, vocab, (const float *)e1,
+                       (const float *)e2, g_emb, g_next, eps, d, rows, S, (float *)Xn, ldx, s, pos_arr, page_table,
+                       mpps);
   return hipGetLastError();
 }
 
 hipError_t launch_load_hidden(const float *h1, const float *h2, const float *g_next, float eps,
-                              int d, int dtype, Rows rows, float *S, void *Xn, int ldx, hipStream_t st) {
+                              int d, int dtype, Rows rows, float *S, void *Xn, int ldx, hipStream_t st,
+                              const StepBegin *sb, int *pos_arr, int *page_table, int mpps) {
   dim3 grid(rows.B, rows.np);
+  StepBegin none;
+  none.n_pos = none.n_pt = 0;
+  none.b0 = 0;
+  const StepBegin &s = sb ? *sb : none;
+  const int threads = std::max(row_threads(d), 64);
   if (dtype == 1)
-    hipLaunchKernelGGL(k_load_hidden<uint16_t>, grid, dim3(row_threads(d)), 0, st, h1, h2, g_next, eps, d, rows, S,
-                       (uint16_t *)Xn, ldx);
+    hipLaunchKernelGGL(k_load_hidden<uint16_t>, grid, dim3(threads), 0, st, h1, h2, g_next, eps, d, rows, S,
+                       (uint16_t *)Xn, ldx, s, pos_arr, page_table, mpps);
   else
-    hipLaunchKernelGGL(k_load_hidden<float>, grid, dim3(row_threads(d)), 0, st, h1, h2, g_next, eps, d, rows, S,
-                       (float *)Xn, ldx);
+    hipLaunchKernelGGL(k_load_hidden<float>, grid, dim3(threads), 0, st, h1, h2, g_next, eps, d, rows, S,
+                       (float *)Xn, ldx, s, pos_arr, page_table, mpps);
   return hipGetLastError();
 }
 
@@ -533,7 +605,7 @@ hipError_t launch_mixture(const MixArgs &m, hipStream_t st) {
   const int nch = (m.V + m.chunk - 1) / m.chunk;
   if (!m.stats_ready) hipLaunchKernelGGL(k_mix_stats, dim3(nch, m.rows.np * m.rows.B), dim3(256), 0, st, m);
   hipLaunchKernelGGL(k_mix_argmax, dim3(nch, m.rows.B), dim3(256), 0, st, m);
-  hipLaunchKernelGGL(k_mix_final, dim3(m.rows.B), dim3(64), 0, st, m);
+  hipLaunchKernelGGL(k_mix_final, dim3((m.rows.B + 63) / 64), dim3(64), 0, st, m);
   return hipGetLastError();
 }
 

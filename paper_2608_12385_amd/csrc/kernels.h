@@ -65,12 +65,16 @@ struct StepBegin {
 hipError_t launch_step_begin(const StepBegin &sb, int *pos_arr, int *page_table, int mpps,
                              hipStream_t st);
 
+// The step's first kernel also applies `sb` (positions and new page-table
+// entries) when sb is not NULL.
 hipError_t launch_embed(const int *tokens, int vocab, const void *e1, const void *e2, const float *g_emb,
                         const float *g_next, float eps, int d, int dtype, Rows rows, float *S,
-                        void *Xn, int ldx, hipStream_t st);
+                        void *Xn, int ldx, hipStream_t st, const StepBegin *sb = nullptr,
+                        int *pos_arr = nullptr, int *page_table = nullptr, int mpps = 0);
 hipError_t launch_load_hidden(const float *h1, const float *h2, const float *g_next, float eps,
                               int d, int dtype, Rows rows, float *S, void *Xn, int ldx,
-                              hipStream_t st);
+                              hipStream_t st, const StepBegin *sb = nullptr, int *pos_arr = nullptr,
+                              int *page_table = nullptr, int mpps = 0);
 hipError_t launch_rmsnorm_rows(const float *S, const float *g, float eps, int d, int dtype,
                                Rows rows, void *Xn, int ldx, hipStream_t st);
 
