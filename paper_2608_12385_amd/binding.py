@@ -227,7 +227,8 @@ class Session:
         self.cfg = dbt_config(
             n_layers=s.n_layers, d_model=s.d_model, n_q_heads=s.n_q_heads, n_kv_heads=s.n_kv_heads,
             head_dim=s.head_dim, d_ff=s.d_ff, vocab=s.vocab, n_experts=s.n_experts,
-            d_ff_expert=s.d_ff_expert, d_ff_shared=s.d_ff_shared, top_k1=s.top_k1, top_k2=s.top_k2,
+            d_ff_expert=s.d_ff_expert, d_ff_shared=s.d_ff_shared * max(0, s.n_shared_experts),
+            top_k1=s.top_k1, top_k2=s.top_k2,
             replay=int(s.replay), dtype=DBT_BF16 if s.dtype == "bf16" else DBT_F32,
             has_embeddings=int(s.has_embeddings), max_batch=max_batch, max_pos=max_pos,
             max_prompt=max_prompt, rms_eps=s.rms_eps, rope_theta=s.rope_theta)
@@ -302,6 +303,13 @@ class Session:
         if hidden:
             t["h1_out"] = torch.empty(batch, s.d_model, dtype=torch.float32, device=self.device)
             t["h2_out"] = torch.empty(batch, s.d_model, dtype=torch.float32, device=self.device)
+        if routing and s.n_experts > 0:
+            k2 = s.top_k1 if s.replay else s.top_k2
+            L = s.n_layers
+            t["route_idx1"] = torch.empty(L, batch, s.top_k1, dtype=torch.int32, device=self.device)
+            t["route_w1"] = torch.empty(L, batch, s.top_k1, dtype=torch.float32, device=self.device)
+            t["route_idx2"] = torch.empty(L, batch, k2, dtype=torch.int32, device=self.device)
+            t["route_w2"] = torch.empty(L, batch, k2, dtype=torch.float32, device=self.device)
         out = dbt_step_out(**{k: v.data_ptr() for k, v in t.items()})
         return out, t
 
@@ -338,7 +346,7 @@ class Session:
         h2d = None if h2 is None else torch.as_tensor(np.ascontiguousarray(h2, np.float32)).to(self.device)
         B = batch if batch is not None else (len(tokens) if tokens is not None else h1.shape[0])
         sin = self.step_in(B, tk, h1d, h2d)
-        out, t = self.outputs(B)
+        out, t = self.outputs(B, routing=True)
         if grouped:
             dbt_decode_step(self.model, self.kv, sin, int(branch_on), out, self.stream)
         else:

@@ -53,6 +53,11 @@ struct Layout {
   int Bp_max = 0, R_max = 0, rows_max = 0, max_in = 0, nqkv = 0, f = 0;
   GemmConfig g_qkv{1, 1, 1}, g_o{1, 1, 1}, g_gu{1, 1, 1}, g_d{1, 1, 1}, g_lm{1, 1, 1};
   int max_splits = 0, nch = 0, nstat = 0;
+  bool moe = false;
+  int fe = 0, fs = 0, amax = 0;
+  GemmConfig g_sgu{1, 1, 1}, g_sd{1, 1, 1};
+  size_t moe_idx = 0, moe_w = 0, moe_aslot = 0, moe_counts = 0, moe_offsets = 0, moe_arow = 0, moe_h = 0,
+         moe_y = 0, ret_idx = 0;
   size_t rope = 0, pos = 0, S = 0, Xn = 0, Xh = 0, Q = 0, O = 0, P = 0, apart = 0, astat = 0,
          logits = 0, mstats = 0, mcand = 0, ret_q = 0, ret_h = 0, ret_m = 0, btok = 0, slast = 0,
          total = 0;
@@ -68,8 +73,18 @@ dbt_status check_config(const dbt_config *c) {
   if (c->head_dim % 4) return fail(DBT_ERR_SHAPE, "head_dim must be a multiple of 4");
   if (c->d_model % 4) return fail(DBT_ERR_SHAPE, "d_model must be a multiple of 4");
   if (c->max_prompt > c->max_pos) return fail(DBT_ERR_SHAPE, "max_prompt > max_pos");
-  if (c->n_experts > 0) return fail(DBT_ERR_UNSUPPORTED, "MoE layers are not built in this library version");
-  if (c->d_ff <= 0) return fail(DBT_ERR_ARG, "d_ff must be positive");
+  if (c->n_experts > 0) {
+    if (c->dtype != DBT_BF16) return fail(DBT_ERR_UNSUPPORTED, "MoE layers run in bf16 only");
+    if (c->n_experts > 256 || c->d_model > 4096) return fail(DBT_ERR_UNSUPPORTED, "MoE needs n_experts <= 256, d_model <= 4096");
+    if (c->top_k1 < 1 || c->top_k1 > 8 || c->top_k2 < 1 || c->top_k2 > 8 || c->top_k1 > c->n_experts ||
+        c->top_k2 > c->n_experts)
+      return fail(DBT_ERR_ARG, "top_k1/top_k2 must be in [1, min(8, n_experts)]");
+    if (c->replay && c->top_k2 != c->top_k1) return fail(DBT_ERR_ARG, "router replay needs top_k2 == top_k1");
+    if (c->d_ff_expert <= 0 || c->d_ff_expert % 128 || c->d_ff_shared < 0 || c->d_ff_shared % 128)
+      return fail(DBT_ERR_UNSUPPORTED, "expert widths must be multiples of 128");
+  } else if (c->d_ff <= 0) {
+    return fail(DBT_ERR_ARG, "d_ff must be positive");
+  }
   if (c->has_embeddings && c->vocab <= 0) return fail(DBT_ERR_SHAPE, "token inputs need a vocabulary");
   if (c->max_prompt > 0 && !c->has_embeddings) return fail(DBT_ERR_SHAPE, "prefill needs token inputs");
   if (!(c->rms_eps >= 0.f) || !(c->rope_theta > 0.f)) return fail(DBT_ERR_ARG, "bad rms_eps/rope_theta");
@@ -79,7 +94,7 @@ dbt_status check_config(const dbt_config *c) {
   if (c->dtype == DBT_BF16) {
     const int dq = c->n_q_heads * c->head_dim, dkv = c->n_kv_heads * c->head_dim;
     if (c->head_dim != 128) return fail(DBT_ERR_UNSUPPORTED, "bf16 attention needs head_dim 128");
-    if (c->d_model % 128 || dq % 128 || c->d_ff % 128)
+    if (c->d_model % 128 || dq % 128 || (c->n_experts == 0 && c->d_ff % 128))
       return fail(DBT_ERR_UNSUPPORTED, "bf16 projections need d_model, n_q*d_h, d_ff multiples of 128");
     if (dkv % 64 || c->vocab % 64) return fail(DBT_ERR_UNSUPPORTED, "bf16 projections need n_kv*d_h, vocab multiples of 64");
   }
@@ -89,7 +104,10 @@ dbt_status check_config(const dbt_config *c) {
 Layout make_layout(const dbt_config *c) {
   Layout L;
   const int d = c->d_model, dq = c->n_q_heads * c->head_dim, dkv = c->n_kv_heads * c->head_dim;
-  L.f = c->d_ff;
+  L.moe = c->n_experts > 0;
+  L.fe = c->d_ff_expert;
+  L.fs = L.moe ? c->d_ff_shared : 0;
+  L.f = L.moe ? std::max(L.fs, 128) : c->d_ff;
   L.Bp_max = round16(c->max_batch);
   L.R_max = 2 * L.Bp_max;
   L.rows_max = std::max(L.R_max, c->max_prompt);
@@ -101,11 +119,16 @@ Layout make_layout(const dbt_config *c) {
   L.g_d = gemm_config(d, L.f, c->dtype, d);
   L.g_lm = gemm_config(std::max(c->vocab, 1), d, c->dtype, std::max(c->vocab, 1));
   L.g_lm.S = 1;  // the logits are written in place (one slab)
+  if (L.moe && L.fs > 0) {
+    L.g_sgu = gemm_config(2 * L.fs, d, c->dtype, L.fs);
+    L.g_sd = gemm_config(d, L.fs, c->dtype, d);
+  }
   const int maxpages = (c->max_pos + kPage - 1) / kPage;
   L.max_splits = (maxpages + kPagesPerSplit - 1) / kPagesPerSplit;
   L.nch = c->vocab > 0 ? (c->vocab + kMixChunk - 1) / kMixChunk : 0;
   size_t part = std::max({(size_t)L.g_qkv.S * L.R_max * L.nqkv, (size_t)L.g_o.S * L.R_max * d,
                           (size_t)L.g_gu.S * L.R_max * 2 * L.f, (size_t)L.g_d.S * L.R_max * d});
+  if (L.moe) part = std::max({part, (size_t)L.g_sgu.S * L.R_max * 2 * L.f, (size_t)L.g_sd.S * L.R_max * d});
   part = std::max(part, (size_t)c->max_prompt * std::max({L.nqkv, d, 2 * L.f}));
   size_t o = 0;
   auto take = [&](size_t bytes) { size_t at = o; o += align256(bytes); return at; };
@@ -127,6 +150,18 @@ Layout make_layout(const dbt_config *c) {
   L.ret_q = take((size_t)c->n_layers * L.Bp_max * dq * 4);
   L.ret_h = take((size_t)c->n_layers * L.Bp_max * L.f * 4);
   L.ret_m = take((size_t)c->n_layers * L.Bp_max * d * 4);
+  if (L.moe) {
+    L.amax = L.rows_max * 8;
+    L.moe_idx = take((size_t)L.rows_max * 8 * 4);
+    L.moe_w = take((size_t)L.rows_max * 8 * 4);
+    L.moe_aslot = take((size_t)L.rows_max * 8 * 4);
+    L.moe_counts = take((size_t)c->n_experts * 4);
+    L.moe_offsets = take((size_t)(c->n_experts + 1) * 4);
+    L.moe_arow = take((size_t)L.amax * 4);
+    L.moe_h = take((size_t)L.amax * L.fe * 2);
+    L.moe_y = take((size_t)L.amax * d * 4);
+    L.ret_idx = take((size_t)c->n_layers * L.Bp_max * 8 * 4);
+  }
   L.btok = take((size_t)c->max_batch * 4);
   L.slast = take((size_t)L.Bp_max * d * 4);
   L.total = o;
@@ -279,7 +314,141 @@ struct LayerCall {
   int seq;           // prefill: the sequence
   int rows_layout;   // prefill: T; decode: 2*Bp
   bool last_norm;    // apply the next norm after the layer
+  const dbt_step_out *out;  // routing outputs (MoE), may be NULL
 };
+
+// MoE MLP of layer l for the active rows: route, dispatch, touched experts,
+// shared expert (with the b coupling), combine (with the c coupling).
+dbt_status run_moe_mlp(dbt_model *m, int l, const LayerCall &c, hipStream_t st) {
+  const dbt_config &cf = m->cfg;
+  const Layout &L = m->L;
+  const dbt_layer_weights &W = m->layers[l];
+  const int d = cf.d_model, fs = L.fs;
+  const int xrow0 = c.rows.p0 * c.rows.Bp;
+  const int M = c.rows.np * c.rows.Bp;
+  const size_t es = esize(cf);
+  float *P = m->at<float>(L.P), *S = m->at<float>(L.S);
+  const size_t rq = (size_t)l * L.Bp_max;
+  float *ret_h = m->at<float>(L.ret_h) + rq * L.f;
+  float *ret_m = m->at<float>(L.ret_m) + rq * d;
+  int *ret_idx = m->at<int>(L.ret_idx) + rq * 8;
+  const int k2 = cf.replay ? cf.top_k1 : cf.top_k2;
+  MoeRoute ro{};
+  ro.Sbar = S;
+  ro.g = W.mlp_norm;
+  ro.eps = cf.rms_eps;
+  ro.d = d;
+  ro.Wr = W.router;
+  ro.E = cf.n_experts;
+  ro.k1 = cf.top_k1;
+  ro.k2 = k2;
+  ro.replay = cf.replay;
+  ro.rows = c.rows;
+  ro.mode = c.mode;
+  ro.idx = m->at<int>(L.moe_idx);
+  ro.wts = m->at<float>(L.moe_w);
+  ro.idx1_in = ret_idx;
+  if (c.out && !c.prefill) {
+    const size_t B = c.rows.B;
+    ro.out_idx1 = c.out->route_idx1 ? c.out->route_idx1 + (size_t)l * B * cf.top_k1 : nullptr;
+    ro.out_w1 = c.out->route_w1 ? c.out->route_w1 + (size_t)l * B * cf.top_k1 : nullptr;
+    ro.out_idx2 = c.out->route_idx2 ? c.out->route_idx2 + (size_t)l * B * k2 : nullptr;
+    ro.out_w2 = c.out->route_w2 ? c.out->route_w2 + (size_t)l * B * k2 : nullptr;
+  }
+  ro.ret_idx = c.retain ? ret_idx : nullptr;
+  ro.ret_src = c.ret_src;
+  ro.ret_dst = c.ret_dst;
+  HIPCHK(launch_moe_route(ro, st));
+  MoeDispatch di{};
+  di.idx = ro.idx;
+  di.rows = c.rows;
+  di.k1 = cf.top_k1;
+  di.k2 = k2;
+  di.E = cf.n_experts;
+  di.counts = m->at<int>(L.moe_counts);
+  di.offsets = m->at<int>(L.moe_offsets);
+  di.arow = m->at<int>(L.moe_arow);
+  di.aslot = m->at<int>(L.moe_aslot);
+  HIPCHK(launch_moe_dispatch(di, st));
+  const int max_rows = c.rows.np * c.rows.B;
+  {
+    Timed tm(m, DBT_STAGE_GATEUP, st);
+    MoeGemm g{};
+    g.X = m->ws + L.Xn;
+    g.ldx = d;
+    g.W0 = W.x_gate;
+    g.W1 = W.x_up;
+    g.E = cf.n_experts;
+    g.N = L.fe;
+    g.K = d;
+    g.counts = di.counts;
+    g.offsets = di.offsets;
+    g.arow = di.arow;
+    g.Y = m->ws + L.moe_h;
+    g.ldy = L.fe;
+    HIPCHK(launch_moe_gemm(g, true, max_rows, st));
+  }
+  {
+    Timed tm(m, DBT_STAGE_DOWN, st);
+    MoeGemm g{};
+    g.X = m->ws + L.moe_h;
+    g.ldx = L.fe;
+    g.W0 = W.x_down;
+    g.E = cf.n_experts;
+    g.N = d;
+    g.K = L.fe;
+    g.counts = di.counts;
+    g.offsets = di.offsets;
+    g.arow = di.arow;
+    g.Y = m->ws + L.moe_y;
+    g.ldy = d;
+    HIPCHK(launch_moe_gemm(g, false, max_rows, st));
+  }
+  // shared expert: dense SwiGLU of width fs with the b coupling on its intermediate
+  long long stride = (long long)c.rows_layout * d;
+  int S_sh = 0;
+  if (fs > 0) {
+    GemmConfig g_sgu = L.g_sgu, g_sd = L.g_sd;
+    if (c.prefill) g_sgu.S = g_sd.S = 1;
+    WSegs gu{{W.s_gate, W.s_up, nullptr}, {fs, fs, 0}};
+    long long st_gu = (long long)c.rows_layout * 2 * fs;
+    HIPCHK(launch_gemm(gu, 2 * fs, d, cf.dtype, m->ws + L.Xn + (size_t)xrow0 * d * es, d, M,
+                       P + (size_t)xrow0 * 2 * fs, 2 * fs, st_gu, g_sgu, st));
+    HIPCHK(launch_swiglu_finish(P, st_gu, g_sgu.S, 2 * fs, fs, c.mode, c.rows, W.b, ret_h,
+                                Retain{c.retain ? ret_h : nullptr, c.ret_src, c.ret_dst}, cf.dtype, m->ws + L.Xh, fs,
+                                st));
+    WSegs sd{{W.s_down, nullptr, nullptr}, {d, 0, 0}};
+    HIPCHK(launch_gemm(sd, d, fs, cf.dtype, m->ws + L.Xh + (size_t)xrow0 * fs * es, fs, M, P + (size_t)xrow0 * d, d,
+                       stride, g_sd, st));
+    S_sh = g_sd.S;
+  }
+  const float *g_next = nullptr;
+  if (l + 1 < cf.n_layers) g_next = m->layers[l + 1].attn_norm;
+  else if (cf.vocab > 0 && c.last_norm) g_next = m->w.final_norm;
+  MoeCombine cb{};
+  cb.rows = c.rows;
+  cb.mode = c.mode;
+  cb.d = d;
+  cb.k1 = cf.top_k1;
+  cb.k2 = k2;
+  cb.idx = ro.idx;
+  cb.wts = ro.wts;
+  cb.aslot = di.aslot;
+  cb.Yexp = m->at<float>(L.moe_y);
+  cb.part = P;
+  cb.stride = stride;
+  cb.S_sh = S_sh;
+  cb.c = W.c;
+  cb.M1_in = ret_m;
+  cb.ret = Retain{c.retain ? ret_m : nullptr, c.ret_src, c.ret_dst};
+  cb.S = S;
+  cb.g_next = g_next;
+  cb.eps = cf.rms_eps;
+  cb.Xn = m->ws + L.Xn;
+  cb.ldx = d;
+  HIPCHK(launch_moe_combine(cb, cf.dtype, st));
+  return DBT_OK;
+}
 
 dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStream_t st) {
   const dbt_config &cf = m->cfg;
@@ -369,6 +538,8 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
                        stride, g_o, st));
   }
   HIPCHK(launch_resid_norm(P, stride, S_o, d, S, W.mlp_norm, cf.rms_eps, d, cf.dtype, c.rows, Xn, d, st));
+
+  if (L.moe) return run_moe_mlp(m, l, c, st);
 
   // 4. gate/up + SwiGLU + b coupling
   WSegs gu{{W.w_gate, W.w_up, nullptr}, {f, f, 0}};
@@ -506,8 +677,9 @@ dbt_status copy_rows(float *dst, const float *src, int B, int d, hipStream_t st)
 }
 
 // Branch-only pass over all layers (ungrouped pass 2 and the boundary).
-dbt_status branch_pass(dbt_model *m, dbt_kv *kv, int B, int Bp, hipStream_t st) {
+dbt_status branch_pass(dbt_model *m, dbt_kv *kv, int B, int Bp, hipStream_t st, const dbt_step_out *out = nullptr) {
   LayerCall lc{};
+  lc.out = out;
   lc.rows = Rows{B, Bp, 1, 1};
   lc.mode = MODE_BRANCH;
   lc.retain = false;
@@ -552,9 +724,14 @@ dbt_status dbt_create(const dbt_config *cfg, const dbt_weights *w, void *workspa
   if (cfg->vocab > 0 && (!w->lm_head || !w->final_norm)) return fail(DBT_ERR_ARG, "output matrix or final norm is NULL");
   for (int l = 0; l < cfg->n_layers; ++l) {
     const dbt_layer_weights &L = w->h_layers[l];
-    if (!L.attn_norm || !L.wq || !L.wk || !L.wv || !L.wo || !L.mlp_norm || !L.w_gate || !L.w_up || !L.w_down ||
-        !L.a || !L.b || !L.c)
+    if (!L.attn_norm || !L.wq || !L.wk || !L.wv || !L.wo || !L.mlp_norm || !L.a || !L.c)
       return fail(DBT_ERR_ARG, "layer %d has a NULL parameter", l);
+    if (cfg->n_experts == 0 && (!L.w_gate || !L.w_up || !L.w_down || !L.b))
+      return fail(DBT_ERR_ARG, "layer %d has a NULL MLP parameter", l);
+    if (cfg->n_experts > 0 && (!L.router || !L.x_gate || !L.x_up || !L.x_down))
+      return fail(DBT_ERR_ARG, "layer %d has a NULL expert parameter", l);
+    if (cfg->n_experts > 0 && cfg->d_ff_shared > 0 && (!L.s_gate || !L.s_up || !L.s_down || !L.b))
+      return fail(DBT_ERR_ARG, "layer %d has a NULL shared-expert parameter", l);
   }
   dbt_model *m = new (std::nothrow) dbt_model();
   if (!m) return fail(DBT_ERR_ARG, "out of host memory");
@@ -702,6 +879,7 @@ dbt_status dbt_decode_step(dbt_model *m, dbt_kv *kv, const dbt_step_in *in, int3
   lc.prefill = false;
   lc.rows_layout = 2 * Bp;
   lc.last_norm = true;
+  lc.out = out;
   for (int l = 0; l < cf.n_layers; ++l)
     if ((s = run_layer(m, kv, l, lc, st))) return s;
   if (cf.vocab > 0 && (s = lm_head(m, rows, st))) return s;
@@ -739,13 +917,14 @@ dbt_status dbt_decode_step_ungrouped(dbt_model *m, dbt_kv *kv, const dbt_step_in
   lc.prefill = false;
   lc.rows_layout = 2 * Bp;
   lc.last_norm = true;
+  lc.out = out;
   for (int l = 0; l < cf.n_layers; ++l)
     if ((s = run_layer(m, kv, l, lc, st))) return s;
   if (cf.vocab > 0 && (s = lm_head(m, prim, st))) return s;
   // pass 2: every branch layer
   const Rows br{B, Bp, 1, 1};
   if ((s = load_inputs(m, kv, in, in->tokens, br, st))) return s;
-  if ((s = branch_pass(m, kv, B, Bp, st))) return s;
+  if ((s = branch_pass(m, kv, B, Bp, st, out))) return s;
   for (int b = 0; b < B; ++b) kv->len[b] += 1;
   if (out) {
     if ((s = readout(m, B, Bp, true, out, st))) return s;

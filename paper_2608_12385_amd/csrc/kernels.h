@@ -149,4 +149,66 @@ struct MixArgs {
 };
 hipError_t launch_mixture(const MixArgs &m, hipStream_t st);
 
+// ---- MoE (Sec. 3.2, Sec. 4.3, Sec. 5) ----
+// Per-row selections live in [2Bp][8] arrays (row = path*Bp + b, k <= 8).
+struct MoeRoute {
+  const float *Sbar;  // [2Bp][d] residual after attention (fp32)
+  const float *g;     // MLP norm gain
+  float eps;
+  int d;
+  const void *Wr;     // [E][d] bf16 router
+  int E, k1, k2, replay;
+  Rows rows;
+  int mode;
+  int *idx;           // [2Bp][8] selected experts (logit descending)
+  float *wts;         // [2Bp][8] renormalised weights
+  const int *idx1_in; // branch mode + replay: retained primary selections [*, 8]
+  int *out_idx1, *out_idx2;
+  float *out_w1, *out_w2;  // caller outputs [B][k] of this layer (may be NULL)
+  int *ret_idx;       // retained primary selections (may be NULL)
+  int ret_src, ret_dst;
+};
+struct MoeDispatch {
+  const int *idx;
+  Rows rows;
+  int k1, k2, E;
+  int *counts;   // [E]
+  int *offsets;  // [E+1]
+  int *arow;     // [A] activation row of each expert-grouped assignment
+  int *aslot;    // [2Bp][8] position of each (row, slot) in the expert-grouped order
+};
+struct MoeGemm {
+  const void *X;  // gate/up: normalized MLP inputs (gathered by arow); down: expert intermediates
+  int ldx;
+  const void *W0, *W1;  // gate/up: x_gate, x_up; down: x_down
+  int E, N, K;
+  const int *counts, *offsets, *arow;
+  void *Y;  // gate/up: [A][N] bf16 intermediates; down: [A][N] fp32 outputs
+  int ldy;
+  int mtiles;
+};
+struct MoeCombine {
+  Rows rows;
+  int mode, d, k1, k2;
+  const int *idx;
+  const float *wts;
+  const int *aslot;
+  const float *Yexp;  // [A][d]
+  const float *part;  // shared-expert down projection slabs (S_sh of them)
+  long long stride;
+  int S_sh;
+  const float *c;
+  const float *M1_in;
+  Retain ret;
+  float *S;
+  const float *g_next;
+  float eps;
+  void *Xn;
+  int ldx;
+};
+hipError_t launch_moe_route(const MoeRoute &a, hipStream_t st);
+hipError_t launch_moe_dispatch(const MoeDispatch &a, hipStream_t st);
+hipError_t launch_moe_gemm(const MoeGemm &a, bool gateup, int max_rows, hipStream_t st);
+hipError_t launch_moe_combine(const MoeCombine &a, int dtype, hipStream_t st);
+
 }  // namespace dbt
