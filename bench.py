@@ -97,6 +97,62 @@ def cpu_baseline(shape, W, h, L, nseq):
                        f"including parameter widening), {dt:.1f} s")
 
 
+def time_workload(name, steps, warmup, **shape_kw):
+    """Grouped / primary-only step times of another workload (extra report)."""
+    import torch
+    import synth
+    from paper_2608_12385_amd import Session
+    w = synth.workload(name, **shape_kw)
+    shape = w["shape"]
+    B = w["batch"]
+    if "cache_len" in w:
+        lengths = [w["cache_len"]] * B
+    else:
+        lengths = [int(x) for x in synth.make_lengths(4, B, w["len_lo"], w["len_hi"])]
+    W = synth.make_weights(shape, seed=0)
+    max_pos = max(lengths) + 16
+    sess = Session(shape, {k: W.device_array(k) for k in W.values}, max_batch=B, max_pos=max_pos,
+                   num_pages=sum((L + 16) // 16 + 1 for L in lengths) + B)
+    for b, L in enumerate(lengths):
+        (_, kb), (_, vb) = synth.make_kv(shape, 0, b, L, seed=3)
+        sess.reserve_fill(b, [kb], [vb])
+    del W
+    h = synth.make_hidden(shape, B, step=0, seed=2)
+    h1d = torch.from_numpy(np.ascontiguousarray(h[0])).cuda()
+    h2d = torch.from_numpy(np.ascontiguousarray(h[1])).cuda()
+    from paper_2608_12385_amd import binding
+    res = {}
+    for mode in ("grouped", "primary"):
+        sin = sess.step_in(B, None, h1d, h2d)
+        out, _t = sess.outputs(B, logits=False, hidden=False)
+        def one():
+            binding.dbt_decode_step(sess.model, sess.kv, sin, 1 if mode == "grouped" else 0, out, sess.stream)
+            for b, L in enumerate(lengths):
+                binding.dbt_kv_truncate(sess.kv, b, L)
+        for _ in range(warmup):
+            one()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            one()
+        torch.cuda.synchronize()
+        res[mode] = (time.perf_counter() - t0) / steps
+    sess.close()
+    d, dq, dkv = shape.d_model, shape.d_q, shape.d_kv
+    attn_w = (d * (dq + 2 * dkv) + dq * d) * 2
+    kv = sum(L + 1 for L in lengths) * 2 * dkv * 2
+    rec = {"workload": name, "batch": B, "grouped_us": res["grouped"] * 1e6, "primary_only_us": res["primary"] * 1e6,
+           "branch_overhead_pct": 100 * (res["grouped"] - res["primary"]) / res["primary"]}
+    if shape.is_moe:
+        rec["k1"], rec["k2"] = shape.top_k1, shape.top_k2
+        rec["note"] = "bytes depend on the touched experts; see profiles"
+    else:
+        mlp = 3 * d * shape.d_ff * 2
+        rec["algorithmic_MB"] = (attn_w + mlp + kv) / 1e6
+        rec["GBps"] = (attn_w + mlp + kv) / res["grouped"] / 1e9
+    return rec
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -104,6 +160,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seqs", type=int, default=16)
+    ap.add_argument("--all", action="store_true",
+                    help="also time the long-context and MoE workloads (extra fields)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build runs the decode path on a single MI355X "
@@ -180,6 +238,12 @@ def main():
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(shape, W, h, L, args.cpu_seqs)
     sess.close()
+    if args.all:
+        del W
+        extra = [time_workload("longctx_bf16", args.steps, args.warmup)]
+        for k2 in (2, 4, 8):
+            extra.append(time_workload("moe_bf16", args.steps, args.warmup, top_k2=k2))
+        line["other_workloads"] = extra
     print(json.dumps(line))
 
 

@@ -56,7 +56,7 @@ struct Layout {
   bool moe = false;
   int fe = 0, fs = 0, amax = 0;
   GemmConfig g_sgu{1, 1, 1}, g_sd{1, 1, 1};
-  size_t moe_idx = 0, moe_w = 0, moe_aslot = 0, moe_counts = 0, moe_offsets = 0, moe_arow = 0, moe_h = 0,
+  size_t moe_idx = 0, moe_logits = 0, moe_w = 0, moe_aslot = 0, moe_counts = 0, moe_offsets = 0, moe_arow = 0, moe_h = 0,
          moe_y = 0, ret_idx = 0;
   size_t rope = 0, pos = 0, S = 0, Xn = 0, Xh = 0, Q = 0, O = 0, P = 0, apart = 0, astat = 0,
          logits = 0, mstats = 0, mcand = 0, ret_q = 0, ret_h = 0, ret_m = 0, btok = 0, slast = 0,
@@ -75,7 +75,8 @@ dbt_status check_config(const dbt_config *c) {
   if (c->max_prompt > c->max_pos) return fail(DBT_ERR_SHAPE, "max_prompt > max_pos");
   if (c->n_experts > 0) {
     if (c->dtype != DBT_BF16) return fail(DBT_ERR_UNSUPPORTED, "MoE layers run in bf16 only");
-    if (c->n_experts > 256 || c->d_model > 4096) return fail(DBT_ERR_UNSUPPORTED, "MoE needs n_experts <= 256, d_model <= 4096");
+    if (c->n_experts > 256 || c->d_model > 4096 || c->d_model % 512)
+      return fail(DBT_ERR_UNSUPPORTED, "MoE needs n_experts <= 256 and d_model a multiple of 512 up to 4096");
     if (c->top_k1 < 1 || c->top_k1 > 8 || c->top_k2 < 1 || c->top_k2 > 8 || c->top_k1 > c->n_experts ||
         c->top_k2 > c->n_experts)
       return fail(DBT_ERR_ARG, "top_k1/top_k2 must be in [1, min(8, n_experts)]");
@@ -113,15 +114,15 @@ Layout make_layout(const dbt_config *c) {
   L.rows_max = std::max(L.R_max, c->max_prompt);
   L.max_in = std::max(std::max(d, dq), L.f);
   L.nqkv = dq + 2 * dkv;
-  L.g_qkv = gemm_config(L.nqkv, d, c->dtype, std::gcd(dq, dkv));
-  L.g_o = gemm_config(d, dq, c->dtype, d);
-  L.g_gu = gemm_config(2 * L.f, d, c->dtype, L.f);
-  L.g_d = gemm_config(d, L.f, c->dtype, d);
-  L.g_lm = gemm_config(std::max(c->vocab, 1), d, c->dtype, std::max(c->vocab, 1));
+  L.g_qkv = gemm_config(L.nqkv, d, c->dtype, std::gcd(dq, dkv), L.R_max);
+  L.g_o = gemm_config(d, dq, c->dtype, d, L.R_max);
+  L.g_gu = gemm_config(2 * L.f, d, c->dtype, L.f, L.R_max);
+  L.g_d = gemm_config(d, L.f, c->dtype, d, L.R_max);
+  L.g_lm = gemm_config(std::max(c->vocab, 1), d, c->dtype, std::max(c->vocab, 1), L.R_max);
   L.g_lm.S = 1;  // the logits are written in place (one slab)
   if (L.moe && L.fs > 0) {
-    L.g_sgu = gemm_config(2 * L.fs, d, c->dtype, L.fs);
-    L.g_sd = gemm_config(d, L.fs, c->dtype, d);
+    L.g_sgu = gemm_config(2 * L.fs, d, c->dtype, L.fs, L.R_max);
+    L.g_sd = gemm_config(d, L.fs, c->dtype, d, L.R_max);
   }
   const int maxpages = (c->max_pos + kPage - 1) / kPage;
   L.max_splits = (maxpages + kPagesPerSplit - 1) / kPagesPerSplit;
@@ -153,6 +154,7 @@ Layout make_layout(const dbt_config *c) {
   if (L.moe) {
     L.amax = L.rows_max * 8;
     L.moe_idx = take((size_t)L.rows_max * 8 * 4);
+    L.moe_logits = take((size_t)L.rows_max * 256 * 4);
     L.moe_w = take((size_t)L.rows_max * 8 * 4);
     L.moe_aslot = take((size_t)L.rows_max * 8 * 4);
     L.moe_counts = take((size_t)c->n_experts * 4);
@@ -345,6 +347,7 @@ dbt_status run_moe_mlp(dbt_model *m, int l, const LayerCall &c, hipStream_t st) 
   ro.replay = cf.replay;
   ro.rows = c.rows;
   ro.mode = c.mode;
+  ro.logits = m->at<float>(L.moe_logits);
   ro.idx = m->at<int>(L.moe_idx);
   ro.wts = m->at<float>(L.moe_w);
   ro.idx1_in = ret_idx;

@@ -18,14 +18,14 @@ namespace {
 
 __device__ __forceinline__ int phys_row(const Rows &r, int path, int b) { return path * r.Bp + b; }
 
-// Sum of the split-K partial slabs in split order (S <= 8).
+// Sum of the split-K partial slabs in split order (S <= 16).
 __device__ __forceinline__ float psum(const float *part, long long stride, int S, size_t idx) {
-  float v[8];
+  float v[16];
 #pragma unroll
-  for (int k = 0; k < 8; ++k) v[k] = k < S ? part[k * stride + idx] : 0.f;
+  for (int k = 0; k < 16; ++k) v[k] = k < S ? part[k * stride + idx] : 0.f;
   float s = 0.f;
 #pragma unroll
-  for (int k = 0; k < 8; ++k)
+  for (int k = 0; k < 16; ++k)
     if (k < S) s += v[k];
   return s;
 }
@@ -70,12 +70,12 @@ __device__ __forceinline__ float4 mul4(float4 a, float s, float4 g) {
   return make_float4(a.x * s * g.x, a.y * s * g.y, a.z * s * g.z, a.w * s * g.w);
 }
 __device__ __forceinline__ float4 psum4(const float *part, long long stride, int S, size_t idx4) {
-  float4 v[8];
+  float4 v[16];
 #pragma unroll
-  for (int k = 0; k < 8; ++k) v[k] = k < S ? ((const float4 *)(part + k * stride))[idx4] : make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int k = 0; k < 16; ++k) v[k] = k < S ? ((const float4 *)(part + k * stride))[idx4] : make_float4(0.f, 0.f, 0.f, 0.f);
   float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-  for (int k = 0; k < 8; ++k)
+  for (int k = 0; k < 16; ++k)
     if (k < S) s = add4(s, v[k]);
   return s;
 }

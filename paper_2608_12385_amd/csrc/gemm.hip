@@ -14,6 +14,8 @@
 #include "common.h"
 #include "kernels.h"
 
+#include <algorithm>
+
 namespace dbt {
 
 namespace {
@@ -39,8 +41,12 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(WSegs segs, int K, const uint
   const int r = lane & 15, gq = lane >> 4;
   const int split = blockIdx.y;
   const int m0 = blockIdx.z * XR;
-  const int kbeg = split * k_per_split;
-  const int nch = k_per_split / kChunk;
+  // split s covers chunks [s*NC/S, (s+1)*NC/S) of the NC = K/128 chunks
+  const int NC = K / kChunk, S = gridDim.y;
+  const int c_lo = split * NC / S, c_hi = (split + 1) * NC / S;
+  const int kbeg = c_lo * kChunk;
+  const int nch = c_hi - c_lo;
+  (void)k_per_split;
   // segment of this workgroup's rows (segment sizes are multiples of 64*RB)
   int nloc = blockIdx.x * 64 * RB;
   const uint16_t *Wseg = (const uint16_t *)segs.w[0];
@@ -236,7 +242,7 @@ __global__ __launch_bounds__(256) void k_gemm_f32(WSegs segs, int N, int K, cons
 // rows), so every output element is summed in the same order whichever paths
 // are active.
 // seg_gran: every segment boundary of the stacked matrices is a multiple of it.
-GemmConfig gemm_config(int n_full, int K, int dtype, int seg_gran) {
+GemmConfig gemm_config(int n_full, int K, int dtype, int seg_gran, int max_rows) {
   GemmConfig g{1, 1, 1};
   if (dtype != 1) return g;
   if (n_full >= 65536 && seg_gran % 256 == 0) {
@@ -244,13 +250,17 @@ GemmConfig gemm_config(int n_full, int K, int dtype, int seg_gran) {
   } else if (n_full >= 16384 && seg_gran % 128 == 0) {
     g = GemmConfig{2, 3, 1};       // MLP up projections
   } else {
-    g = GemmConfig{1, 2, 1};       // thin matrices: split the reduction
-    const int tiles = n_full / 64;
-    for (int S = 1; S <= 8; ++S) {
-      if (K % (kChunk * S) != 0 || K / S < 4 * kChunk) continue;
-      g.S = S;
-      if (tiles * S >= 448) break;
-    }
+    // thin matrices: split the reduction so ~448 workgroups run; at least 4
+    // chunks per split unless the matrix has very few row tiles; the fp32
+    // slabs of up to max_rows stacked rows never exceed the weight bytes
+    g = GemmConfig{1, 2, 1};
+    const int tiles = std::max(1, n_full / 64);  // n_full may be 0 (no output matrix)
+    const int nc = K / kChunk;
+    int S = (448 + tiles - 1) / tiles;
+    S = std::min(S, std::max(1, nc / (tiles >= 64 ? 4 : 1)));
+    S = std::min(S, std::max(1, K / (2 * std::max(max_rows, 1))));
+    S = std::min(S, 16);
+    g.S = std::max(S, 1);
   }
   return g;
 }
@@ -280,7 +290,7 @@ hipError_t launch_gemm(const WSegs &segs, int N, int K, int dtype, const void *X
     const int mb_total = (M + 15) / 16;
     const int MB = mb_total >= 8 ? 8 : mb_total;
     dim3 grid(N / (64 * g.RB), g.S, (mb_total + MB - 1) / MB);
-    const int kps = K / g.S;
+    const int kps = 0;  // splits take chunk ranges [s*NC/S, (s+1)*NC/S)
     const uint16_t *Xb = (const uint16_t *)X;
     float *rs = g.S == 1 ? row_stats : nullptr;
     switch (MB) {

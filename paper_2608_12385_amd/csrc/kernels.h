@@ -47,7 +47,7 @@ struct GemmConfig {
   int PD;  // weight prefetch depth in 128-element chunks
   int S;   // reduction splits (one fp32 output slab per split)
 };
-GemmConfig gemm_config(int n_full, int K, int dtype, int seg_gran);
+GemmConfig gemm_config(int n_full, int K, int dtype, int seg_gran, int max_rows);
 hipError_t launch_gemm(const WSegs &segs, int N, int K, int dtype, const void *X, int ldx, int M,
                        float *Y, int ldy, long long y_split_stride, const GemmConfig &g, hipStream_t st,
                        float *row_stats = nullptr);
@@ -160,6 +160,7 @@ struct MoeRoute {
   int E, k1, k2, replay;
   Rows rows;
   int mode;
+  float *logits;      // [2Bp][256] router logits (fp32)
   int *idx;           // [2Bp][8] selected experts (logit descending)
   float *wts;         // [2Bp][8] renormalised weights
   const int *idx1_in; // branch mode + replay: retained primary selections [*, 8]

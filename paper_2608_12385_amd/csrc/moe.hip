@@ -2,9 +2,9 @@
 // Sec. 4.3 Eq. (19); independent primary/branch fan-outs k1, k2, Sec. 5
 // Eq. (22)).
 //
-// 1. k_moe_route: per sequence, the router logits of its primary and branch
-//    rows from the fp32 MLP input (RMSNorm recomputed from S_bar), top-k
-//    (logit descending, ties to the lower index) and the renormalised
+// 1. k_moe_logits + k_moe_topk: the router logits of each sequence's primary
+//    and branch rows from the fp32 MLP input (RMSNorm recomputed from S_bar),
+//    top-k (logit descending, ties to the lower index) and the renormalised
 //    softmax weights of the selected experts.
 // 2. k_moe_dispatch: per expert, the list of (path, sequence, slot)
 //    assignments in (path, sequence, slot) order; each assignment's
@@ -26,61 +26,90 @@ namespace {
 
 __device__ __forceinline__ int prow(const Rows &r, int path, int b) { return path * r.Bp + b; }
 
-// Router: one workgroup per sequence, 256 threads; E <= 256, k <= 8.
-__global__ __launch_bounds__(256) void k_moe_route(MoeRoute a) {
+// Router logits: workgroup = (sequence, 16 experts).  The fp32 MLP inputs
+// RMSNorm(S_bar) * g of the active rows are rebuilt in LDS; wave w computes
+// experts 4w..4w+3 of the group for both rows, lanes covering the model
+// dimension 8 elements at a time.
+__global__ __launch_bounds__(256) void k_moe_logits(MoeRoute a) {
   __shared__ float u[2][4096 + 4];
-  __shared__ float logits[2][256];
   __shared__ float red[16];
-  const int b = blockIdx.x;
+  const int b = blockIdx.x, e0 = blockIdx.y * 16;
   const bool prim = a.mode != MODE_BRANCH, br = a.mode != MODE_PRIMARY;
   const int d = a.d, E = a.E;
-  // fp32 MLP inputs of the active rows: RMSNorm(S_bar) * g
   for (int p = 0; p < 2; ++p) {
     if ((p == 0 && !prim) || (p == 1 && !br)) continue;
-    const float *s = a.Sbar + (size_t)prow(a.rows, p, b) * d;
+    const float4 *s = (const float4 *)(a.Sbar + (size_t)prow(a.rows, p, b) * d);
     float ss = 0.f;
-    for (int i = threadIdx.x; i < d; i += blockDim.x) ss += s[i] * s[i];
+    for (int i = threadIdx.x; i < d / 4; i += blockDim.x) {
+      const float4 v = s[i];
+      ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+    }
     ss = block_sum(ss, red);
     const float inv = 1.0f / sqrtf(ss / (float)d + a.eps);
-    for (int i = threadIdx.x; i < d; i += blockDim.x) u[p][i] = s[i] * inv * a.g[i];
+    for (int i = threadIdx.x; i < d / 4; i += blockDim.x) {
+      const float4 v = s[i], g = ((const float4 *)a.g)[i];
+      u[p][4 * i + 0] = v.x * inv * g.x;
+      u[p][4 * i + 1] = v.y * inv * g.y;
+      u[p][4 * i + 2] = v.z * inv * g.z;
+      u[p][4 * i + 3] = v.w * inv * g.w;
+    }
   }
   __syncthreads();
-  // logits: wave w takes experts w, w+4, ...; lanes stride the model dimension
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int e = wave; e < E; e += 4) {
+  constexpr int MAXIT = 8;  // d <= 4096 = 8 * 64 lanes * 8 elements
+  const int nit = d / 512;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = e0 + wave * 4 + q;
+    if (e >= E) break;
     const uint16_t *wr = (const uint16_t *)a.Wr + (size_t)e * d;
+    u32x4 wv[MAXIT];
+#pragma unroll
+    for (int it = 0; it < MAXIT; ++it)
+      wv[it] = it < nit ? *(const u32x4 *)(wr + (it * 64 + lane) * 8) : u32x4{0u, 0u, 0u, 0u};
     float s0 = 0.f, s1 = 0.f;
-    for (int i = lane; i < d; i += 64) {
-      const float w = bf2f(wr[i]);
-      if (prim) s0 = fmaf(u[0][i], w, s0);
-      if (br) s1 = fmaf(u[1][i], w, s1);
+#pragma unroll
+    for (int it = 0; it < MAXIT; ++it) {
+      if (it >= nit) break;
+      const int base = (it * 64 + lane) * 8;
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        const float w0 = __uint_as_float(wv[it][h] << 16), w1 = __uint_as_float(wv[it][h] & 0xffff0000u);
+        if (prim) s0 = fmaf(u[0][base + 2 * h + 1], w1, fmaf(u[0][base + 2 * h], w0, s0));
+        if (br) s1 = fmaf(u[1][base + 2 * h + 1], w1, fmaf(u[1][base + 2 * h], w0, s1));
+      }
     }
     s0 = wave_sum(s0);
     s1 = wave_sum(s1);
     if (lane == 0) {
-      logits[0][e] = s0;
-      logits[1][e] = s1;
+      if (prim) a.logits[(size_t)prow(a.rows, 0, b) * 256 + e] = s0;
+      if (br) a.logits[(size_t)prow(a.rows, 1, b) * 256 + e] = s1;
     }
   }
-  __syncthreads();
-  if (threadIdx.x >= 64) return;
-  // top-k per path by repeated wave argmax over the E logits (lane holds e = lane + 64j)
+}
+
+// Top-k per path (logit descending, ties to the lower index) by repeated wave
+// argmax, and the renormalised softmax weights.  One wave per sequence.
+__global__ __launch_bounds__(64) void k_moe_topk(MoeRoute a) {
+  const int b = blockIdx.x, lane = threadIdx.x;
+  const bool prim = a.mode != MODE_BRANCH, br = a.mode != MODE_PRIMARY;
+  const int E = a.E;
   int sel0[8];
   for (int p = 0; p < 2; ++p) {
     if ((p == 0 && !prim) || (p == 1 && !br)) continue;
     const int k = p == 0 ? a.k1 : a.k2;
+    const float *lg = a.logits + (size_t)prow(a.rows, p, b) * 256;
     int sel[8];
     float val[8];
-    const bool replay = p == 1 && a.replay;
-    if (replay) {
+    if (p == 1 && a.replay) {
       // the branch reuses the primary's experts (wave-uniform values)
       for (int j = 0; j < k; ++j) sel[j] = prim ? sel0[j] : a.idx1_in[(size_t)b * 8 + j];
-      for (int j = 0; j < k; ++j) val[j] = logits[p][sel[j]];
+      for (int j = 0; j < k; ++j) val[j] = lg[sel[j]];
     } else {
       float v[4];
-      for (int j = 0; j < 4; ++j) {
-        const int e = lane + 64 * j;
-        v[j] = e < E ? logits[p][e] : -INFINITY;
+      for (int q = 0; q < 4; ++q) {
+        const int e = lane + 64 * q;
+        v[q] = e < E ? lg[e] : -INFINITY;
       }
       for (int j = 0; j < k; ++j) {
         float best = -INFINITY;
@@ -102,8 +131,8 @@ __global__ __launch_bounds__(256) void k_moe_route(MoeRoute a) {
     }
     if (p == 0)
       for (int j = 0; j < k; ++j) sel0[j] = sel[j];
-    // weights: softmax over the full router gathered at the selection and
-    // renormalised = exp(r_e - max_sel) / sum over the selection
+    // softmax over all experts gathered at the selection and renormalised
+    // = exp(r_e - max_sel) / sum over the selection
     float mx = -INFINITY;
     for (int j = 0; j < k; ++j) mx = fmaxf(mx, val[j]);
     float den = 0.f;
@@ -128,19 +157,93 @@ __global__ __launch_bounds__(256) void k_moe_route(MoeRoute a) {
   }
 }
 
-// One workgroup: thread e lists expert e's assignments in (path, b, slot) order.
-__global__ void k_moe_dispatch(MoeDispatch a) {
+// Entry q of the active rows' selections -> (row, slot j); padding slots
+// j >= k carry expert -1.
+__device__ __forceinline__ int moe_entry(const MoeDispatch &a, int q, int &row, int &j) {
+  const int B = a.rows.B, n = a.rows.np * B * 8;
+  const int pp = q / (B * 8), rem = q % (B * 8), b = rem / 8;
+  j = rem % 8;
+  row = prow(a.rows, a.rows.p0 + pp, b);
+  const int k = (a.rows.p0 + pp) == 0 ? a.k1 : a.k2;
+  return (q < n && j < k) ? a.idx[(size_t)row * 8 + j] : -1;
+}
+
+// Expert-grouped order as a stable counting sort of the assignments
+// (path, b, slot) by expert, for up to 64 chunks of 64 entries (one
+// workgroup).  A lane's rank among equal experts of its chunk comes from a
+// shuffle loop; per-chunk counts are prefix-summed per expert in chunk order.
+__global__ __launch_bounds__(256) void k_moe_dispatch(MoeDispatch a) {
+  constexpr int MAXC = 64;
+  __shared__ int ccnt[MAXC][257];
+  __shared__ int offs[257];
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int n = a.rows.np * a.rows.B * 8;
+  const int nch = (n + 63) / 64;
+  for (int q = t; q < nch * 257; q += blockDim.x) (&ccnt[0][0])[q] = 0;
+  __syncthreads();
+  for (int c = wave; c < nch; c += 4) {
+    int row, j;
+    const int e = moe_entry(a, c * 64 + lane, row, j);
+    int before = 0, total = 0;
+    for (int o = 0; o < 64; ++o) {
+      const int v = __shfl(e, o, 64);
+      if (v == e) {
+        ++total;
+        if (o < lane) ++before;
+      }
+    }
+    if (e >= 0 && before == 0) ccnt[c][e] = total;
+  }
+  __syncthreads();
+  if (t < a.E) {
+    int acc = 0;
+    for (int c = 0; c < nch; ++c) {
+      const int v = ccnt[c][t];
+      ccnt[c][t] = acc;
+      acc += v;
+    }
+    offs[t] = acc;  // count for now
+  }
+  __syncthreads();
+  if (t == 0) {
+    int acc = 0;
+    for (int e = 0; e < a.E; ++e) {
+      const int ce = offs[e];
+      a.counts[e] = ce;
+      a.offsets[e] = acc;
+      offs[e] = acc;
+      acc += ce;
+    }
+    a.offsets[a.E] = acc;
+  }
+  __syncthreads();
+  for (int c = wave; c < nch; c += 4) {
+    int row, j;
+    const int e = moe_entry(a, c * 64 + lane, row, j);
+    int before = 0;
+    for (int o = 0; o < 64; ++o) {
+      const int v = __shfl(e, o, 64);
+      if (v == e && o < lane) ++before;
+    }
+    if (e >= 0) {
+      const int pos = offs[e] + ccnt[c][e] + before;
+      a.arow[pos] = row;
+      a.aslot[(size_t)row * 8 + j] = pos;
+    }
+  }
+}
+
+// Same order for more than 4096 entries (long prompts): thread e scans all
+// entries in order.
+__global__ __launch_bounds__(256) void k_moe_dispatch_scan(MoeDispatch a) {
+  __shared__ int cnt[256];
   const int e = threadIdx.x;
-  __shared__ int cnt[257];
-  const int np = a.rows.np, B = a.rows.B;
+  const int n = a.rows.np * a.rows.B * 8;
   int c = 0;
   if (e < a.E) {
-    for (int pp = 0; pp < np; ++pp) {
-      const int p = a.rows.p0 + pp;
-      const int k = p == 0 ? a.k1 : a.k2;
-      for (int b = 0; b < B; ++b)
-        for (int j = 0; j < k; ++j)
-          if (a.idx[(size_t)prow(a.rows, p, b) * 8 + j] == e) ++c;
+    for (int q = 0; q < n; ++q) {
+      int row, j;
+      if (moe_entry(a, q, row, j) == e) ++c;
     }
     cnt[e] = c;
   }
@@ -149,27 +252,23 @@ __global__ void k_moe_dispatch(MoeDispatch a) {
     int acc = 0;
     for (int i = 0; i < a.E; ++i) {
       a.offsets[i] = acc;
-      acc += cnt[i];
       a.counts[i] = cnt[i];
+      const int ci = cnt[i];
+      cnt[i] = acc;
+      acc += ci;
     }
     a.offsets[a.E] = acc;
-    cnt[256] = acc;
   }
   __syncthreads();
   if (e < a.E) {
-    int pos = a.offsets[e];
-    for (int pp = 0; pp < np; ++pp) {
-      const int p = a.rows.p0 + pp;
-      const int k = p == 0 ? a.k1 : a.k2;
-      for (int b = 0; b < B; ++b)
-        for (int j = 0; j < k; ++j) {
-          const size_t r = (size_t)prow(a.rows, p, b);
-          if (a.idx[r * 8 + j] == e) {
-            a.arow[pos] = (int)r;
-            a.aslot[r * 8 + j] = pos;
-            ++pos;
-          }
-        }
+    int pos = cnt[e];
+    for (int q = 0; q < n; ++q) {
+      int row, j;
+      if (moe_entry(a, q, row, j) == e) {
+        a.arow[pos] = row;
+        a.aslot[(size_t)row * 8 + j] = pos;
+        ++pos;
+      }
     }
   }
 }
@@ -297,64 +396,84 @@ __global__ __launch_bounds__(256) void k_moe_gemm(MoeGemm a) {
 }
 
 // Routed sum (ascending expert id) + shared expert + c coupling + residual +
-// next norm.  One workgroup per sequence (both paths).
+// next norm.  One workgroup per sequence (both paths), float4 columns.
 template <typename T>
 __global__ void k_moe_combine(MoeCombine a) {
   __shared__ float red[16];
+  __shared__ int sl[2][8];
+  __shared__ float sw[2][8];
   const int b = blockIdx.x;
   const bool prim = a.mode != MODE_BRANCH, br = a.mode != MODE_PRIMARY;
-  const int d = a.d;
+  const int d = a.d, d4 = d / 4;
   const int r1 = prow(a.rows, 0, b), r2 = prow(a.rows, 1, b);
-  // selected experts of each path in ascending id order (insertion sort, k <= 8)
-  int ord[2][8];
-  for (int p = 0; p < 2; ++p) {
+  if (threadIdx.x < 2) {
+    // selected experts of this path in ascending id order (insertion sort, k <= 8)
+    const int p = threadIdx.x;
     const int k = p == 0 ? a.k1 : a.k2;
     const int r = p == 0 ? r1 : r2;
-    if ((p == 0 && !prim) || (p == 1 && !br)) continue;
-    for (int j = 0; j < k; ++j) ord[p][j] = j;
-    for (int j = 1; j < k; ++j)
-      for (int q = j; q > 0 && a.idx[(size_t)r * 8 + ord[p][q]] < a.idx[(size_t)r * 8 + ord[p][q - 1]]; --q) {
-        const int tmp = ord[p][q];
-        ord[p][q] = ord[p][q - 1];
-        ord[p][q - 1] = tmp;
+    if ((p == 0 && prim) || (p == 1 && br)) {
+      int ord[8];
+      for (int j = 0; j < k; ++j) ord[j] = j;
+      for (int j = 1; j < k; ++j)
+        for (int q = j; q > 0 && a.idx[(size_t)r * 8 + ord[q]] < a.idx[(size_t)r * 8 + ord[q - 1]]; --q) {
+          const int tmp = ord[q];
+          ord[q] = ord[q - 1];
+          ord[q - 1] = tmp;
+        }
+      for (int j = 0; j < k; ++j) {
+        sl[p][j] = a.aslot[(size_t)r * 8 + ord[j]];
+        sw[p][j] = a.wts[(size_t)r * 8 + ord[j]];
       }
+    }
   }
-  float *s1 = a.S + (size_t)r1 * d;
-  float *s2 = a.S + (size_t)r2 * d;
+  __syncthreads();
+  float4 *s1 = (float4 *)(a.S + (size_t)r1 * d);
+  float4 *s2 = (float4 *)(a.S + (size_t)r2 * d);
   const bool keep = a.ret.ptr && (a.ret.src_row < 0 || a.ret.src_row == b);
-  float *kept = keep ? a.ret.ptr + (size_t)(a.ret.src_row < 0 ? b : a.ret.dst_row) * d : nullptr;
-  for (int i = threadIdx.x; i < d; i += blockDim.x) {
-    float m1 = 0.f;
+  float4 *kept = keep ? (float4 *)(a.ret.ptr + (size_t)(a.ret.src_row < 0 ? b : a.ret.dst_row) * d) : nullptr;
+  auto routed = [&](int p, int k, int row, int i) {
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int j = 0; j < k; ++j) {
+      const float4 y = ((const float4 *)(a.Yexp + (size_t)sl[p][j] * d))[i];
+      const float w = sw[p][j];
+      acc.x += w * y.x;
+      acc.y += w * y.y;
+      acc.z += w * y.z;
+      acc.w += w * y.w;
+    }
+    float4 sh = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int q = 0; q < a.S_sh; ++q) {
+      const float4 v = ((const float4 *)(a.part + q * a.stride + (size_t)row * d))[i];
+      sh.x += v.x;
+      sh.y += v.y;
+      sh.z += v.z;
+      sh.w += v.w;
+    }
+    return make_float4(acc.x + sh.x, acc.y + sh.y, acc.z + sh.z, acc.w + sh.w);
+  };
+  for (int i = threadIdx.x; i < d4; i += blockDim.x) {
+    float4 m1;
     if (prim) {
-      float rsum = 0.f;
-      for (int j = 0; j < a.k1; ++j) {
-        const int q = ord[0][j];
-        rsum += a.wts[(size_t)r1 * 8 + q] * a.Yexp[(size_t)a.aslot[(size_t)r1 * 8 + q] * d + i];
-      }
-      float sh = 0.f;
-      for (int k = 0; k < a.S_sh; ++k) sh += a.part[k * a.stride + (size_t)r1 * d + i];
-      m1 = rsum + sh;
-      s1[i] += m1;
+      m1 = routed(0, a.k1, r1, i);
+      const float4 s = s1[i];
+      s1[i] = make_float4(s.x + m1.x, s.y + m1.y, s.z + m1.z, s.w + m1.w);
       if (keep) kept[i] = m1;
     } else {
-      m1 = a.M1_in[(size_t)b * d + i];
+      m1 = ((const float4 *)(a.M1_in + (size_t)b * d))[i];
     }
     if (br) {
-      float rsum = 0.f;
-      for (int j = 0; j < a.k2; ++j) {
-        const int q = ord[1][j];
-        rsum += a.wts[(size_t)r2 * 8 + q] * a.Yexp[(size_t)a.aslot[(size_t)r2 * 8 + q] * d + i];
-      }
-      float sh = 0.f;
-      for (int k = 0; k < a.S_sh; ++k) sh += a.part[k * a.stride + (size_t)r2 * d + i];
-      s2[i] += (rsum + sh) + a.c[i] * m1;
+      const float4 m2 = routed(1, a.k2, r2, i);
+      const float4 c = ((const float4 *)a.c)[i];
+      const float4 s = s2[i];
+      s2[i] = make_float4(s.x + (m2.x + c.x * m1.x), s.y + (m2.y + c.y * m1.y), s.z + (m2.z + c.z * m1.z),
+                          s.w + (m2.w + c.w * m1.w));
     }
   }
   if (!a.g_next) return;
   __syncthreads();
   for (int p = 0; p < 2; ++p) {
     if ((p == 0 && !prim) || (p == 1 && !br)) continue;
-    const float *x = p == 0 ? s1 : s2;
+    const float *x = (const float *)(p == 0 ? s1 : s2);
     T *out = (T *)a.Xn + (size_t)(p == 0 ? r1 : r2) * a.ldx;
     float ss = 0.f;
     for (int i = threadIdx.x; i < d; i += blockDim.x) ss += x[i] * x[i];
@@ -370,9 +489,7 @@ hipError_t launch_moe_gemm_t(const MoeGemm &a, int MB, hipStream_t st) {
   dim3 grid(a.E * (a.N / 64), 1, a.mtiles);
   switch (MB) {
     case 1: hipLaunchKernelGGL((k_moe_gemm<1, GATEUP>), grid, dim3(256), 0, st, a); break;
-    case 2: hipLaunchKernelGGL((k_moe_gemm<2, GATEUP>), grid, dim3(256), 0, st, a); break;
-    case 4: hipLaunchKernelGGL((k_moe_gemm<4, GATEUP>), grid, dim3(256), 0, st, a); break;
-    default: hipLaunchKernelGGL((k_moe_gemm<8, GATEUP>), grid, dim3(256), 0, st, a); break;
+    default: hipLaunchKernelGGL((k_moe_gemm<2, GATEUP>), grid, dim3(256), 0, st, a); break;
   }
   return hipGetLastError();
 }
@@ -380,18 +497,23 @@ hipError_t launch_moe_gemm_t(const MoeGemm &a, int MB, hipStream_t st) {
 }  // namespace
 
 hipError_t launch_moe_route(const MoeRoute &a, hipStream_t st) {
-  hipLaunchKernelGGL(k_moe_route, dim3(a.rows.B), dim3(256), 0, st, a);
+  hipLaunchKernelGGL(k_moe_logits, dim3(a.rows.B, (a.E + 15) / 16), dim3(256), 0, st, a);
+  hipLaunchKernelGGL(k_moe_topk, dim3(a.rows.B), dim3(64), 0, st, a);
   return hipGetLastError();
 }
 
 hipError_t launch_moe_dispatch(const MoeDispatch &a, hipStream_t st) {
-  hipLaunchKernelGGL(k_moe_dispatch, dim3(1), dim3(256), 0, st, a);
+  if (a.rows.np * a.rows.B * 8 <= 64 * 64)
+    hipLaunchKernelGGL(k_moe_dispatch, dim3(1), dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL(k_moe_dispatch_scan, dim3(1), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
+// 32-row activation tiles: an expert usually gets a handful of rows; the
+// rare crowded expert takes more tiles (its weights are then read again).
 hipError_t launch_moe_gemm(const MoeGemm &a, bool gateup, int max_rows, hipStream_t st) {
-  const int mb = (max_rows + 15) / 16;
-  const int MB = mb >= 8 ? 8 : mb > 2 ? 4 : mb;
+  const int MB = max_rows > 16 ? 2 : 1;
   MoeGemm b = a;
   b.mtiles = (max_rows + 16 * MB - 1) / (16 * MB);
   return gateup ? launch_moe_gemm_t<true>(b, MB, st) : launch_moe_gemm_t<false>(b, MB, st);

@@ -64,6 +64,12 @@ def test_config_checks():
     # bf16 shapes the kernels support
     ok = _cfg(dtype=B.DBT_BF16, d_model=512, n_q_heads=4, n_kv_heads=2, head_dim=128, d_ff=1024, vocab=512)
     assert B.dbt_workspace_bytes(ok) > 0
+    # a layer stack without output matrix or embeddings (hidden states in and
+    # out), at several batch caps: sizing must not depend on a nonzero vocab
+    for mb in (1, 3, 64):
+        hid = _cfg(dtype=B.DBT_BF16, d_model=512, n_q_heads=4, n_kv_heads=2, head_dim=128, d_ff=1024,
+                   vocab=0, has_embeddings=0, max_prompt=0, max_batch=mb)
+        assert B.dbt_workspace_bytes(hid) > 0, mb
 
 
 def test_create_rejects_null_and_misaligned():
