@@ -2,9 +2,9 @@
 // the two paths' residual rows are stacked so each weight tile is read once
 // for both; Sec. 4.5, Eq. (20): the step is bound by weight + KV traffic).
 //
-// bf16 weights: MFMA v_mfma_f32_16x16x32_bf16.  A workgroup owns 64 weight
-// rows and up to 128 activation rows; its four waves split the reduction
-// dimension in 128-wide chunks and are summed through LDS in a fixed order.
+// bf16 weights: MFMA v_mfma_f32_16x16x32_bf16.  A workgroup owns 64*RB weight
+// rows and up to 128 activation rows; each wave owns 16*RB of the weight rows
+// and accumulates over the whole reduction range in 128-wide chunks.
 // Optional split of the reduction across workgroups (grid.y) writes one fp32
 // slab per split; the consumer kernel adds the slabs in split order.  The
 // per-element arithmetic never depends on how many rows are stacked, so the
@@ -27,16 +27,28 @@ constexpr int kLdsRow = kChunk + 8;  // padded LDS row of a staged activation ch
 // owns rows w*16*RB .. +16*RB and runs the whole reduction range of its split.
 // The activation chunk [16*MB rows][128] is staged once per workgroup in LDS
 // (contiguous loads) and read by the four waves in MFMA operand layout.
-// Weight loads are issued PD chunks ahead into a register ring; the
-// activation chunks use an LDS ring of the same depth.
+//
+// Pipeline: the weights and the activations of chunk c+PD are loaded together
+// while chunk c is multiplied; the activation chunk c+1, loaded PD chunks
+// earlier, is then written to the other of two LDS slots.  Vector loads
+// complete in issue order, so that write only waits for loads that are
+// already consumed and the PD chunks of weights behind it stay in flight.
+// Loads are never predicated (rows past M re-read row M-1, chunks past the
+// end re-read the last one), and the loop body always runs PD chunks, so the
+// compiler's wait counts stay exact across the loop's back edge.
+//
+// Each workgroup starts at its own chunk of the split, (tile * 7) mod chunks,
+// and wraps around: workgroups running at the same time then read different
+// column ranges of their rows instead of all hitting the same few memory
+// channels (row strides are powers of two).  The order is a function of the
+// row tile and the split only.
 template <int MB, int RB, int PD>
 __global__ __launch_bounds__(256) void k_gemm_bf16(WSegs segs, int K, const uint16_t *__restrict__ X, int ldx,
                                                    int M, float *__restrict__ Y, int ldy, long long y_split_stride,
-                                                   int k_per_split, float *__restrict__ row_stats) {
+                                                   float *__restrict__ row_stats) {
   constexpr int XR = 16 * MB;
-  constexpr int PIECES = XR * (kChunk / 8);  // 16-byte pieces of one activation chunk
-  constexpr int PPT = (PIECES + 255) / 256;
-  __shared__ uint16_t xs[PD][XR * kLdsRow];
+  constexpr int PPT = MB;  // 16-byte pieces of one activation chunk per thread (XR * 16 / 256)
+  __shared__ uint16_t xs[2][XR * kLdsRow];
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int r = lane & 15, gq = lane >> 4;
   const int split = blockIdx.y;
@@ -46,7 +58,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(WSegs segs, int K, const uint
   const int c_lo = split * NC / S, c_hi = (split + 1) * NC / S;
   const int kbeg = c_lo * kChunk;
   const int nch = c_hi - c_lo;
-  (void)k_per_split;
+  const int crot = (int)(blockIdx.x * 7u % (unsigned)nch);
   // segment of this workgroup's rows (segment sizes are multiples of 64*RB)
   int nloc = blockIdx.x * 64 * RB;
   const uint16_t *Wseg = (const uint16_t *)segs.w[0];
@@ -63,6 +75,14 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(WSegs segs, int K, const uint
   const uint16_t *wrow[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) wrow[rb] = Wseg + (size_t)(nw + rb * 16 + r) * K + kbeg + gq * 8;
+  const uint16_t *xsrc[PPT];
+  int xdst[PPT];
+#pragma unroll
+  for (int j = 0; j < PPT; ++j) {
+    const int p = t + 256 * j, row = p >> 4, col = (p & 15) * 8;
+    xsrc[j] = X + (size_t)min(m0 + row, M - 1) * ldx + kbeg + col;
+    xdst[j] = row * kLdsRow + col;
+  }
 
   floatx4 acc[RB][MB];
 #pragma unroll
@@ -70,66 +90,54 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(WSegs segs, int K, const uint
 #pragma unroll
     for (int cb = 0; cb < MB; ++cb) acc[rb][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  u32x4 a[PD][RB][4];
-  u32x4 stage[PPT];
-  auto wload = [&](int slot, int c) {
+  u32x4 a[PD][RB][4], stg[PD][PPT];
+  auto load = [&](int slot, int c) {  // logical chunk c (clamped) of this workgroup's rotated order
+    c = min(c, nch - 1) + crot;
+    c = c >= nch ? c - nch : c;
+    const int ko = c * kChunk;
+#pragma unroll
+    for (int j = 0; j < PPT; ++j) stg[slot][j] = *(const u32x4 *)(xsrc[j] + ko);
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-      for (int s = 0; s < 4; ++s) a[slot][rb][s] = *(const u32x4 *)(wrow[rb] + c * kChunk + s * 32);
+      for (int s = 0; s < 4; ++s) a[slot][rb][s] = *(const u32x4 *)(wrow[rb] + ko + s * 32);
   };
-  auto xload = [&](int c) {
+  auto xstore = [&](int lds, int slot) {
 #pragma unroll
-    for (int j = 0; j < PPT; ++j) {
-      const int p = t + 256 * j;
-      const int row = p >> 4, col = (p & 15) * 8;
-      const bool ok = p < PIECES && m0 + row < M;
-      stage[j] = ok ? *(const u32x4 *)(X + (size_t)(m0 + row) * ldx + kbeg + c * kChunk + col)
-                    : u32x4{0u, 0u, 0u, 0u};
-    }
+    for (int j = 0; j < PPT; ++j) *(u32x4 *)(&xs[lds][xdst[j]]) = stg[slot][j];
   };
-  auto xstore = [&](int slot) {
+  auto step = [&](int c, int u) {  // multiply chunk c (ring slot u), refill, stage chunk c+1
+    const uint16_t *xl = xs[c & 1];
 #pragma unroll
-    for (int j = 0; j < PPT; ++j) {
-      const int p = t + 256 * j;
-      if (p < PIECES) *(u32x4 *)(&xs[slot][(p >> 4) * kLdsRow + (p & 15) * 8]) = stage[j];
+    for (int s = 0; s < 4; ++s) {
+      u32x4 bx[MB];
+#pragma unroll
+      for (int cb = 0; cb < MB; ++cb) bx[cb] = *(const u32x4 *)(&xl[(cb * 16 + r) * kLdsRow + s * 32 + gq * 8]);
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int cb = 0; cb < MB; ++cb)
+          acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a[u][rb][s]),
+                                                                __builtin_bit_cast(bf16x8, bx[cb]), acc[rb][cb], 0, 0,
+                                                                0);
     }
+    load(u, c + PD);
+    xstore((c + 1) & 1, (u + 1) % PD);
+    __syncthreads();
   };
 
 #pragma unroll
-  for (int u = 0; u < PD; ++u)
-    if (u < nch) {
-      xload(u);
-      xstore(u);
-      wload(u, u);
-    }
+  for (int u = 0; u < PD; ++u) load(u, u);
+  xstore(0, 0);
   __syncthreads();
-  for (int c0 = 0; c0 < nch; c0 += PD) {
+  int c0 = 0;
+  for (; c0 + PD <= nch; c0 += PD) {
 #pragma unroll
-    for (int u = 0; u < PD; ++u) {
-      const int c = c0 + u;
-      if (c < nch) {
-        const bool more = c + PD < nch;
-        if (more) xload(c + PD);
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-          u32x4 bx[MB];
-#pragma unroll
-          for (int cb = 0; cb < MB; ++cb) bx[cb] = *(const u32x4 *)(&xs[u][(cb * 16 + r) * kLdsRow + s * 32 + gq * 8]);
-#pragma unroll
-          for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-            for (int cb = 0; cb < MB; ++cb)
-              acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a[u][rb][s]),
-                                                                    __builtin_bit_cast(bf16x8, bx[cb]), acc[rb][cb], 0,
-                                                                    0, 0);
-        }
-        if (more) wload(u, c + PD);
-        __syncthreads();
-        if (more) xstore(u);
-      }
-    }
+    for (int u = 0; u < PD; ++u) step(c0 + u, u);
   }
+#pragma unroll
+  for (int u = 0; u + 1 < PD; ++u)
+    if (c0 + u < nch) step(c0 + u, u);
   // lane holds D[n = rb*16 + 4*gq + i][m = cb*16 + r]: Y[m][n .. n+3]
   if (row_stats) {
     // Softmax statistics of each activation row over this workgroup's 64*RB
@@ -248,18 +256,17 @@ GemmConfig gemm_config(int n_full, int K, int dtype, int seg_gran, int max_rows)
   if (n_full >= 65536 && seg_gran % 256 == 0) {
     g = GemmConfig{4, 1, 1};       // output-matrix shapes: 256 rows per workgroup
   } else if (n_full >= 16384 && seg_gran % 128 == 0) {
-    g = GemmConfig{2, 3, 1};       // MLP up projections
+    g = GemmConfig{2, 2, 1};       // MLP up projections
   } else {
-    // thin matrices: split the reduction so ~448 workgroups run; at least 4
-    // chunks per split unless the matrix has very few row tiles; the fp32
-    // slabs of up to max_rows stacked rows never exceed the weight bytes
+    // thin matrices: split the reduction so about one workgroup per compute
+    // unit runs; the fp32 slabs of up to max_rows stacked rows never exceed
+    // the weight bytes, and every split keeps at least one chunk
     g = GemmConfig{1, 2, 1};
     const int tiles = std::max(1, n_full / 64);  // n_full may be 0 (no output matrix)
     const int nc = K / kChunk;
-    int S = (448 + tiles - 1) / tiles;
-    S = std::min(S, std::max(1, nc / (tiles >= 64 ? 4 : 1)));
+    int S = (256 + tiles / 2) / tiles;
     S = std::min(S, std::max(1, K / (2 * std::max(max_rows, 1))));
-    S = std::min(S, 16);
+    S = std::min({S, 16, std::max(nc, 1)});
     g.S = std::max(S, 1);
   }
   return g;
@@ -268,14 +275,13 @@ GemmConfig gemm_config(int n_full, int K, int dtype, int seg_gran, int max_rows)
 namespace {
 template <int MB>
 void launch_mb(const GemmConfig &g, dim3 grid, hipStream_t st, const WSegs &segs, int K, const uint16_t *X, int ldx,
-               int M, float *Y, int ldy, long long yss, int kps, float *rs) {
+               int M, float *Y, int ldy, long long yss, float *rs) {
   if (g.RB == 4)
-    hipLaunchKernelGGL((k_gemm_bf16<MB, 4, 1>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, kps, rs);
+    hipLaunchKernelGGL((k_gemm_bf16<MB, 4, 1>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs);
   else if (g.RB == 2)
-    hipLaunchKernelGGL((k_gemm_bf16<MB, 2, (MB > 4 ? 2 : 3)>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss,
-                       kps, rs);
+    hipLaunchKernelGGL((k_gemm_bf16<MB, 2, 2>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs);
   else
-    hipLaunchKernelGGL((k_gemm_bf16<MB, 1, 2>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, kps, rs);
+    hipLaunchKernelGGL((k_gemm_bf16<MB, 1, 2>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs);
 }
 }  // namespace
 
@@ -290,18 +296,17 @@ hipError_t launch_gemm(const WSegs &segs, int N, int K, int dtype, const void *X
     const int mb_total = (M + 15) / 16;
     const int MB = mb_total >= 8 ? 8 : mb_total;
     dim3 grid(N / (64 * g.RB), g.S, (mb_total + MB - 1) / MB);
-    const int kps = 0;  // splits take chunk ranges [s*NC/S, (s+1)*NC/S)
     const uint16_t *Xb = (const uint16_t *)X;
     float *rs = g.S == 1 ? row_stats : nullptr;
     switch (MB) {
-      case 1: launch_mb<1>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps, rs); break;
-      case 2: launch_mb<2>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps, rs); break;
-      case 3: launch_mb<3>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps, rs); break;
-      case 4: launch_mb<4>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps, rs); break;
-      case 5: launch_mb<5>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps, rs); break;
-      case 6: launch_mb<6>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps, rs); break;
-      case 7: launch_mb<7>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps, rs); break;
-      default: launch_mb<8>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, kps, rs); break;
+      case 1: launch_mb<1>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, rs); break;
+      case 2: launch_mb<2>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, rs); break;
+      case 3: launch_mb<3>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, rs); break;
+      case 4: launch_mb<4>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, rs); break;
+      case 5: launch_mb<5>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, rs); break;
+      case 6: launch_mb<6>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, rs); break;
+      case 7: launch_mb<7>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, rs); break;
+      default: launch_mb<8>(g, grid, st, segs, K, Xb, ldx, M, Y, ldy, y_split_stride, rs); break;
     }
   } else {
     dim3 grid((N + 63) / 64, (M + 15) / 16);
