@@ -4,14 +4,19 @@
 // A workgroup owns one (sequence, KV head, split of the cache).  Its query
 // rows are the G primary heads of that KV head followed by the G branch heads
 // (2G <= 16), so each K/V page is read once for both paths.  Scores and the
-// value sum run on MFMA (v_mfma_f32_16x16x32_bf16): scores S = K Q^T with the
-// 16 positions of a page as rows; the output is accumulated transposed,
-// O^T = V^T P^T, with V pages stored dim-major so the operand loads are
-// contiguous and the probabilities never leave the lane that computed them.
-// Softmax is online per split (base-2 exponent, running max and sum), the
-// four waves of a workgroup merge through LDS, and a combine kernel merges
-// the splits in split order.  The split size is fixed (pages_per_split), so
-// a row's result depends only on its own query and the cache.
+// value sum run on MFMA (v_mfma_f32_16x16x32_bf16), one pair of 16-position
+// pages per step.  Scores are computed as S = K Q^T by two MFMAs whose 16
+// "rows" are a chosen set of positions of the pair: the first covers
+// positions 8h+0..3 of page p in rows 4(2p+h)+i, the second positions
+// 8h+4..7, so after both each lane (query r, group 2p+h) holds the scores of
+// eight consecutive positions 8h..8h+7 of page p.  That is exactly the
+// operand layout of the value MFMA O^T = V^T P^T with reduction index
+// k = 8(2p+h) + j, and with V pages stored dim-major each lane loads its V^T
+// operand as one 16-byte piece.  Softmax is online per split (base-2
+// exponent, running max and sum), the four waves of a workgroup merge
+// through LDS, and a combine kernel merges the splits in split order.  The
+// split size is fixed (pages_per_split), so a row's result depends only on
+// its own query and the cache.
 #include "common.h"
 #include "kernels.h"
 
@@ -25,16 +30,17 @@ __device__ __forceinline__ uint32_t pack2(float lo, float hi) {
   return (uint32_t)f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
 }
 
-// Zero the bf16 halves of v whose slot (4*gq + k, k = 0..3) is >= nvalid.
-__device__ __forceinline__ u32x2 mask_slots(u32x2 v, int first_slot, int nvalid) {
-  if (first_slot + 0 >= nvalid) v[0] &= 0xffff0000u;
-  if (first_slot + 1 >= nvalid) v[0] &= 0x0000ffffu;
-  if (first_slot + 2 >= nvalid) v[1] &= 0xffff0000u;
-  if (first_slot + 3 >= nvalid) v[1] &= 0x0000ffffu;
+// Zero the bf16 lanes of v (positions first .. first+7) at positions >= nvalid.
+__device__ __forceinline__ u32x4 mask8(u32x4 v, int first, int nvalid) {
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    if (first + 2 * w >= nvalid) v[w] &= 0xffff0000u;
+    if (first + 2 * w + 1 >= nvalid) v[w] &= 0x0000ffffu;
+  }
   return v;
 }
 
-// Requires d_h == 128 and np*G <= 16.
+// Requires d_h == 128, np*G <= 16 and pages_per_split <= 64.
 __global__ __launch_bounds__(256) void k_attn_decode_bf16(AttnArgs a) {
   constexpr int DH = 128;
   const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
@@ -50,6 +56,9 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(AttnArgs a) {
   const int nrows = a.rows.np * G;
   const int dq = a.n_q * DH;
   const float scale = kLog2e / sqrtf((float)DH);
+  // page ids of the split: lane i holds page pb + i
+  const int *ptab = a.kv.page_table + (size_t)b * a.kv.mpps;
+  const int myid = (pb + lane < pe) ? ptab[pb + lane] : 0;
 
   // Query operand: lane (query r, group gq) holds Q[r][s*32 + gq*8 .. +8].
   u32x4 qf[4];
@@ -69,53 +78,53 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(AttnArgs a) {
 
   const uint16_t *kbase = (const uint16_t *)a.kv.k;
   const uint16_t *vbase = (const uint16_t *)a.kv.v;
-  const int *ptab = a.kv.page_table + (size_t)b * a.kv.mpps;
 
   float m_run = -INFINITY, l_run = 0.f;
   floatx4 acc[8];
 #pragma unroll
   for (int c = 0; c < 8; ++c) acc[c] = floatx4{0.f, 0.f, 0.f, 0.f};
 
+  // Score-MFMA row r of this lane: page r/8, positions 8*((r/4)&1) + (r&3)
+  // (first MFMA) and +4 (second).  Value operand of this lane: page gq/2,
+  // positions 8*(gq&1) .. +7.
+  const int kpage = r >> 3, kpos = 8 * ((r >> 2) & 1) + (r & 3);
+  const int vpage = gq >> 1, vpos = 8 * (gq & 1);
   const int npairs = (pe - pb + 1) >> 1;
   for (int q = wave; q < npairs; q += 4) {
-    const int pg0 = pb + 2 * q;
-    const bool has1 = pg0 + 1 < pe;
-    const int phys0 = ptab[pg0];
-    const int phys1 = has1 ? ptab[pg0 + 1] : phys0;
-    const uint16_t *k0 = kbase + ((size_t)phys0 * n_kv + g) * 16 * DH;
-    const uint16_t *k1 = kbase + ((size_t)phys1 * n_kv + g) * 16 * DH;
-    const uint16_t *v0 = vbase + ((size_t)phys0 * n_kv + g) * DH * 16;
-    const uint16_t *v1 = vbase + ((size_t)phys1 * n_kv + g) * DH * 16;
-
-    u32x4 kf0[4], kf1[4];
+    const int pg0 = pb + 2 * q;                 // first page of the pair
+    const int last = pe - pb - 1;               // a missing second page re-reads the first (masked)
+    const int phys0 = __shfl(myid, 2 * q, 64);
+    const int phys1 = __shfl(myid, min(2 * q + 1, last), 64);
+    const int kphys = kpage ? phys1 : phys0;
+    const int vphys = vpage ? phys1 : phys0;
+    const uint16_t *kp = kbase + ((size_t)kphys * n_kv + g) * 16 * DH + kpos * DH + gq * 8;
+    const uint16_t *vp = vbase + ((size_t)vphys * n_kv + g) * DH * 16 + r * 16 + vpos;
+    u32x4 ka[4], kb[4], vf[8];
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-      kf0[s] = *(const u32x4 *)(k0 + r * DH + s * 32 + gq * 8);
-      kf1[s] = has1 ? *(const u32x4 *)(k1 + r * DH + s * 32 + gq * 8) : u32x4{0u, 0u, 0u, 0u};
+      ka[s] = *(const u32x4 *)(kp + s * 32);
+      kb[s] = *(const u32x4 *)(kp + 4 * DH + s * 32);
     }
-    u32x2 vf0[8], vf1[8];
 #pragma unroll
-    for (int c = 0; c < 8; ++c) {
-      vf0[c] = *(const u32x2 *)(v0 + (c * 16 + r) * 16 + gq * 4);
-      vf1[c] = has1 ? *(const u32x2 *)(v1 + (c * 16 + r) * 16 + gq * 4) : u32x2{0u, 0u};
-    }
+    for (int c = 0; c < 8; ++c) vf[c] = *(const u32x4 *)(vp + c * 16 * 16);
 
     floatx4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kf0[s]),
+      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ka[s]),
                                                    __builtin_bit_cast(bf16x8, qf[s]), s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kf1[s]),
+      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kb[s]),
                                                    __builtin_bit_cast(bf16x8, qf[s]), s1, 0, 0, 0);
     }
-    // lane holds scores of slots 4*gq+i (i = 0..3) of both pages for query r
-    const int nv0 = min(16, len - pg0 * 16);
-    const int nv1 = has1 ? min(16, len - (pg0 + 1) * 16) : 0;
+    // lane (query r, gq) now holds positions vpos + 0..3 (s0) and vpos + 4..7
+    // (s1) of page vpage of the pair
+    // valid positions of that page (<= 0: none; a page past the split's end is not this pair's)
+    const int nv = pg0 + vpage < pe ? min(16, len - (pg0 + vpage) * 16) : 0;
     float sc[8];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      sc[i] = (4 * gq + i < nv0) ? s0[i] * scale : -INFINITY;
-      sc[4 + i] = (4 * gq + i < nv1) ? s1[i] * scale : -INFINITY;
+      sc[i] = (vpos + i < nv) ? s0[i] * scale : -INFINITY;
+      sc[4 + i] = (vpos + 4 + i < nv) ? s1[i] * scale : -INFINITY;
     }
     float mt = sc[0];
 #pragma unroll
@@ -123,7 +132,6 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(AttnArgs a) {
     mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
     mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
     const float m_new = fmaxf(m_run, mt);
-    const float corr = exp2f(m_run - m_new);
     float p[8];
     float ps = 0.f;
 #pragma unroll
@@ -131,18 +139,26 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(AttnArgs a) {
       p[i] = exp2f(sc[i] - m_new);
       ps += p[i];
     }
-    l_run = l_run * corr + ps;
+    // rescale the running sums only when some row's max grew (wave-uniform
+    // test; a factor of exactly 1 otherwise)
+    if (__any(m_new > m_run)) {
+      const float corr = exp2f(m_run - m_new);
+      l_run *= corr;
+#pragma unroll
+      for (int c = 0; c < 8; ++c) acc[c] = acc[c] * corr;
+    }
+    l_run += ps;
     m_run = m_new;
     const u32x4 pf = u32x4{pack2(p[0], p[1]), pack2(p[2], p[3]), pack2(p[4], p[5]), pack2(p[6], p[7])};
+    // positions past the end may hold stale values: zero them (0 * NaN)
+    if (__any(nv < 16)) {
 #pragma unroll
-    for (int c = 0; c < 8; ++c) {
-      const u32x2 lo = mask_slots(vf0[c], 4 * gq, nv0);
-      const u32x2 hi = mask_slots(vf1[c], 4 * gq, nv1);
-      const u32x4 vv = u32x4{lo[0], lo[1], hi[0], hi[1]};
-      acc[c] = acc[c] * corr;
-      acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vv),
-                                                       __builtin_bit_cast(bf16x8, pf), acc[c], 0, 0, 0);
+      for (int c = 0; c < 8; ++c) vf[c] = mask8(vf[c], vpos, nv);
     }
+#pragma unroll
+    for (int c = 0; c < 8; ++c)
+      acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vf[c]),
+                                                       __builtin_bit_cast(bf16x8, pf), acc[c], 0, 0, 0);
   }
   l_run += __shfl_xor(l_run, 16, 64);
   l_run += __shfl_xor(l_run, 32, 64);
@@ -184,7 +200,7 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(AttnArgs a) {
 
 // fp32 cache: scores in LDS, exact two-pass softmax over the split.
 __global__ __launch_bounds__(256) void k_attn_decode_f32(AttnArgs a) {
-  constexpr int MAXP = 512;  // positions per split (pages_per_split * 16)
+  constexpr int MAXP = 1024;  // positions per split (pages_per_split * 16, pages_per_split <= 64)
   __shared__ float qs[16][128];
   __shared__ float sc[16][MAXP];
   __shared__ float red[16];
@@ -363,6 +379,8 @@ __global__ __launch_bounds__(256) void k_attn_prefill(const float *Q, int ldq, K
 }  // namespace
 
 hipError_t launch_attn_decode(const AttnArgs &a, hipStream_t st) {
+  // both kernels hold one page id per lane / 16 positions per page in LDS
+  if (a.pages_per_split < 1 || a.pages_per_split > 64) return hipErrorInvalidValue;
   dim3 grid(a.max_splits, a.kv.n_kv, a.rows.B);
   if (a.dtype == 1)
     hipLaunchKernelGGL(k_attn_decode_bf16, grid, dim3(256), 0, st, a);

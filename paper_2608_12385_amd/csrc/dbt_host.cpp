@@ -42,7 +42,7 @@ dbt_status fail(dbt_status s, const char *fmt, ...) {
   } while (0)
 
 constexpr int kPage = 16;
-constexpr int kPagesPerSplit = 32;  // attention split: 512 positions
+constexpr int kPagesPerSplit = 64;  // attention split: 1024 positions (at most 64: one page id per lane)
 constexpr int kMixChunk = 4096;
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }

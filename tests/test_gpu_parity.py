@@ -115,21 +115,26 @@ def sess_pages(sess, b):
 # layer-only bf16 model with hidden-state inputs and a ragged cache
 # ----------------------------------------------------------------------------
 
-def _layer_case(lengths, steps=2, vocab=512, seed_h=2):
+def _layer_case(lengths, steps=2, vocab=512, seed_h=2, poison=0):
     shape = _small_bf16(n_layers=1, vocab=vocab, has_embeddings=False, coupling_std=0.5)
     W = synth.make_weights(shape, seed=0)
     B = len(lengths)
     orc = Oracle(shape, W.values)
     sess = make_session(shape, W, max_batch=B, max_pos=max(lengths) + steps + 1)
-    sess.k_pages.zero_()
-    sess.v_pages.zero_()
+    sess.k_pages.fill_(poison)
+    sess.v_pages.fill_(poison)
     fill_cache(sess, orc, shape, lengths)
     return shape, W, orc, sess
 
 
-@pytest.mark.parametrize("lengths", [[1, 15, 16, 17, 600], [511, 512, 513]])
-def test_layer_bf16_ragged_cache(lengths):
-    shape, W, orc, sess = _layer_case(lengths)
+# The cache is read in splits of 1024 positions: lengths at and around split
+# boundaries, a last split of one page, and (second set) page bytes poisoned
+# with 0xFF (bf16 0xFFFF, a NaN) so slots past each sequence's end hold NaN:
+# they must be masked, not multiplied by a zero probability.
+@pytest.mark.parametrize("lengths,poison", [([1, 15, 16, 17, 600], 0), ([511, 512, 513], 0),
+                                            ([1023, 1024, 1025, 2063], 0xFF), ([3, 1041, 17], 0xFF)])
+def test_layer_bf16_ragged_cache(lengths, poison):
+    shape, W, orc, sess = _layer_case(lengths, poison=poison)
     B = len(lengths)
     for step in range(2):
         h = synth.make_hidden(shape, B, step=step, seed=2)
