@@ -31,7 +31,95 @@ if ROOT not in sys.path:
 import numpy as np  # noqa: E402
 
 HBM_PEAK_GBPS = 8000.0
+CALIB_BYTES = 256 << 20   # plain device copy used to calibrate the memory counters
 METRIC = "grouped decode step µs + tokens/s; HBM GB/s vs peak; branch overhead % vs primary-only"
+
+
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "lmhead_traffic_layer8b_b32_l4096.md")
+GEMM_SOURCE = os.path.join(ROOT, "paper_2608_12385_amd", "csrc", "gemm.hip")
+LMHEAD_KERNEL = "k_gemm_bf16<4, 4, 1>"   # grouped step: 64 stacked rows, 4 row blocks per wave
+
+
+def _sha256(path):
+    import hashlib
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def _db(path):
+    import glob
+    import sqlite3
+    dbs = [path] if path.endswith(".db") else sorted(glob.glob(os.path.join(path, "**", "*.db"), recursive=True))
+    if not dbs:
+        raise SystemExit(f"no rocpd database under {path}")
+    return sqlite3.connect(dbs[0])
+
+
+def _short(name):
+    name = name.replace("dbt::(anonymous namespace)::", "")
+    return name.split("(")[0].replace("void ", "")
+
+
+def kernel_table(path):
+    """Markdown table of per-kernel durations from a rocprofv3 --kernel-trace database."""
+    c = _db(path)
+    rows = c.execute(
+        "select name, grid_x / workgroup_x, grid_y, grid_z, count(*), "
+        "avg(end - start), min(end - start), max(end - start) from kernels "
+        "group by name, grid_x, grid_y, grid_z order by count(*) * avg(end - start) desc"
+    ).fetchall()
+    out = ["| kernel | grid | launches | avg us | min us | max us |", "|---|---|---|---|---|---|"]
+    for name, gx, gy, gz, n, avg, mn, mx in rows:
+        out.append(f"| {_short(name)} | {gx} x {gy} x {gz} | {n} | {avg / 1e3:.2f} | {mn / 1e3:.2f} | {mx / 1e3:.2f} |")
+    return "\n".join(out)
+
+
+def _counter(path, counter):
+    c = _db(path)
+    return c.execute("select kernel_name, value from counters_collection where counter_name = ? order by dispatch_id",
+                     (counter,)).fetchall()
+
+
+def traffic_summary(fetch_path, write_path):
+    """Memory-counter traffic of the output-matrix projection, calibrated on a plain device copy.
+
+    Each counter (KiB per dispatch) is scaled by known bytes / counter reading of
+    the 256 MiB device-to-device copies bench.py --calib-copy launches (the only
+    copies of that size in the run)."""
+    lines = []
+    res = {}
+    for counter, path in (("FETCH_SIZE", fetch_path), ("WRITE_SIZE", write_path)):
+        vals = _counter(path, counter)
+        calib = [v for k, v in vals if "copyBuffer" in k and v > 0.4 * CALIB_BYTES / 1024]
+        if len(calib) != 3:
+            raise SystemExit(f"{counter}: expected 3 calibration copies, found {len(calib)}")
+        factor = (CALIB_BYTES / 1024) / (sum(calib) / len(calib))
+        lm = [v for k, v in vals if _short(k) == LMHEAD_KERNEL]
+        if not lm:
+            raise SystemExit(f"{counter}: no {LMHEAD_KERNEL} dispatches")
+        kib = sum(lm) / len(lm)
+        res[counter] = kib * 1024 * factor
+        lines.append(f"| {counter} | {sum(calib) / len(calib):.1f} | {factor:.4f} | {len(lm)} | {kib:.1f} | "
+                     f"{kib * 1024 * factor / 1e6:.1f} |")
+    total = res["FETCH_SIZE"] + res["WRITE_SIZE"]
+    head = ["| counter | calibration copy reads (KiB, 256 MiB moved) | scale | LM-head dispatches | "
+            "LM-head avg (KiB) | LM-head scaled (MB) |", "|---|---|---|---|---|---|"]
+    tail = ["", f"lmhead_traffic_bytes_per_launch: {int(round(total))}",
+            f"gemm_source_sha256: {_sha256(GEMM_SOURCE)}"]
+    return "\n".join(head + lines + tail)
+
+
+def recorded_traffic():
+    """Counter-derived HBM bytes per launch of the output-matrix projection, or
+    None when no record exists or the projection kernel changed since."""
+    try:
+        text = open(TRAFFIC_PROFILE).read()
+    except OSError:
+        return None
+    kv = dict(l.split(": ", 1) for l in text.splitlines() if l.startswith(("lmhead_traffic", "gemm_source")))
+    if kv.get("gemm_source_sha256") != _sha256(GEMM_SOURCE):
+        return None
+    return int(kv["lmhead_traffic_bytes_per_launch"])
 
 
 def algorithmic_bytes(shape, B, L):
@@ -73,9 +161,11 @@ def time_mode(sess, B, L, h1d, h2d, mode, steps, warmup):
     return (t1 - t0) / steps, lm_ms, lm_n
 
 
-def cpu_baseline(shape, W, h, L, nseq):
-    """The oracle as it stands, on nseq sequences of the same workload (one
-    grouped step each, fresh oracle: parameter widening included)."""
+def cpu_baseline(shape, W, h, L, B, min_seconds):
+    """The oracle as it stands on the same workload: all B sequences, one
+    grouped step after another (each sequence truncated back to L cached
+    positions, as in the timed GPU steps) until min_seconds have passed; the
+    first step includes the oracle's one-time parameter widening."""
     import synth
     from oracle import Oracle
     try:
@@ -83,18 +173,24 @@ def cpu_baseline(shape, W, h, L, nseq):
         threads = max([i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()] or [1])
     except Exception:  # pragma: no cover
         threads = os.cpu_count()
-    kvs = [synth.make_kv(shape, 0, b, L, seed=3) for b in range(nseq)]
+    kvs = [synth.make_kv(shape, 0, b, L, seed=3) for b in range(B)]
     t0 = time.perf_counter()
     orc = Oracle(shape, W.values)
-    for b in range(nseq):
+    for b in range(B):
         (k, _), (v, _) = kvs[b]
         orc.kv_fill(b, L, [k], [v])
-    outs = [orc.step_one(b, h1=h[0, b], h2=h[1, b], readout=False) for b in range(nseq)]
-    orc._readout(outs)
-    dt = time.perf_counter() - t0
-    return dict(value=nseq / dt, unit="tokens/s", cores=int(threads), kind="oracle",
-                sample=f"{nseq} of 32 sequences, one grouped step each (float64 NumPy, fresh oracle "
-                       f"including parameter widening), {dt:.1f} s")
+    steps = 0
+    while True:
+        orc.decode_step(h1=h[0], h2=h[1])
+        for b in range(B):
+            orc.truncate(b, L)
+        steps += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds or steps >= 64:
+            break
+    return dict(value=steps * B / dt, unit="tokens/s", cores=int(threads), kind="oracle",
+                sample=f"{steps} grouped steps of all {B} sequences (float64 NumPy oracle, parameter widening "
+                       f"included), {dt:.1f} s")
 
 
 def time_workload(name, steps, warmup, **shape_kw):
@@ -159,10 +255,25 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seqs", type=int, default=16)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="minimum CPU time of the oracle baseline (whole grouped steps)")
     ap.add_argument("--all", action="store_true",
                     help="also time the long-context and MoE workloads (extra fields)")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="launch a plain 256 MiB device copy three times first (counter calibration)")
+    ap.add_argument("--only", metavar="WORKLOAD", choices=("longctx_bf16", "moe_bf16"),
+                    help="time only this other workload (one JSON line of its fields)")
+    ap.add_argument("--top-k2", type=int, default=4, help="branch fan-out of --only moe_bf16")
+    ap.add_argument("--kernel-table", metavar="DB", help="print the kernel-duration table of a rocprofv3 database")
+    ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DB", "WRITE_DB"),
+                    help="print the calibrated LM-head traffic from two rocprofv3 --pmc databases")
     args = ap.parse_args()
+    if args.kernel_table:
+        print(kernel_table(args.kernel_table))
+        return
+    if args.traffic_summary:
+        print(traffic_summary(*args.traffic_summary))
+        return
     if args.gpus != 1:
         print("bench.py measures one GPU: this build runs the decode path on a single MI355X "
               "(sharding is described, not built); use --gpus 1", file=sys.stderr)
@@ -173,6 +284,10 @@ def main():
     from paper_2608_12385_amd import Session
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.only:
+        kw = {"top_k2": args.top_k2} if args.only == "moe_bf16" else {}
+        print(json.dumps(time_workload(args.only, args.steps, args.warmup, **kw)))
+        return
     w = synth.workload("layer8b_bf16")
     shape = w["shape"]
     B, L = w["batch"], w["cache_len"]
@@ -186,6 +301,13 @@ def main():
     h1d = torch.from_numpy(np.ascontiguousarray(h[0])).cuda()
     h2d = torch.from_numpy(np.ascontiguousarray(h[1])).cuda()
 
+    if args.calib_copy:
+        src = torch.empty(CALIB_BYTES // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     t_grp, lm_ms, lm_n = time_mode(sess, B, L, h1d, h2d, "grouped", args.steps, args.warmup)
     t_pri, _, _ = time_mode(sess, B, L, h1d, h2d, "primary", args.steps, args.warmup)
     t_ung, _, _ = time_mode(sess, B, L, h1d, h2d, "ungrouped", args.steps, args.warmup)
@@ -230,13 +352,13 @@ def main():
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": lm_gbps / HBM_PEAK_GBPS,
-            "traffic": None,
+            "traffic": recorded_traffic(),
             "launch_us": lm_s * 1e6,
             "algorithmic_MB_per_launch": lm_alg / 1e6,
         },
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(shape, W, h, L, args.cpu_seqs)
+        line["cpu_baseline"] = cpu_baseline(shape, W, h, L, B, args.cpu_seconds)
     sess.close()
     if args.all:
         del W
