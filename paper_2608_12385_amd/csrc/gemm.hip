@@ -2,9 +2,10 @@
 // the two paths' residual rows are stacked so each weight tile is read once
 // for both; Sec. 4.5, Eq. (20): the step is bound by weight + KV traffic).
 //
-// bf16 weights: MFMA v_mfma_f32_16x16x32_bf16.  A workgroup owns 64*RB weight
-// rows and up to 128 activation rows; each wave owns 16*RB of the weight rows
-// and accumulates over the whole reduction range in 128-wide chunks.
+// bf16 weights: MFMA v_mfma_f32_16x16x32_bf16.  A workgroup of NW waves owns
+// NW*16*RB weight rows and up to 128 activation rows; each wave owns 16*RB of
+// the weight rows and accumulates over the whole reduction range in 128-wide
+// chunks.
 // Optional split of the reduction across workgroups (grid.y) writes one fp32
 // slab per split; the consumer kernel adds the slabs in split order.  The
 // per-element arithmetic never depends on how many rows are stacked, so the
@@ -23,10 +24,13 @@ namespace {
 constexpr int kChunk = 128;  // reduction elements per pipeline stage
 constexpr int kLdsRow = kChunk + 8;  // padded LDS row of a staged activation chunk (elements)
 
-// A workgroup owns 64*RB consecutive weight rows (all in one segment); wave w
-// owns rows w*16*RB .. +16*RB and runs the whole reduction range of its split.
-// The activation chunk [16*MB rows][128] is staged once per workgroup in LDS
-// (contiguous loads) and read by the four waves in MFMA operand layout.
+// A workgroup owns NW*16*RB consecutive weight rows of one segment (the last
+// tile of a segment may be partial: its rows past the end re-read the last
+// row and are not stored); wave w owns rows w*16*RB .. +16*RB and runs the
+// whole reduction range of its split.  The activation chunk [16*MB rows][128]
+// is staged once per workgroup in LDS (contiguous loads) and read by all waves
+// in MFMA operand layout, so larger workgroups re-read the activations from
+// L2 less often per weight byte.
 //
 // Pipeline: the weights and the activations of chunk c+PD are loaded together
 // while chunk c is multiplied; the activation chunk c+1, loaded PD chunks
@@ -42,12 +46,14 @@ constexpr int kLdsRow = kChunk + 8;  // padded LDS row of a staged activation ch
 // column ranges of their rows instead of all hitting the same few memory
 // channels (row strides are powers of two).  The order is a function of the
 // row tile and the split only.
-template <int MB, int RB, int PD>
-__global__ __launch_bounds__(256) void k_gemm_bf16(WSegs segs, int K, const uint16_t *__restrict__ X, int ldx,
-                                                   int M, float *__restrict__ Y, int ldy, long long y_split_stride,
-                                                   float *__restrict__ row_stats) {
+template <int MB, int RB, int PD, int NW>
+__global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const uint16_t *__restrict__ X, int ldx,
+                                                       int M, float *__restrict__ Y, int ldy,
+                                                       long long y_split_stride, float *__restrict__ row_stats) {
   constexpr int XR = 16 * MB;
-  constexpr int PPT = MB;  // 16-byte pieces of one activation chunk per thread (XR * 16 / 256)
+  constexpr int PIECES = XR * (kChunk / 8);  // 16-byte pieces of one activation chunk
+  constexpr int PPT = (PIECES + NW * 64 - 1) / (NW * 64);
+  constexpr int ROWS = NW * 16 * RB;  // weight rows per workgroup
   __shared__ uint16_t xs[2][XR * kLdsRow];
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int r = lane & 15, gq = lane >> 4;
@@ -59,29 +65,33 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(WSegs segs, int K, const uint
   const int kbeg = c_lo * kChunk;
   const int nch = c_hi - c_lo;
   const int crot = (int)(blockIdx.x * 7u % (unsigned)nch);
-  // segment of this workgroup's rows (segment sizes are multiples of 64*RB)
-  int nloc = blockIdx.x * 64 * RB;
+  // segment of this workgroup's rows: every segment but the last holds a
+  // multiple of ROWS rows; the tiles of the last one are numbered on
+  int nloc = blockIdx.x * ROWS;
   const uint16_t *Wseg = (const uint16_t *)segs.w[0];
-  if (nloc >= segs.rows[0]) {
+  int segrows = segs.rows[0];
+  if (nloc >= segs.rows[0] && segs.rows[1] > 0) {
     nloc -= segs.rows[0];
     Wseg = (const uint16_t *)segs.w[1];
-    if (nloc >= segs.rows[1]) {
+    segrows = segs.rows[1];
+    if (nloc >= segs.rows[1] && segs.rows[2] > 0) {
       nloc -= segs.rows[1];
       Wseg = (const uint16_t *)segs.w[2];
+      segrows = segs.rows[2];
     }
   }
   const int nw = nloc + wave * 16 * RB;             // first row of this wave within the segment
-  const int ny = blockIdx.x * 64 * RB + wave * 16 * RB;  // first output column of this wave
+  const int ny = blockIdx.x * ROWS + wave * 16 * RB;  // first output column of this wave
   const uint16_t *wrow[RB];
 #pragma unroll
-  for (int rb = 0; rb < RB; ++rb) wrow[rb] = Wseg + (size_t)(nw + rb * 16 + r) * K + kbeg + gq * 8;
+  for (int rb = 0; rb < RB; ++rb) wrow[rb] = Wseg + (size_t)min(nw + rb * 16 + r, segrows - 1) * K + kbeg + gq * 8;
   const uint16_t *xsrc[PPT];
   int xdst[PPT];
 #pragma unroll
   for (int j = 0; j < PPT; ++j) {
-    const int p = t + 256 * j, row = p >> 4, col = (p & 15) * 8;
+    const int p = t + NW * 64 * j, row = min(p >> 4, XR - 1), col = (p & 15) * 8;
     xsrc[j] = X + (size_t)min(m0 + row, M - 1) * ldx + kbeg + col;
-    xdst[j] = row * kLdsRow + col;
+    xdst[j] = p < PIECES ? row * kLdsRow + col : -1;
   }
 
   floatx4 acc[RB][MB];
@@ -104,7 +114,8 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(WSegs segs, int K, const uint
   };
   auto xstore = [&](int lds, int slot) {
 #pragma unroll
-    for (int j = 0; j < PPT; ++j) *(u32x4 *)(&xs[lds][xdst[j]]) = stg[slot][j];
+    for (int j = 0; j < PPT; ++j)
+      if (PIECES % (NW * 64) == 0 || xdst[j] >= 0) *(u32x4 *)(&xs[lds][xdst[j]]) = stg[slot][j];
   };
   auto step = [&](int c, int u) {  // multiply chunk c (ring slot u), refill, stage chunk c+1
     const uint16_t *xl = xs[c & 1];
@@ -139,18 +150,22 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(WSegs segs, int K, const uint
   for (int u = 0; u + 1 < PD; ++u)
     if (c0 + u < nch) step(c0 + u, u);
   // lane holds D[n = rb*16 + 4*gq + i][m = cb*16 + r]: Y[m][n .. n+3]
+  bool rvalid[RB];  // 16-row block inside its segment (else a re-read of the last row)
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) rvalid[rb] = nw + rb * 16 < segrows;
   if (row_stats) {
-    // Softmax statistics of each activation row over this workgroup's 64*RB
+    // Softmax statistics of each activation row over this workgroup's valid
     // outputs (one tile): max, sum e^(y - max), sum e^(2(y - max)); waves are
     // merged in wave order.  Used by the mixture readout (no split here).
-    __shared__ float smx[4][XR], s1[4][XR], s2[4][XR];
+    __shared__ float smx[NW][XR], s1[NW][XR], s2[NW][XR];
 #pragma unroll
     for (int cb = 0; cb < MB; ++cb) {
       float mx = -INFINITY;
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb)
+        if (rvalid[rb])
 #pragma unroll
-        for (int i = 0; i < 4; ++i) mx = fmaxf(mx, acc[rb][cb][i]);
+          for (int i = 0; i < 4; ++i) mx = fmaxf(mx, acc[rb][cb][i]);
       mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
       if (gq == 0) smx[wave][cb * 16 + r] = mx;
@@ -159,16 +174,19 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(WSegs segs, int K, const uint
 #pragma unroll
     for (int cb = 0; cb < MB; ++cb) {
       const int mm = cb * 16 + r;
-      const float mx = fmaxf(fmaxf(smx[0][mm], smx[1][mm]), fmaxf(smx[2][mm], smx[3][mm]));
+      float mx = smx[0][mm];
+#pragma unroll
+      for (int w = 1; w < NW; ++w) mx = fmaxf(mx, smx[w][mm]);
       float e1 = 0.f, e2 = 0.f;
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb)
+        if (rvalid[rb])
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float e = expf(acc[rb][cb][i] - mx);
-          e1 += e;
-          e2 += e * e;
-        }
+          for (int i = 0; i < 4; ++i) {
+            const float e = expf(acc[rb][cb][i] - mx);
+            e1 += e;
+            e2 += e * e;
+          }
       e1 += __shfl_xor(e1, 16, 64);
       e1 += __shfl_xor(e1, 32, 64);
       e2 += __shfl_xor(e2, 16, 64);
@@ -180,11 +198,17 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(WSegs segs, int K, const uint
     }
     __syncthreads();
     if (t < XR && m0 + t < M) {
-      const float mx = fmaxf(fmaxf(smx[0][t], smx[1][t]), fmaxf(smx[2][t], smx[3][t]));
+      float mx = smx[0][t], a1 = s1[0][t], a2 = s2[0][t];
+#pragma unroll
+      for (int w = 1; w < NW; ++w) {
+        mx = fmaxf(mx, smx[w][t]);
+        a1 += s1[w][t];
+        a2 += s2[w][t];
+      }
       float *o = row_stats + ((size_t)(m0 + t) * gridDim.x + blockIdx.x) * 3;
       o[0] = mx;
-      o[1] = ((s1[0][t] + s1[1][t]) + s1[2][t]) + s1[3][t];
-      o[2] = ((s2[0][t] + s2[1][t]) + s2[2][t]) + s2[3][t];
+      o[1] = a1;
+      o[2] = a2;
     }
   }
   float *Ys = Y + (long long)split * y_split_stride;
@@ -193,7 +217,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(WSegs segs, int K, const uint
 #pragma unroll
     for (int cb = 0; cb < MB; ++cb) {
       const int m = m0 + cb * 16 + r;
-      if (m < M) *(floatx4 *)(Ys + (size_t)m * ldy + ny + rb * 16 + gq * 4) = acc[rb][cb];
+      if (m < M && rvalid[rb]) *(floatx4 *)(Ys + (size_t)m * ldy + ny + rb * 16 + gq * 4) = acc[rb][cb];
     }
 }
 
@@ -251,17 +275,19 @@ __global__ __launch_bounds__(256) void k_gemm_f32(WSegs segs, int N, int K, cons
 // are active.
 // seg_gran: every segment boundary of the stacked matrices is a multiple of it.
 GemmConfig gemm_config(int n_full, int K, int dtype, int seg_gran, int max_rows) {
-  GemmConfig g{1, 1, 1};
+  GemmConfig g{1, 1, 1, 4};
   if (dtype != 1) return g;
-  if (n_full >= 65536 && seg_gran % 256 == 0) {
-    g = GemmConfig{4, 1, 1};       // output-matrix shapes: 256 rows per workgroup
+  if (n_full >= 65536 && seg_gran == n_full && n_full % 64 == 0) {
+    // output-matrix shapes (one segment): 8 waves x 64 rows = 512 rows per
+    // workgroup, so each staged activation chunk serves 512 weight rows
+    g = GemmConfig{4, 1, 1, 8};
   } else if (n_full >= 16384 && seg_gran % 128 == 0) {
-    g = GemmConfig{2, 2, 1};       // MLP up projections
+    g = GemmConfig{2, 2, 1, 4};    // MLP up projections
   } else {
     // thin matrices: split the reduction so about one workgroup per compute
     // unit runs; the fp32 slabs of up to max_rows stacked rows never exceed
     // the weight bytes, and every split keeps at least one chunk
-    g = GemmConfig{1, 2, 1};
+    g = GemmConfig{1, 2, 1, 4};
     const int tiles = std::max(1, n_full / 64);  // n_full may be 0 (no output matrix)
     const int nc = K / kChunk;
     int S = (256 + tiles / 2) / tiles;
@@ -276,17 +302,19 @@ namespace {
 template <int MB>
 void launch_mb(const GemmConfig &g, dim3 grid, hipStream_t st, const WSegs &segs, int K, const uint16_t *X, int ldx,
                int M, float *Y, int ldy, long long yss, float *rs) {
-  if (g.RB == 4)
-    hipLaunchKernelGGL((k_gemm_bf16<MB, 4, 1>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs);
+  if (g.NW == 8)
+    hipLaunchKernelGGL((k_gemm_bf16<MB, 4, 1, 8>), grid, dim3(512), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs);
   else if (g.RB == 2)
-    hipLaunchKernelGGL((k_gemm_bf16<MB, 2, 2>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs);
+    hipLaunchKernelGGL((k_gemm_bf16<MB, 2, 2, 4>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs);
   else
-    hipLaunchKernelGGL((k_gemm_bf16<MB, 1, 2>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs);
+    hipLaunchKernelGGL((k_gemm_bf16<MB, 1, 2, 4>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs);
 }
 }  // namespace
 
+static int gemm_rows_per_wg(const GemmConfig &g) { return g.NW * 16 * g.RB; }
+
 int gemm_stats_tiles(int N, const GemmConfig &g, int dtype) {
-  return (dtype == 1 && g.S == 1) ? N / (64 * g.RB) : 0;
+  return (dtype == 1 && g.S == 1) ? (N + gemm_rows_per_wg(g) - 1) / gemm_rows_per_wg(g) : 0;
 }
 
 hipError_t launch_gemm(const WSegs &segs, int N, int K, int dtype, const void *X, int ldx, int M, float *Y,
@@ -295,7 +323,7 @@ hipError_t launch_gemm(const WSegs &segs, int N, int K, int dtype, const void *X
   if (dtype == 1) {
     const int mb_total = (M + 15) / 16;
     const int MB = mb_total >= 8 ? 8 : mb_total;
-    dim3 grid(N / (64 * g.RB), g.S, (mb_total + MB - 1) / MB);
+    dim3 grid((N + gemm_rows_per_wg(g) - 1) / gemm_rows_per_wg(g), g.S, (mb_total + MB - 1) / MB);
     const uint16_t *Xb = (const uint16_t *)X;
     float *rs = g.S == 1 ? row_stats : nullptr;
     switch (MB) {

@@ -43,9 +43,10 @@ struct KVRef {
 
 // ---- projections ----
 struct GemmConfig {
-  int RB;  // 16-row blocks per wave (a workgroup owns 64*RB weight rows)
-  int PD;  // weight prefetch depth in 128-element chunks
-  int S;   // reduction splits (one fp32 output slab per split)
+  int RB;      // 16-row blocks per wave (a workgroup owns NW*16*RB weight rows)
+  int PD;      // weight prefetch depth in 128-element chunks
+  int S;       // reduction splits (one fp32 output slab per split)
+  int NW = 4;  // waves per workgroup (4 or 8)
 };
 GemmConfig gemm_config(int n_full, int K, int dtype, int seg_gran, int max_rows);
 hipError_t launch_gemm(const WSegs &segs, int N, int K, int dtype, const void *X, int ldx, int M,
