@@ -81,45 +81,69 @@ def _counter(path, counter):
 
 
 def traffic_summary(fetch_path, write_path):
-    """Memory-counter traffic of the output-matrix projection, calibrated on a plain device copy.
+    """Memory-counter traffic, calibrated on a plain device copy, of the
+    output-matrix projection and of whole grouped steps.
 
     Each counter (KiB per dispatch) is scaled by known bytes / counter reading of
     the 256 MiB device-to-device copies bench.py --calib-copy launches (the only
-    copies of that size in the run)."""
-    lines = []
-    res = {}
+    copies of that size in the run).  The runs use --grouped-only, so every
+    dispatch after the last calibration copy belongs to a grouped step; steps
+    are counted by the mixture's final kernel (one launch per step)."""
+    lines, steps = [], []
+    res, step_bytes = {}, {}
     for counter, path in (("FETCH_SIZE", fetch_path), ("WRITE_SIZE", write_path)):
         vals = _counter(path, counter)
-        calib = [v for k, v in vals if "copyBuffer" in k and v > 0.4 * CALIB_BYTES / 1024]
-        if len(calib) != 3:
-            raise SystemExit(f"{counter}: expected 3 calibration copies, found {len(calib)}")
+        idx = [i for i, (k, v) in enumerate(vals) if "copyBuffer" in k and v > 0.4 * CALIB_BYTES / 1024]
+        if len(idx) != 3:
+            raise SystemExit(f"{counter}: expected 3 calibration copies, found {len(idx)}")
+        calib = [vals[i][1] for i in idx]
         factor = (CALIB_BYTES / 1024) / (sum(calib) / len(calib))
-        lm = [v for k, v in vals if _short(k) == LMHEAD_KERNEL]
+        after = vals[idx[-1] + 1:]
+        lm = [v for k, v in after if _short(k) == LMHEAD_KERNEL]
         if not lm:
             raise SystemExit(f"{counter}: no {LMHEAD_KERNEL} dispatches")
+        n_steps = sum(1 for k, _ in after if _short(k) == "k_mix_final")
         kib = sum(lm) / len(lm)
         res[counter] = kib * 1024 * factor
+        step_bytes[counter] = sum(v for _, v in after) * 1024 * factor / max(n_steps, 1)
         lines.append(f"| {counter} | {sum(calib) / len(calib):.1f} | {factor:.4f} | {len(lm)} | {kib:.1f} | "
-                     f"{kib * 1024 * factor / 1e6:.1f} |")
+                     f"{kib * 1024 * factor / 1e6:.1f} | {n_steps} | {step_bytes[counter] / 1e6:.1f} |")
     total = res["FETCH_SIZE"] + res["WRITE_SIZE"]
+    step_total = step_bytes["FETCH_SIZE"] + step_bytes["WRITE_SIZE"]
     head = ["| counter | calibration copy reads (KiB, 256 MiB moved) | scale | LM-head dispatches | "
-            "LM-head avg (KiB) | LM-head scaled (MB) |", "|---|---|---|---|---|---|"]
+            "LM-head avg (KiB) | LM-head scaled (MB) | grouped steps | per step scaled (MB) |",
+            "|---|---|---|---|---|---|---|---|"]
     tail = ["", f"lmhead_traffic_bytes_per_launch: {int(round(total))}",
-            f"gemm_source_sha256: {_sha256(GEMM_SOURCE)}"]
+            f"step_traffic_bytes: {int(round(step_total))}",
+            f"gemm_source_sha256: {_sha256(GEMM_SOURCE)}",
+            f"sources_sha256: {_sources_sha()}"]
     return "\n".join(head + lines + tail)
 
 
+def _sources_sha():
+    import hashlib
+    import glob
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2608_12385_amd", "csrc", "*"))):
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
 def recorded_traffic():
-    """Counter-derived HBM bytes per launch of the output-matrix projection, or
-    None when no record exists or the projection kernel changed since."""
+    """Counter-derived HBM bytes: (per launch of the output-matrix projection,
+    per grouped step), each None when no record exists or the code it was
+    measured on changed since (the projection source / all kernel sources)."""
     try:
         text = open(TRAFFIC_PROFILE).read()
     except OSError:
-        return None
-    kv = dict(l.split(": ", 1) for l in text.splitlines() if l.startswith(("lmhead_traffic", "gemm_source")))
-    if kv.get("gemm_source_sha256") != _sha256(GEMM_SOURCE):
-        return None
-    return int(kv["lmhead_traffic_bytes_per_launch"])
+        return None, None
+    kv = dict(l.split(": ", 1) for l in text.splitlines()
+              if l.startswith(("lmhead_traffic", "step_traffic", "gemm_source", "sources_sha")))
+    lm = int(kv["lmhead_traffic_bytes_per_launch"]) if kv.get("gemm_source_sha256") == _sha256(GEMM_SOURCE) else None
+    st = int(kv["step_traffic_bytes"]) if ("step_traffic_bytes" in kv and
+                                          kv.get("sources_sha256") == _sources_sha()) else None
+    return lm, st
 
 
 def algorithmic_bytes(shape, B, L):
@@ -261,6 +285,9 @@ def main():
                     help="also time the long-context and MoE workloads (extra fields)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="launch a plain 256 MiB device copy three times first (counter calibration)")
+    ap.add_argument("--grouped-only", action="store_true",
+                    help="time only the grouped step (counter runs: every dispatch after the calibration "
+                         "copies belongs to a grouped step)")
     ap.add_argument("--only", metavar="WORKLOAD", choices=("longctx_bf16", "moe_bf16"),
                     help="time only this other workload (one JSON line of its fields)")
     ap.add_argument("--top-k2", type=int, default=4, help="branch fan-out of --only moe_bf16")
@@ -309,9 +336,13 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     t_grp, lm_ms, lm_n = time_mode(sess, B, L, h1d, h2d, "grouped", args.steps, args.warmup)
-    t_pri, _, _ = time_mode(sess, B, L, h1d, h2d, "primary", args.steps, args.warmup)
-    t_ung, _, _ = time_mode(sess, B, L, h1d, h2d, "ungrouped", args.steps, args.warmup)
+    if args.grouped_only:
+        t_pri = t_ung = float("nan")
+    else:
+        t_pri, _, _ = time_mode(sess, B, L, h1d, h2d, "primary", args.steps, args.warmup)
+        t_ung, _, _ = time_mode(sess, B, L, h1d, h2d, "ungrouped", args.steps, args.warmup)
 
+    traffic_lm, traffic_step = recorded_traffic()
     layer_b, head_b, kv_b = algorithmic_bytes(shape, B, L)
     step_bytes = layer_b + head_b + kv_b
     x_bytes = 2 * B * shape.d_model * 2
@@ -345,6 +376,8 @@ def main():
         "algorithmic_MB_per_step": step_bytes / 1e6,
         "step_GBps": step_bytes / t_grp / 1e9,
         "step_frac_of_peak": step_bytes / t_grp / 1e9 / HBM_PEAK_GBPS,
+        "step_traffic_MB": None if traffic_step is None else traffic_step / 1e6,
+        "step_traffic_vs_algorithmic": None if traffic_step is None else traffic_step / step_bytes,
         "roofline": {
             "kernel": "LM-head projection (k_gemm_bf16, 64 stacked rows)",
             "bound": "hbm",
@@ -352,7 +385,7 @@ def main():
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": lm_gbps / HBM_PEAK_GBPS,
-            "traffic": recorded_traffic(),
+            "traffic": traffic_lm,
             "launch_us": lm_s * 1e6,
             "algorithmic_MB_per_launch": lm_alg / 1e6,
         },

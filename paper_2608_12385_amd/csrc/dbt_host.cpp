@@ -544,16 +544,25 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
 
   if (L.moe) return run_moe_mlp(m, l, c, st);
 
-  // 4. gate/up + SwiGLU + b coupling
-  WSegs gu{{W.w_gate, W.w_up, nullptr}, {f, f, 0}};
-  stride = (long long)c.rows_layout * 2 * f;
-  {
+  // 4. gate/up + SwiGLU + b coupling (fused into the projection's epilogue
+  // when the tiles fill the chip)
+  const Retain ret_h_keep{c.retain ? ret_h : nullptr, c.ret_src, c.ret_dst};
+  if (gemm_glu_ok(f, M, c.rows.np, cf.dtype)) {
+    const GluEpi ep{c.rows, c.mode, f, W.b, ret_h, ret_h_keep, (uint16_t *)Xh, f};
     Timed tm(m, DBT_STAGE_GATEUP, st);
-    HIPCHK(launch_gemm(gu, 2 * f, d, cf.dtype, Xn + (size_t)xrow0 * d * es, d, M, P + (size_t)xrow0 * 2 * f,
-                       2 * f, stride, g_gu, st));
+    HIPCHK(launch_gemm_glu((const uint16_t *)W.w_gate, (const uint16_t *)W.w_up, f, d, Xn + (size_t)xrow0 * d * es,
+                           d, M, ep, st));
+  } else {
+    WSegs gu{{W.w_gate, W.w_up, nullptr}, {f, f, 0}};
+    stride = (long long)c.rows_layout * 2 * f;
+    {
+      Timed tm(m, DBT_STAGE_GATEUP, st);
+      HIPCHK(launch_gemm(gu, 2 * f, d, cf.dtype, Xn + (size_t)xrow0 * d * es, d, M, P + (size_t)xrow0 * 2 * f,
+                         2 * f, stride, g_gu, st));
+    }
+    HIPCHK(launch_swiglu_finish(P, stride, S_gu, 2 * f, f, c.mode, c.rows, W.b, ret_h, ret_h_keep, cf.dtype, Xh, f,
+                                st));
   }
-  HIPCHK(launch_swiglu_finish(P, stride, S_gu, 2 * f, f, c.mode, c.rows, W.b, ret_h,
-                              Retain{c.retain ? ret_h : nullptr, c.ret_src, c.ret_dst}, cf.dtype, Xh, f, st));
 
   // 5. down projection + c coupling + residual + next norm
   WSegs wd{{W.w_down, nullptr, nullptr}, {d, 0, 0}};

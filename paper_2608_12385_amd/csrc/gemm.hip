@@ -46,10 +46,15 @@ constexpr int kLdsRow = kChunk + 8;  // padded LDS row of a staged activation ch
 // column ranges of their rows instead of all hitting the same few memory
 // channels (row strides are powers of two).  The order is a function of the
 // row tile and the split only.
-template <int MB, int RB, int PD, int NW>
+//
+// GLU: the workgroup owns 32*RB rows of segment 0 (gate, waves 0-1) and the
+// same rows of segment 1 (up, waves 2-3); instead of storing Y it finishes
+// the MLP intermediate in its epilogue (see GluEpi).
+template <int MB, int RB, int PD, int NW, bool GLU = false>
 __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const uint16_t *__restrict__ X, int ldx,
                                                        int M, float *__restrict__ Y, int ldy,
-                                                       long long y_split_stride, float *__restrict__ row_stats) {
+                                                       long long y_split_stride, float *__restrict__ row_stats,
+                                                       GluEpi ep) {
   constexpr int XR = 16 * MB;
   constexpr int PIECES = XR * (kChunk / 8);  // 16-byte pieces of one activation chunk
   constexpr int PPT = (PIECES + NW * 64 - 1) / (NW * 64);
@@ -70,7 +75,14 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
   int nloc = blockIdx.x * ROWS;
   const uint16_t *Wseg = (const uint16_t *)segs.w[0];
   int segrows = segs.rows[0];
-  if (nloc >= segs.rows[0] && segs.rows[1] > 0) {
+  if (GLU) {
+    static_assert(!GLU || NW == 4, "GLU tiles are 4 waves");
+    nloc = blockIdx.x * 32 * RB - (wave & 2) * 16 * RB;  // + wave*16*RB below: rows (wave&1)*16*RB of the tile
+    if (wave >= 2) {
+      Wseg = (const uint16_t *)segs.w[1];
+      segrows = segs.rows[1];
+    }
+  } else if (nloc >= segs.rows[0] && segs.rows[1] > 0) {
     nloc -= segs.rows[0];
     Wseg = (const uint16_t *)segs.w[1];
     segrows = segs.rows[1];
@@ -150,6 +162,58 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
   for (int u = 0; u + 1 < PD; ++u)
     if (c0 + u < nch) step(c0 + u, u);
   // lane holds D[n = rb*16 + 4*gq + i][m = cb*16 + r]: Y[m][n .. n+3]
+  if constexpr (GLU) {
+    // hb[m][c]: the tile's 32*RB gate/up columns c for activation row m
+    // (reuses the activation slots: the loop's last barrier has passed)
+    constexpr int HC = 32 * RB + 1;
+    static_assert(XR * HC * 4 <= (int)sizeof(xs), "GLU staging exceeds the activation slots");
+    float *hb = (float *)&xs[0][0];
+    const int c0 = (wave & 1) * 16 * RB;
+    if (wave >= 2)
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int cb = 0; cb < MB; ++cb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) hb[(cb * 16 + r) * HC + c0 + rb * 16 + 4 * gq + i] = acc[rb][cb][i];
+    __syncthreads();
+    if (wave < 2)
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int cb = 0; cb < MB; ++cb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int idx = (cb * 16 + r) * HC + c0 + rb * 16 + 4 * gq + i;
+            const float g = acc[rb][cb][i];
+            hb[idx] = g / (1.0f + expf(-g)) * hb[idx];
+          }
+    __syncthreads();
+    const int Bp = ep.rows.Bp, row0 = ep.rows.p0 * Bp;
+    for (int e = t; e < XR * 32 * RB; e += NW * 64) {
+      const int mm = e / (32 * RB), cc = e % (32 * RB);
+      const int gm = m0 + mm;  // row of this call (relative to its first row)
+      if (gm >= M) continue;
+      const int path = ep.rows.p0 + gm / Bp, b = gm % Bp;
+      if (b >= ep.rows.B) continue;
+      const int n = blockIdx.x * 32 * RB + cc;
+      const float h = hb[mm * HC + cc];
+      float out;
+      if (path == 0) {
+        out = h;
+        const Retain &rt = ep.ret;
+        if (rt.ptr && (rt.src_row < 0 || rt.src_row == b))
+          rt.ptr[(size_t)(rt.src_row < 0 ? b : rt.dst_row) * ep.f + n] = h;
+      } else {
+        // H2~ = H2 + b * H1: the primary row of the same sequence is in this
+        // tile (both paths, M <= 16*MB) or comes from the retained H1
+        const float h1 = ep.rows.np == 2 ? hb[(mm - Bp) * HC + cc] : ep.H1_in[(size_t)b * ep.f + n];
+        out = h + ep.bvec[n] * h1;
+      }
+      ep.Xh[(size_t)(row0 + gm) * ep.ldh + n] = f2bf(out);
+    }
+    return;
+  }
   bool rvalid[RB];  // 16-row block inside its segment (else a re-read of the last row)
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) rvalid[rb] = nw + rb * 16 < segrows;
@@ -302,12 +366,20 @@ namespace {
 template <int MB>
 void launch_mb(const GemmConfig &g, dim3 grid, hipStream_t st, const WSegs &segs, int K, const uint16_t *X, int ldx,
                int M, float *Y, int ldy, long long yss, float *rs) {
+  const GluEpi none{};
   if (g.NW == 8)
-    hipLaunchKernelGGL((k_gemm_bf16<MB, 4, 1, 8>), grid, dim3(512), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs);
+    hipLaunchKernelGGL((k_gemm_bf16<MB, 4, 1, 8>), grid, dim3(512), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs, none);
   else if (g.RB == 2)
-    hipLaunchKernelGGL((k_gemm_bf16<MB, 2, 2, 4>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs);
+    hipLaunchKernelGGL((k_gemm_bf16<MB, 2, 2, 4>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs, none);
   else
-    hipLaunchKernelGGL((k_gemm_bf16<MB, 1, 2, 4>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs);
+    hipLaunchKernelGGL((k_gemm_bf16<MB, 1, 2, 4>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs, none);
+}
+
+template <int MB>
+void launch_glu_mb(dim3 grid, hipStream_t st, const WSegs &segs, int K, const uint16_t *X, int ldx, int M,
+                   const GluEpi &ep) {
+  hipLaunchKernelGGL((k_gemm_bf16<MB, 2, 2, 4, true>), grid, dim3(256), 0, st, segs, K, X, ldx, M, nullptr, 0, 0LL,
+                     nullptr, ep);
 }
 }  // namespace
 
@@ -315,6 +387,34 @@ static int gemm_rows_per_wg(const GemmConfig &g) { return g.NW * 16 * g.RB; }
 
 int gemm_stats_tiles(int N, const GemmConfig &g, int dtype) {
   return (dtype == 1 && g.S == 1) ? (N + gemm_rows_per_wg(g) - 1) / gemm_rows_per_wg(g) : 0;
+}
+
+// Tiles of 64 gate + 64 up rows; enough of them to fill the chip, and a
+// branch row's primary partner in the same activation tile (M <= 128).
+bool gemm_glu_ok(int f, int M, int np, int dtype) {
+  return dtype == 1 && f % 64 == 0 && f / 64 >= 192 && (np == 1 || M <= 128);
+}
+
+hipError_t launch_gemm_glu(const uint16_t *w_gate, const uint16_t *w_up, int f, int K, const void *X, int ldx, int M,
+                           const GluEpi &ep, hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  if (!gemm_glu_ok(f, M, ep.rows.np, 1)) return hipErrorInvalidValue;
+  const WSegs segs{{w_gate, w_up, nullptr}, {f, f, 0}};
+  const int mb_total = (M + 15) / 16;
+  const int MB = mb_total >= 8 ? 8 : mb_total;
+  dim3 grid(f / 64, 1, (mb_total + MB - 1) / MB);
+  const uint16_t *Xb = (const uint16_t *)X;
+  switch (MB) {
+    case 1: launch_glu_mb<1>(grid, st, segs, K, Xb, ldx, M, ep); break;
+    case 2: launch_glu_mb<2>(grid, st, segs, K, Xb, ldx, M, ep); break;
+    case 3: launch_glu_mb<3>(grid, st, segs, K, Xb, ldx, M, ep); break;
+    case 4: launch_glu_mb<4>(grid, st, segs, K, Xb, ldx, M, ep); break;
+    case 5: launch_glu_mb<5>(grid, st, segs, K, Xb, ldx, M, ep); break;
+    case 6: launch_glu_mb<6>(grid, st, segs, K, Xb, ldx, M, ep); break;
+    case 7: launch_glu_mb<7>(grid, st, segs, K, Xb, ldx, M, ep); break;
+    default: launch_glu_mb<8>(grid, st, segs, K, Xb, ldx, M, ep); break;
+  }
+  return hipGetLastError();
 }
 
 hipError_t launch_gemm(const WSegs &segs, int N, int K, int dtype, const void *X, int ldx, int M, float *Y,

@@ -49,6 +49,25 @@ struct GemmConfig {
   int NW = 4;  // waves per workgroup (4 or 8)
 };
 GemmConfig gemm_config(int n_full, int K, int dtype, int seg_gran, int max_rows);
+
+// Gate/up projection with the SwiGLU + b-coupling epilogue fused (Eqs. (13)-(14)):
+// writes the MLP intermediate H (bf16, rows p*Bp + b, leading dimension ldh)
+// instead of fp32 gate/up outputs.  Branch rows take H1 from the primary rows of
+// the same call (mode GROUPED) or from H1_in (mode BRANCH); primary rows are
+// kept in ret when asked.  Usable when gemm_glu_ok() holds.
+struct GluEpi {
+  Rows rows;
+  int mode;
+  int f;
+  const float *bvec;   // [f]
+  const float *H1_in;  // [B][f] (mode BRANCH)
+  Retain ret;
+  uint16_t *Xh;
+  int ldh;
+};
+bool gemm_glu_ok(int f, int M, int np, int dtype);
+hipError_t launch_gemm_glu(const uint16_t *w_gate, const uint16_t *w_up, int f, int K, const void *X, int ldx, int M,
+                           const GluEpi &ep, hipStream_t st);
 hipError_t launch_gemm(const WSegs &segs, int N, int K, int dtype, const void *X, int ldx, int M,
                        float *Y, int ldy, long long y_split_stride, const GemmConfig &g, hipStream_t st,
                        float *row_stats = nullptr);

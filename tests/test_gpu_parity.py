@@ -19,7 +19,7 @@ BF16_TOL = 2e-2
 
 
 def _np(t):
-    return t.detach().cpu().numpy()
+    return t if isinstance(t, np.ndarray) else t.detach().cpu().numpy()
 
 
 def _check_readout(t, outs, tol, tag, branch=True):
@@ -219,16 +219,33 @@ def test_cache_append_exactly_one_slot_per_layer_and_no_branch_entries():
 # one 8B-shape layer + LM head, batch 32, cache 4096: sampled rows at full size
 # ----------------------------------------------------------------------------
 
-@pytest.mark.slow
-def test_layer8b_full_size_sampled():
+@pytest.fixture(scope="module")
+def layer8b():
+    """The benchmark layer at full size (d 4096, vocab 128256, batch 32, 4096
+    cached positions), built once for the tests below."""
     w = synth.workload("layer8b_bf16")
     shape = w["shape"]
     B, L = w["batch"], w["cache_len"]
     W = synth.make_weights(shape, seed=0)
     sess = make_session(shape, W, max_batch=B, max_pos=L + 16)
     fill_cache(sess, None, shape, [L] * B)
+    yield shape, W, sess, B, L
+    sess.close()
+
+
+def _truncate_all(sess, B, L):
+    from paper_2608_12385_amd import binding
+    for b in range(B):
+        binding.dbt_kv_truncate(sess.kv, b, L)
+
+
+@pytest.mark.slow
+def test_layer8b_full_size_sampled(layer8b):
+    shape, W, sess, B, L = layer8b
     h = synth.make_hidden(shape, B, step=0, seed=2)
     t = sess.decode(h1=h[0], h2=h[1])
+    t = {k: _np(v).copy() for k, v in t.items()}
+    _truncate_all(sess, B, L)
     sample = [0, 17, 31]
     orc = Oracle(shape, W.values)
     for b in sample:
@@ -240,10 +257,39 @@ def test_layer8b_full_size_sampled():
     orc._readout(outs)
     sub = {k: v[sample] for k, v in t.items()}
     _check_readout(sub, outs, BF16_TOL, "layer8b")
-    assert row_err(_np(sub["h1_out"]), np.stack([o["h1"] for o in outs])).max() <= BF16_TOL
-    assert row_err(_np(sub["h2_out"]), np.stack([o["h2"] for o in outs])).max() <= BF16_TOL
+    assert row_err(sub["h1_out"], np.stack([o["h1"] for o in outs])).max() <= BF16_TOL
+    assert row_err(sub["h2_out"], np.stack([o["h2"] for o in outs])).max() <= BF16_TOL
     # properties at full size for every row: alpha in [0.5, 1]; tokens valid
-    a = _np(t["alpha"])
+    a = t["alpha"]
     assert np.all((a >= 0.5) & (a <= 1.0))
-    nt = _np(t["next_token"])
+    nt = t["next_token"]
     assert np.all((nt >= 0) & (nt < shape.vocab))
+
+
+@pytest.mark.slow
+def test_layer8b_full_size_modes_bitwise(layer8b):
+    """At the benchmark shape (fused gate/up epilogue, 8-wave output
+    projection): primary outputs and the cache are bit-identical with the
+    branch on or off, and the grouped step equals the two-pass step bit for
+    bit (Sec. 4.4: the branch never feeds the primary; grouping only
+    reorganises the work)."""
+    shape, W, sess, B, L = layer8b
+    h = synth.make_hidden(shape, B, step=1, seed=2)
+    res = {}
+    for mode in ("on", "off", "ungrouped"):
+        if mode == "ungrouped":
+            t = sess.decode(h1=h[0], h2=h[1], grouped=False)
+        else:
+            t = sess.decode(h1=h[0], h2=h[1], branch_on=(mode == "on"))
+        res[mode] = {k: _np(v).copy() for k, v in t.items()}
+        res[mode]["k"] = sess.k_pages.clone()
+        res[mode]["v"] = sess.v_pages.clone()
+        _truncate_all(sess, B, L)
+    on, off, ug = res["on"], res["off"], res["ungrouped"]
+    np.testing.assert_array_equal(on["h1_out"], off["h1_out"])
+    np.testing.assert_array_equal(on["logits1"], off["logits1"])
+    assert bool((on["k"] == off["k"]).all()) and bool((on["v"] == off["v"]).all())
+    assert np.all(off["alpha"] == 1.0)
+    for k in ("h1_out", "h2_out", "logits1", "logits2", "alpha", "next_token"):
+        np.testing.assert_array_equal(on[k], ug[k], err_msg=k)
+    assert bool((on["k"] == ug["k"]).all()) and bool((on["v"] == ug["v"]).all())
