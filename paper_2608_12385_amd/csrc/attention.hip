@@ -302,6 +302,137 @@ __global__ void k_attn_combine(AttnArgs a, T *O, int ldo) {
   st<T>(O, out + 3, o.w / l);
 }
 
+// Causal attention over the prompt of one sequence on MFMA (bf16 cache,
+// d_h = 128; Sec. 4.4, prefill through the primary path).  A workgroup owns
+// 16 consecutive query positions and one KV head; wave w is query head
+// g*G + w, so the G waves read the same K/V pages.  Each wave walks the page
+// pairs up to its last position with the decode kernel's permuted score rows
+// (lane: eight consecutive key positions of one page for one query), masks
+// keys after the query (causal) and cache slots past the prompt, and keeps an
+// online softmax per query row.  Tiles are issued longest first.
+__global__ __launch_bounds__(1024) void k_attn_prefill_bf16(const float *Q, int ldq, int T, KVRef kv, int seq,
+                                                           int n_q, uint16_t *O, int ldo) {
+  constexpr int DH = 128;
+  const int ntiles = (T + 15) >> 4;
+  const int q0 = (ntiles - 1 - (int)blockIdx.x) * 16;  // longest tiles first
+  const int g = blockIdx.y;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r = lane & 15, gq = lane >> 4;
+  const int n_kv = kv.n_kv;
+  const int G = n_q / n_kv;
+  const int head = g * G + wave;
+  const float scale = kLog2e / sqrtf((float)DH);
+  const int qpos = q0 + r;  // query position of this lane's column
+  const int qlast = min(q0 + 15, T - 1);
+
+  u32x4 qf[4];
+  {
+    const bool valid = qpos < T;
+    const float *qp = Q + (size_t)(valid ? qpos : 0) * ldq + head * DH + gq * 8;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      float x[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] = valid ? qp[s * 32 + e] : 0.f;
+      qf[s] = u32x4{pack2(x[0], x[1]), pack2(x[2], x[3]), pack2(x[4], x[5]), pack2(x[6], x[7])};
+    }
+  }
+  const uint16_t *kbase = (const uint16_t *)kv.k;
+  const uint16_t *vbase = (const uint16_t *)kv.v;
+  const int *ptab = kv.page_table + (size_t)seq * kv.mpps;
+  float m_run = -INFINITY, l_run = 0.f;
+  floatx4 acc[8];
+#pragma unroll
+  for (int c = 0; c < 8; ++c) acc[c] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const int kpage = r >> 3, kpos = 8 * ((r >> 2) & 1) + (r & 3);
+  const int vpage = gq >> 1, vpos = 8 * (gq & 1);
+  const int npg = (qlast >> 4) + 1;  // pages holding keys 0..qlast
+  const int npairs = (npg + 1) >> 1;
+  int nid0 = ptab[0], nid1 = ptab[min(1, npg - 1)];
+  for (int q = 0; q < npairs; ++q) {
+    const int pg0 = 2 * q;
+    const int phys0 = nid0, phys1 = nid1;
+    if (q + 1 < npairs) {  // page ids of the next pair
+      nid0 = ptab[pg0 + 2];
+      nid1 = ptab[min(pg0 + 3, npg - 1)];
+    }
+    const int kphys = kpage ? phys1 : phys0;
+    const int vphys = vpage ? phys1 : phys0;
+    const uint16_t *kp = kbase + ((size_t)kphys * n_kv + g) * 16 * DH + kpos * DH + gq * 8;
+    const uint16_t *vp = vbase + ((size_t)vphys * n_kv + g) * DH * 16 + r * 16 + vpos;
+    u32x4 ka[4], kb[4], vf[8];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      ka[s] = *(const u32x4 *)(kp + s * 32);
+      kb[s] = *(const u32x4 *)(kp + 4 * DH + s * 32);
+    }
+#pragma unroll
+    for (int c = 0; c < 8; ++c) vf[c] = *(const u32x4 *)(vp + c * 16 * 16);
+    floatx4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ka[s]),
+                                                   __builtin_bit_cast(bf16x8, qf[s]), s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kb[s]),
+                                                   __builtin_bit_cast(bf16x8, qf[s]), s1, 0, 0, 0);
+    }
+    // key position of this lane's first score; keys after the query are masked
+    const int kp0 = (pg0 + vpage) * 16 + vpos;
+    const bool page_ok = pg0 + vpage < npg;
+    float sc[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      sc[i] = (page_ok && kp0 + i <= qpos) ? s0[i] * scale : -INFINITY;
+      sc[4 + i] = (page_ok && kp0 + 4 + i <= qpos) ? s1[i] * scale : -INFINITY;
+    }
+    float mt = sc[0];
+#pragma unroll
+    for (int i = 1; i < 8; ++i) mt = fmaxf(mt, sc[i]);
+    mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
+    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+    const float m_new = fmaxf(m_run, mt);
+    // a query row with no key yet in this pair keeps m = -inf: use 0 as the base
+    const float m_use = m_new == -INFINITY ? 0.f : m_new;
+    float p[8];
+    float ps = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      p[i] = exp2f(sc[i] - m_use);
+      ps += p[i];
+    }
+    if (__any(m_new > m_run)) {
+      const float corr = m_run == -INFINITY ? 0.f : exp2f(m_run - m_new);
+      l_run *= corr;
+#pragma unroll
+      for (int c = 0; c < 8; ++c) acc[c] = acc[c] * corr;
+    }
+    l_run += ps;
+    m_run = m_new;
+    const u32x4 pf = u32x4{pack2(p[0], p[1]), pack2(p[2], p[3]), pack2(p[4], p[5]), pack2(p[6], p[7])};
+    // cache slots past the prompt (or a missing second page) may hold stale values
+    const int nv = page_ok ? min(16, T - (pg0 + vpage) * 16) : 0;
+    if (__any(nv < 16)) {
+#pragma unroll
+      for (int c = 0; c < 8; ++c) vf[c] = mask8(vf[c], vpos, nv);
+    }
+#pragma unroll
+    for (int c = 0; c < 8; ++c)
+      acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vf[c]),
+                                                       __builtin_bit_cast(bf16x8, pf), acc[c], 0, 0, 0);
+  }
+  l_run += __shfl_xor(l_run, 16, 64);
+  l_run += __shfl_xor(l_run, 32, 64);
+  if (qpos < T) {
+    const float inv = 1.f / l_run;
+    uint16_t *o = O + (size_t)qpos * ldo + head * DH;
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      const int dh = c * 16 + 4 * gq;
+      *(u32x2 *)(o + dh) = u32x2{pack2(acc[c][0] * inv, acc[c][1] * inv), pack2(acc[c][2] * inv, acc[c][3] * inv)};
+    }
+  }
+}
+
 // Causal attention over the prompt of one sequence: workgroup per
 // (position t, KV head), keys 0..t in chunks of 256 with an online softmax.
 template <typename T>
@@ -402,6 +533,12 @@ hipError_t launch_attn_combine(const AttnArgs &a, void *O, int ldo, hipStream_t 
 
 hipError_t launch_attn_prefill(const float *Q, int ldq, int T, KVRef kv, int seq, int n_q, int dtype, void *O,
                                int ldo, hipStream_t st) {
+  const int G = n_q / kv.n_kv;
+  if (dtype == 1 && kv.d_h == 128 && G >= 1 && G <= 16) {
+    dim3 grid((T + 15) / 16, kv.n_kv);
+    hipLaunchKernelGGL(k_attn_prefill_bf16, grid, dim3(64 * G), 0, st, Q, ldq, T, kv, seq, n_q, (uint16_t *)O, ldo);
+    return hipGetLastError();
+  }
   dim3 grid(T, kv.n_kv);
   if (dtype == 1)
     hipLaunchKernelGGL(k_attn_prefill<uint16_t>, grid, dim3(256), 0, st, Q, ldq, kv, seq, n_q, (uint16_t *)O, ldo);

@@ -106,6 +106,27 @@ def test_small_bf16_prefill_boundary_steps():
         np.testing.assert_array_equal(dev_tab[b, :len(tab)], tab)
 
 
+def test_bf16_long_prefill_poisoned_pages():
+    """Prefill attention on MFMA: prompts spanning many 16-position query tiles
+    and page pairs (odd page counts, a one-token prompt), every cache byte
+    poisoned with 0xFF (bf16 NaN) first, so slots past each prompt hold NaN."""
+    shape = _small_bf16(n_layers=2)
+    W = synth.make_weights(shape, seed=0)
+    lens = [1500, 1, 2063, 31]
+    prompts = [synth.make_tokens(1, 40 + i, (L,), shape.vocab) for i, L in enumerate(lens)]
+    orc = Oracle(shape, W.values)
+    obs = orc.prefill(prompts, run_boundary=True)
+    sess = make_session(shape, W, max_batch=len(lens), max_pos=2100, max_prompt=2063)
+    sess.k_pages.fill_(0xFF)
+    sess.v_pages.fill_(0xFF)
+    t = sess.prefill(prompts, run_boundary=True)
+    _check_readout(t, obs, BF16_TOL, "long prefill")
+    toks = [o["next"] for o in obs]
+    outs = orc.decode_step(tokens=toks)
+    t = sess.decode(tokens=toks)
+    _check_readout(t, outs, BF16_TOL, "step after long prefill")
+
+
 def sess_pages(sess, b):
     from paper_2608_12385_amd import binding
     return binding.dbt_kv_pages(sess.kv, b)
