@@ -273,6 +273,54 @@ def time_workload(name, steps, warmup, **shape_kw):
     return rec
 
 
+def time_full24(steps):
+    """The full dense model: prefill of all prompts (primary path), then greedy
+    grouped steps with the branch on, then the same number with the branch
+    off (caches truncated back to the prompt), tokens fed back on the device."""
+    import torch
+    import synth
+    from paper_2608_12385_amd import Session, binding
+    w = synth.workload("full24_bf16")
+    shape = w["shape"]
+    B, T = w["batch"], w["prompt_len"]
+    steps = steps or w["steps"]
+    W = synth.make_weights(shape, seed=0)
+    sess = Session(shape, {k: W.device_array(k) for k in W.values}, max_batch=B, max_pos=T + steps + 16,
+                   max_prompt=T)
+    del W
+    prompts = [synth.make_tokens(1, 1000 + b, (T,), shape.vocab) for b in range(B)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    t = sess.prefill(prompts, run_boundary=True)
+    torch.cuda.synchronize()
+    t_pre = time.perf_counter() - t0
+    first = t["next_token"].clone()
+    res = {}
+    for mode in ("on", "off"):
+        for b in range(B):
+            binding.dbt_kv_truncate(sess.kv, b, T)
+        tok = first.clone()
+        outs = [sess.outputs(B, logits=False, hidden=False) for _ in range(2)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(steps):
+            out, tt = outs[i % 2]
+            binding.dbt_decode_step(sess.model, sess.kv, sess.step_in(B, tok), 1 if mode == "on" else 0, out,
+                                    sess.stream)
+            tok = tt["next_token"]
+        torch.cuda.synchronize()
+        res[mode] = time.perf_counter() - t0
+    sess.close()
+    return {"workload": "full24_bf16", "batch": B, "prompt_len": T, "steps": steps,
+            "prefill_s": t_pre, "prefill_tokens_per_s": B * T / t_pre,
+            "decode_step_us_branch_on": res["on"] / steps * 1e6, "decode_step_us_branch_off": res["off"] / steps * 1e6,
+            "decode_tokens_per_s_branch_on": B * steps / res["on"],
+            "decode_tokens_per_s_branch_off": B * steps / res["off"],
+            "end_to_end_tokens_per_s_branch_on": B * steps / (t_pre + res["on"]),
+            "end_to_end_tokens_per_s_branch_off": B * steps / (t_pre + res["off"]),
+            "branch_overhead_pct": 100 * (res["on"] - res["off"]) / res["off"]}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -288,7 +336,7 @@ def main():
     ap.add_argument("--grouped-only", action="store_true",
                     help="time only the grouped step (counter runs: every dispatch after the calibration "
                          "copies belongs to a grouped step)")
-    ap.add_argument("--only", metavar="WORKLOAD", choices=("longctx_bf16", "moe_bf16"),
+    ap.add_argument("--only", metavar="WORKLOAD", choices=("longctx_bf16", "moe_bf16", "full24_bf16"),
                     help="time only this other workload (one JSON line of its fields)")
     ap.add_argument("--top-k2", type=int, default=4, help="branch fan-out of --only moe_bf16")
     ap.add_argument("--kernel-table", metavar="DB", help="print the kernel-duration table of a rocprofv3 database")
@@ -311,6 +359,9 @@ def main():
     from paper_2608_12385_amd import Session
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.only == "full24_bf16":
+        print(json.dumps(time_full24(0)))
+        return
     if args.only:
         kw = {"top_k2": args.top_k2} if args.only == "moe_bf16" else {}
         print(json.dumps(time_workload(args.only, args.steps, args.warmup, **kw)))

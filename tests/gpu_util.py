@@ -43,3 +43,24 @@ def row_err(g, o):
 def near_tie_ok(m_oracle, tok, tol):
     """GPU token acceptable: its oracle mixture value is within tol of the max."""
     return m_oracle[tok] >= np.max(m_oracle) - tol
+
+
+def to_np(t):
+    return t if isinstance(t, np.ndarray) else t.detach().cpu().numpy()
+
+
+def check_readout(t, outs, tol, tag, branch=True):
+    """Logits (per-row relative error), alpha, and greedy tokens (equal, or a
+    certified near-tie of the oracle's mixture) of a step against the oracle."""
+    z1 = np.stack([o["z1"] for o in outs])
+    assert row_err(to_np(t["logits1"]), z1).max() <= tol, (tag, row_err(to_np(t["logits1"]), z1))
+    if branch:
+        z2 = np.stack([o["z2"] for o in outs])
+        assert row_err(to_np(t["logits2"]), z2).max() <= tol, (tag, row_err(to_np(t["logits2"]), z2))
+    alpha = np.array([o["alpha"] for o in outs])
+    np.testing.assert_allclose(to_np(t["alpha"]), alpha, rtol=max(tol, 1e-6), atol=1e-7, err_msg=tag)
+    for i, o in enumerate(outs):
+        tok = int(to_np(t["next_token"])[i])
+        if tok != o["next"]:
+            assert near_tie_ok(o["m"], tok, 10 * tol * np.max(o["m"])), (tag, i, tok, o["next"])
+

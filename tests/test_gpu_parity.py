@@ -9,7 +9,7 @@ import pytest
 
 import synth
 from oracle import Oracle
-from tests.gpu_util import fill_cache, make_session, near_tie_ok, row_err
+from tests.gpu_util import check_readout, fill_cache, make_session, near_tie_ok, row_err, to_np
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -18,22 +18,8 @@ F32_TOL = 1e-5
 BF16_TOL = 2e-2
 
 
-def _np(t):
-    return t if isinstance(t, np.ndarray) else t.detach().cpu().numpy()
-
-
-def _check_readout(t, outs, tol, tag, branch=True):
-    z1 = np.stack([o["z1"] for o in outs])
-    assert row_err(_np(t["logits1"]), z1).max() <= tol, (tag, row_err(_np(t["logits1"]), z1))
-    if branch:
-        z2 = np.stack([o["z2"] for o in outs])
-        assert row_err(_np(t["logits2"]), z2).max() <= tol, (tag, row_err(_np(t["logits2"]), z2))
-    alpha = np.array([o["alpha"] for o in outs])
-    np.testing.assert_allclose(_np(t["alpha"]), alpha, rtol=max(tol, 1e-6), atol=1e-7, err_msg=tag)
-    for i, o in enumerate(outs):
-        tok = int(_np(t["next_token"])[i])
-        if tok != o["next"]:
-            assert near_tie_ok(o["m"], tok, 10 * tol * np.max(o["m"])), (tag, i, tok, o["next"])
+_np = to_np
+_check_readout = check_readout
 
 
 # ----------------------------------------------------------------------------
