@@ -14,9 +14,11 @@
 // k = 8(2p+h) + j, and with V pages stored dim-major each lane loads its V^T
 // operand as one 16-byte piece.  Softmax is online per split (base-2
 // exponent, running max and sum), the four waves of a workgroup merge
-// through LDS, and a combine kernel merges the splits in split order.  The
-// split size is fixed (pages_per_split), so a row's result depends only on
-// its own query and the cache.
+// through LDS, and a combine kernel merges the splits in split order.  A
+// sequence of P pages is read in ceil(P / target) splits of equal size (the
+// last at most one page shorter per split): a function of its own length
+// only, so a row's result depends only on its own query and cache, and equal
+// splits keep the workgroups of a launch equally long.
 #include "common.h"
 #include "kernels.h"
 
@@ -31,6 +33,17 @@ __device__ __forceinline__ uint32_t pack2(float lo, float hi) {
 }
 
 // Zero the bf16 lanes of v (positions first .. first+7) at positions >= nvalid.
+// Split s of a sequence of npages pages: pages [*pb, *pe); false when the
+// sequence has fewer splits.
+__device__ __forceinline__ bool split_range(int npages, int target, int s, int *pb, int *pe) {
+  const int nsplit = (npages + target - 1) / target;
+  if (s >= nsplit) return false;
+  const int pps = (npages + nsplit - 1) / nsplit;
+  *pb = s * pps;
+  *pe = min(npages, *pb + pps);
+  return *pb < *pe;
+}
+
 __device__ __forceinline__ u32x4 mask8(u32x4 v, int first, int nvalid) {
 #pragma unroll
   for (int w = 0; w < 4; ++w) {
@@ -40,15 +53,14 @@ __device__ __forceinline__ u32x4 mask8(u32x4 v, int first, int nvalid) {
   return v;
 }
 
-// Requires d_h == 128, np*G <= 16 and pages_per_split <= 64.
+// Requires d_h == 128, np*G <= 16 and pages_per_split <= 128.
 __global__ __launch_bounds__(256) void k_attn_decode_bf16(AttnArgs a) {
   constexpr int DH = 128;
   const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int len = a.pos_arr[b] + 1;
   const int npages = (len + 15) >> 4;
-  const int pb = split * a.pages_per_split;
-  if (pb >= npages) return;
-  const int pe = min(npages, pb + a.pages_per_split);
+  int pb, pe;
+  if (!split_range(npages, a.pages_per_split, split, &pb, &pe)) return;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r = lane & 15, gq = lane >> 4;
   const int n_kv = a.kv.n_kv;
@@ -56,9 +68,11 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(AttnArgs a) {
   const int nrows = a.rows.np * G;
   const int dq = a.n_q * DH;
   const float scale = kLog2e / sqrtf((float)DH);
-  // page ids of the split: lane i holds page pb + i
+  // page ids of the split: lane i holds pages pb + i and pb + 64 + i
   const int *ptab = a.kv.page_table + (size_t)b * a.kv.mpps;
-  const int myid = (pb + lane < pe) ? ptab[pb + lane] : 0;
+  const int myid0 = (pb + lane < pe) ? ptab[pb + lane] : 0;
+  const int myid1 = (pb + 64 + lane < pe) ? ptab[pb + 64 + lane] : 0;
+  auto page_id = [&](int j) { return __shfl(j < 64 ? myid0 : myid1, j & 63, 64); };
 
   // Query operand: lane (query r, group gq) holds Q[r][s*32 + gq*8 .. +8].
   u32x4 qf[4];
@@ -93,8 +107,8 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(AttnArgs a) {
   for (int q = wave; q < npairs; q += 4) {
     const int pg0 = pb + 2 * q;                 // first page of the pair
     const int last = pe - pb - 1;               // a missing second page re-reads the first (masked)
-    const int phys0 = __shfl(myid, 2 * q, 64);
-    const int phys1 = __shfl(myid, min(2 * q + 1, last), 64);
+    const int phys0 = page_id(2 * q);
+    const int phys1 = page_id(min(2 * q + 1, last));
     const int kphys = kpage ? phys1 : phys0;
     const int vphys = vpage ? phys1 : phys0;
     const uint16_t *kp = kbase + ((size_t)kphys * n_kv + g) * 16 * DH + kpos * DH + gq * 8;
@@ -200,16 +214,16 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(AttnArgs a) {
 
 // fp32 cache: scores in LDS, exact two-pass softmax over the split.
 __global__ __launch_bounds__(256) void k_attn_decode_f32(AttnArgs a) {
-  constexpr int MAXP = 1024;  // positions per split (pages_per_split * 16, pages_per_split <= 64)
+  constexpr int MAXP = 1024;  // positions per split (at most 64 pages)
   __shared__ float qs[16][128];
   __shared__ float sc[16][MAXP];
   __shared__ float red[16];
   const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int len = a.pos_arr[b] + 1;
   const int npages = (len + 15) >> 4;
-  const int pb = split * a.pages_per_split;
-  if (pb >= npages) return;
-  const int p_lo = pb * 16, p_hi = min(len, (pb + a.pages_per_split) * 16);
+  int pb, pe;
+  if (!split_range(npages, a.pages_per_split, split, &pb, &pe)) return;
+  const int p_lo = pb * 16, p_hi = min(len, pe * 16);
   const int np = p_hi - p_lo;
   const int n_kv = a.kv.n_kv, DH = a.kv.d_h;
   const int G = a.n_q / n_kv;
@@ -272,7 +286,7 @@ __global__ void k_attn_combine(AttnArgs a, T *O, int ldo) {
   const int g = blockIdx.x, b = blockIdx.y;
   const int len = a.pos_arr[b] + 1;
   const int npages = (len + 15) >> 4;
-  const int nsplit = (npages + a.pages_per_split - 1) / a.pages_per_split;
+  const int nsplit = (npages + a.pages_per_split - 1) / a.pages_per_split;  // as split_range
   const int n_kv = a.kv.n_kv, DH = a.kv.d_h, Q4 = DH / 4;
   const int G = a.n_q / n_kv;
   const int nrows = a.rows.np * G;
@@ -510,8 +524,8 @@ __global__ __launch_bounds__(256) void k_attn_prefill(const float *Q, int ldq, K
 }  // namespace
 
 hipError_t launch_attn_decode(const AttnArgs &a, hipStream_t st) {
-  // both kernels hold one page id per lane / 16 positions per page in LDS
-  if (a.pages_per_split < 1 || a.pages_per_split > 64) return hipErrorInvalidValue;
+  // the bf16 kernel holds two page ids per lane, the fp32 one 1024 positions in LDS
+  if (a.pages_per_split < 1 || a.pages_per_split > (a.dtype == 1 ? 128 : 64)) return hipErrorInvalidValue;
   dim3 grid(a.max_splits, a.kv.n_kv, a.rows.B);
   if (a.dtype == 1)
     hipLaunchKernelGGL(k_attn_decode_bf16, grid, dim3(256), 0, st, a);

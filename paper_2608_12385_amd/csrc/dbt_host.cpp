@@ -42,7 +42,11 @@ dbt_status fail(dbt_status s, const char *fmt, ...) {
   } while (0)
 
 constexpr int kPage = 16;
-constexpr int kPagesPerSplit = 64;  // attention split: 1024 positions (at most 64: one page id per lane)
+// Decode attention reads a sequence of P pages in ceil(P / target) equal
+// splits; 86 pages (1376 positions) keeps the splits long enough to amortise a
+// workgroup's start, and e.g. 4097 positions (257 pages) in three equal splits.
+// The fp32 kernel holds a split's scores in LDS (at most 64 pages).
+constexpr int kSplitTargetBf16 = 86, kSplitTargetF32 = 64;
 constexpr int kMixChunk = 4096;
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -125,7 +129,8 @@ Layout make_layout(const dbt_config *c) {
     L.g_sd = gemm_config(d, L.fs, c->dtype, d, L.R_max);
   }
   const int maxpages = (c->max_pos + kPage - 1) / kPage;
-  L.max_splits = (maxpages + kPagesPerSplit - 1) / kPagesPerSplit;
+  const int split_target = c->dtype == DBT_BF16 ? kSplitTargetBf16 : kSplitTargetF32;
+  L.max_splits = (maxpages + split_target - 1) / split_target;
   L.nch = c->vocab > 0 ? (c->vocab + kMixChunk - 1) / kMixChunk : 0;
   size_t part = std::max({(size_t)L.g_qkv.S * L.R_max * L.nqkv, (size_t)L.g_o.S * L.R_max * d,
                           (size_t)L.g_gu.S * L.R_max * 2 * L.f, (size_t)L.g_d.S * L.R_max * d});
@@ -520,7 +525,7 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
     aa.pos_arr = m->at<int>(L.pos);
     aa.rows = c.rows;
     aa.n_q = cf.n_q_heads;
-    aa.pages_per_split = kPagesPerSplit;
+    aa.pages_per_split = cf.dtype == DBT_BF16 ? kSplitTargetBf16 : kSplitTargetF32;
     aa.max_splits = L.max_splits;
     aa.opart = m->at<float>(L.apart);
     aa.ostat = m->at<float>(L.astat);

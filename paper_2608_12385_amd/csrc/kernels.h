@@ -137,7 +137,7 @@ struct AttnArgs {
   const int *pos_arr;  // length of sequence b = pos_arr[b] + 1
   Rows rows;
   int n_q;
-  int pages_per_split;
+  int pages_per_split;  // target: a sequence of P pages is read in ceil(P / target) equal splits
   int max_splits;
   float *opart;  // [B][n_kv][max_splits][16][d_h]
   float *ostat;  // [B][n_kv][max_splits][16][2]
