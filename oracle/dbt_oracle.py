@@ -24,8 +24,10 @@ It is written to be read against the paper (arXiv 2608.12385,
   keeps the final position's Q1, H1, M1; one branch evaluation at the final
   prompt position (the boundary); then continuation steps in which the
   primary appends one key/value per layer and both paths query the cache;
-* compute-matched variant, App. B.3: A2 = g_A * A1 and the branch gets
-  g_G * G(N1) instead of its own shared-expert output;
+* compute-matched variant, App. B.3 (MoE): the branch evaluates no
+  attention, A2 = g_A * A1, and its MoE output is its own routed experts
+  plus g_G * G(N1), the gated primary shared-expert output (no other
+  coupling term);
 * more than one decode branch, App. C.1: the branch distributions are
   averaged before the mixture.
 
@@ -394,13 +396,16 @@ class Oracle:
                 idx2, w2 = route(r2, s.top_k2)
             R2 = self._experts(l, U2, idx2, w2)
             if s.compute_matched:
-                G2 = self.w(p + "g_G") * inter["G1"]
-            elif s.n_shared_experts > 0:
-                Hs2 = silu(self.lin(U2, p + "S_gate")) * self.lin(U2, p + "S_up")
-                G2 = self.lin(Hs2 + self.w(p + "b") * inter["H1"], p + "S_down")
+                # App. B.3: the branch's own routed experts plus the gated
+                # primary shared-expert output, nothing else
+                M2 = R2 + self.w(p + "g_G") * inter["G1"]
             else:
-                G2 = np.zeros(s.d_model, self.ft)
-            M2 = R2 + G2 + self.w(p + "c") * inter["M1"]
+                if s.n_shared_experts > 0:
+                    Hs2 = silu(self.lin(U2, p + "S_gate")) * self.lin(U2, p + "S_up")
+                    G2 = self.lin(Hs2 + self.w(p + "b") * inter["H1"], p + "S_down")
+                else:
+                    G2 = np.zeros(s.d_model, self.ft)
+                M2 = R2 + G2 + self.w(p + "c") * inter["M1"]
             out.update(r2=r2, idx2=idx2, w2=w2)
         return Sb2 + M2, out
 

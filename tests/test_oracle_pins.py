@@ -454,6 +454,61 @@ def test_moe_fanouts_independent_and_primary_unaffected():
                 np.testing.assert_array_equal(a["layers"][0]["idx1"], b["layers"][0]["idx1"])
 
 
+def test_compute_matched_unit_gates_and_replay_reduce_branch_to_primary():
+    """App. B.3 with unit gates, the same residual input on both paths and
+    router replay: the gated copies hand the branch exactly the primary's
+    attention and shared-expert outputs and the routed experts coincide, so
+    the branch output equals the primary bit for bit (an extra c * M1 term
+    would break this)."""
+    shape = tiny_moe_shape(compute_matched=True, replay=True, top_k1=2, top_k2=2)
+    P = params(shape)
+    h = synth.make_hidden(shape, 3)
+    orc = Oracle(shape, P)
+    _fill(orc, shape, 3, 13)
+    for o in orc.decode_step(h1=h[0], h2=h[0]):
+        np.testing.assert_array_equal(o["h1"], o["h2"])
+
+
+def test_compute_matched_zero_gates_is_routed_experts_of_own_state():
+    """App. B.3 with g_A = g_G = 0: the branch layer is its residual plus its
+    own routed experts.  That is the primary path of the standard model with
+    the attention output and the shared expert switched off (W_O = 0,
+    S_down = 0) and the same fan-out."""
+    shape = tiny_moe_shape(compute_matched=True, top_k1=3, top_k2=3)
+    P = dict(params(shape))
+    P["L0.g_A"] = np.zeros_like(P["L0.g_A"])
+    P["L0.g_G"] = np.zeros_like(P["L0.g_G"])
+    std = with_shape(shape, compute_matched=False)
+    Q = dict(params(std))
+    Q["L0.W_O"] = np.zeros_like(Q["L0.W_O"])
+    Q["L0.S_down"] = np.zeros_like(Q["L0.S_down"])
+    h = synth.make_hidden(shape, 3)
+    cm, ref = Oracle(shape, P), Oracle(std, Q)
+    _fill(cm, shape, 3, 7)
+    _fill(ref, std, 3, 7)
+    for a, b in zip(cm.decode_step(h1=h[0], h2=h[1]), ref.decode_step(h1=h[1], h2=h[0])):
+        assert rel_err(a["h2"], b["h1"]) < 1e-13
+
+
+def test_compute_matched_branch_never_reads_the_cache():
+    """App. B.3: attention is evaluated once, on the primary path.  Replacing
+    every cached key/value after the primary pass leaves the branch output
+    unchanged."""
+    shape = tiny_moe_shape(compute_matched=True)
+    P = params(shape)
+    h = synth.make_hidden(shape, 2)
+    orc = Oracle(shape, P)
+    _fill(orc, shape, 2, 11)
+    outs = orc.decode_step(h1=h[0], h2=h[1], grouped=False)
+    keep = [o["h2"] for o in outs]
+    for b in range(2):
+        orc.K[0][b] = orc.K[0][b] * 0 + 7.0
+        orc.V[0][b] = orc.V[0][b] * 0 - 3.0
+    for b, o in enumerate(outs):
+        again = orc.branch_layer(0, b, h[1, b].astype(np.float64), len(orc.K[0][b]) - 1, o["layers"][0])[0]
+        np.testing.assert_array_equal(again, keep[b])
+
+
 def test_expert_assignments_brute():
     idx1 = [[0, 3], [3, 1]]
     idx2 = [[3, 2, 0], [1, 0, 2]]
