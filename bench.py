@@ -265,6 +265,7 @@ def time_workload(name, steps, warmup, **shape_kw):
            "branch_overhead_pct": 100 * (res["grouped"] - res["primary"]) / res["primary"]}
     if shape.is_moe:
         rec["k1"], rec["k2"] = shape.top_k1, shape.top_k2
+        rec["compute_matched"] = bool(shape.compute_matched)
         rec["note"] = "bytes depend on the touched experts; see profiles"
     else:
         mlp = 3 * d * shape.d_ff * 2
@@ -339,6 +340,8 @@ def main():
     ap.add_argument("--only", metavar="WORKLOAD", choices=("longctx_bf16", "moe_bf16", "full24_bf16"),
                     help="time only this other workload (one JSON line of its fields)")
     ap.add_argument("--top-k2", type=int, default=4, help="branch fan-out of --only moe_bf16")
+    ap.add_argument("--compute-matched", action="store_true",
+                    help="--only moe_bf16: the compute-matched variant (App. B.3 of the paper)")
     ap.add_argument("--kernel-table", metavar="DB", help="print the kernel-duration table of a rocprofv3 database")
     ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DB", "WRITE_DB"),
                     help="print the calibrated LM-head traffic from two rocprofv3 --pmc databases")
@@ -363,7 +366,7 @@ def main():
         print(json.dumps(time_full24(0)))
         return
     if args.only:
-        kw = {"top_k2": args.top_k2} if args.only == "moe_bf16" else {}
+        kw = {"top_k2": args.top_k2, "compute_matched": args.compute_matched} if args.only == "moe_bf16" else {}
         print(json.dumps(time_workload(args.only, args.steps, args.warmup, **kw)))
         return
     w = synth.workload("layer8b_bf16")
@@ -449,6 +452,7 @@ def main():
         extra = [time_workload("longctx_bf16", args.steps, args.warmup)]
         for k2 in (2, 4, 8):
             extra.append(time_workload("moe_bf16", args.steps, args.warmup, top_k2=k2))
+        extra.append(time_workload("moe_bf16", args.steps, args.warmup, top_k2=2, compute_matched=True))
         line["other_workloads"] = extra
     print(json.dumps(line))
 

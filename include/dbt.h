@@ -75,12 +75,17 @@ enum { DBT_F32 = 0, DBT_BF16 = 1 };
  * primary fan-out top_k1 and branch fan-out top_k2 (Sec. 5, Eq. (22)).
  * replay = 1: the branch reuses the primary's selected experts with its own
  * renormalised router probabilities (Sec. 4.3, Eq. (19)); needs
- * top_k2 = top_k1.  vocab = 0: no output matrix (layer-only models return
- * residual states).  has_embeddings = 0: steps take residual-state inputs
- * instead of tokens. */
+ * top_k2 = top_k1.  compute_matched = 1 (MoE only): the compute-matched
+ * variant of App. B.3, where the branch evaluates no attention and no shared
+ * expert: its attention update is g_A * A1 and its MoE output is its own
+ * routed experts plus g_G * G(N1) (the layer weights g_attn_copy,
+ * g_shared_copy; a and b are unused, and c too).  vocab = 0: no output
+ * matrix (layer-only models return residual states).  has_embeddings = 0:
+ * steps take residual-state inputs instead of tokens. */
 typedef struct {
   int32_t n_layers, d_model, n_q_heads, n_kv_heads, head_dim, d_ff, vocab;
   int32_t n_experts, d_ff_expert, d_ff_shared, top_k1, top_k2, replay;
+  int32_t compute_matched; /* 0 or 1 (App. B.3) */
   int32_t dtype;          /* DBT_F32 or DBT_BF16 */
   int32_t has_embeddings; /* 1: token inputs through E1/E2 */
   int32_t max_batch;      /* sequences per call */
@@ -108,6 +113,8 @@ typedef struct {
   const void *x_down;              /* MoE: [n_experts][d][d_ff_expert] */
   const void *s_gate, *s_up;       /* MoE shared expert: [d_ff_shared][d] */
   const void *s_down;              /* MoE shared expert: [d][d_ff_shared] */
+  const float *g_attn_copy;        /* compute-matched: [d] gate g_A of the attention copy */
+  const float *g_shared_copy;      /* compute-matched: [d] gate g_G of the shared-expert copy */
 } dbt_layer_weights;
 
 typedef struct {

@@ -31,7 +31,7 @@ class DbtError(RuntimeError):
 class dbt_config(ctypes.Structure):
     _fields_ = [(n, I32) for n in (
         "n_layers", "d_model", "n_q_heads", "n_kv_heads", "head_dim", "d_ff", "vocab",
-        "n_experts", "d_ff_expert", "d_ff_shared", "top_k1", "top_k2", "replay",
+        "n_experts", "d_ff_expert", "d_ff_shared", "top_k1", "top_k2", "replay", "compute_matched",
         "dtype", "has_embeddings", "max_batch", "max_pos", "max_prompt")] + [
         ("rms_eps", ctypes.c_float), ("rope_theta", ctypes.c_float)]
 
@@ -39,7 +39,8 @@ class dbt_config(ctypes.Structure):
 class dbt_layer_weights(ctypes.Structure):
     _fields_ = [(n, P) for n in (
         "attn_norm", "wq", "wk", "wv", "wo", "mlp_norm", "w_gate", "w_up", "w_down",
-        "a", "b", "c", "router", "x_gate", "x_up", "x_down", "s_gate", "s_up", "s_down")]
+        "a", "b", "c", "router", "x_gate", "x_up", "x_down", "s_gate", "s_up", "s_down",
+        "g_attn_copy", "g_shared_copy")]
 
 
 class dbt_weights(ctypes.Structure):
@@ -229,7 +230,8 @@ class Session:
             head_dim=s.head_dim, d_ff=s.d_ff, vocab=s.vocab, n_experts=s.n_experts,
             d_ff_expert=s.d_ff_expert, d_ff_shared=s.d_ff_shared * max(0, s.n_shared_experts),
             top_k1=s.top_k1, top_k2=s.top_k2,
-            replay=int(s.replay), dtype=DBT_BF16 if s.dtype == "bf16" else DBT_F32,
+            replay=int(s.replay), compute_matched=int(s.compute_matched),
+            dtype=DBT_BF16 if s.dtype == "bf16" else DBT_F32,
             has_embeddings=int(s.has_embeddings), max_batch=max_batch, max_pos=max_pos,
             max_prompt=max_prompt, rms_eps=s.rms_eps, rope_theta=s.rope_theta)
         self._keep = {}
@@ -239,7 +241,8 @@ class Session:
         names = dict(attn_norm="g_attn", wq="W_Q", wk="W_K", wv="W_V", wo="W_O", mlp_norm="g_mlp",
                      w_gate="W_gate", w_up="W_up", w_down="W_down", a="a", b="b", c="c",
                      router="W_router", x_gate="X_gate", x_up="X_up", x_down="X_down",
-                     s_gate="S_gate", s_up="S_up", s_down="S_down")
+                     s_gate="S_gate", s_up="S_up", s_down="S_down", g_attn_copy="g_A",
+                     g_shared_copy="g_G")
         for l in range(s.n_layers):
             for field, nm in names.items():
                 setattr(self._layers[l], field, _ptr(self._keep.get(f"L{l}.{nm}")))

@@ -63,7 +63,7 @@ struct Layout {
   size_t moe_idx = 0, moe_logits = 0, moe_w = 0, moe_aslot = 0, moe_counts = 0, moe_offsets = 0, moe_arow = 0, moe_h = 0,
          moe_y = 0, ret_idx = 0;
   size_t rope = 0, pos = 0, S = 0, Xn = 0, Xh = 0, Q = 0, O = 0, P = 0, apart = 0, astat = 0,
-         logits = 0, mstats = 0, mcand = 0, ret_q = 0, ret_h = 0, ret_m = 0, btok = 0, slast = 0,
+         logits = 0, mstats = 0, mcand = 0, ret_q = 0, ret_h = 0, ret_m = 0, ret_a = 0, btok = 0, slast = 0,
          total = 0;
 };
 
@@ -85,10 +85,13 @@ dbt_status check_config(const dbt_config *c) {
         c->top_k2 > c->n_experts)
       return fail(DBT_ERR_ARG, "top_k1/top_k2 must be in [1, min(8, n_experts)]");
     if (c->replay && c->top_k2 != c->top_k1) return fail(DBT_ERR_ARG, "router replay needs top_k2 == top_k1");
+    if (c->compute_matched != 0 && c->compute_matched != 1) return fail(DBT_ERR_ARG, "compute_matched must be 0 or 1");
     if (c->d_ff_expert <= 0 || c->d_ff_expert % 128 || c->d_ff_shared < 0 || c->d_ff_shared % 128)
       return fail(DBT_ERR_UNSUPPORTED, "expert widths must be multiples of 128");
   } else if (c->d_ff <= 0) {
     return fail(DBT_ERR_ARG, "d_ff must be positive");
+  } else if (c->compute_matched) {
+    return fail(DBT_ERR_UNSUPPORTED, "the compute-matched variant (App. B.3) is an MoE variant");
   }
   if (c->has_embeddings && c->vocab <= 0) return fail(DBT_ERR_SHAPE, "token inputs need a vocabulary");
   if (c->max_prompt > 0 && !c->has_embeddings) return fail(DBT_ERR_SHAPE, "prefill needs token inputs");
@@ -156,6 +159,7 @@ Layout make_layout(const dbt_config *c) {
   L.ret_q = take((size_t)c->n_layers * L.Bp_max * dq * 4);
   L.ret_h = take((size_t)c->n_layers * L.Bp_max * L.f * 4);
   L.ret_m = take((size_t)c->n_layers * L.Bp_max * d * 4);
+  L.ret_a = take(c->compute_matched ? (size_t)c->n_layers * L.Bp_max * d * 4 : 0);
   if (L.moe) {
     L.amax = L.rows_max * 8;
     L.moe_idx = take((size_t)L.rows_max * 8 * 4);
@@ -412,22 +416,27 @@ dbt_status run_moe_mlp(dbt_model *m, int l, const LayerCall &c, hipStream_t st) 
     g.ldy = d;
     HIPCHK(launch_moe_gemm(g, false, max_rows, st));
   }
-  // shared expert: dense SwiGLU of width fs with the b coupling on its intermediate
+  // shared expert: dense SwiGLU of width fs with the b coupling on its
+  // intermediate; compute-matched variant (App. B.3): primary rows only
+  const bool cm = cf.compute_matched != 0;
+  const Rows srows = cm ? Rows{c.rows.B, c.rows.Bp, 0, 1} : c.rows;
+  const int smode = cm ? (int)MODE_PRIMARY : c.mode;
+  const int sxrow0 = srows.p0 * srows.Bp, sM = srows.np * srows.Bp;
   long long stride = (long long)c.rows_layout * d;
   int S_sh = 0;
-  if (fs > 0) {
+  if (fs > 0 && !(cm && c.mode == MODE_BRANCH)) {
     GemmConfig g_sgu = L.g_sgu, g_sd = L.g_sd;
     if (c.prefill) g_sgu.S = g_sd.S = 1;
     WSegs gu{{W.s_gate, W.s_up, nullptr}, {fs, fs, 0}};
     long long st_gu = (long long)c.rows_layout * 2 * fs;
-    HIPCHK(launch_gemm(gu, 2 * fs, d, cf.dtype, m->ws + L.Xn + (size_t)xrow0 * d * es, d, M,
-                       P + (size_t)xrow0 * 2 * fs, 2 * fs, st_gu, g_sgu, st));
-    HIPCHK(launch_swiglu_finish(P, st_gu, g_sgu.S, 2 * fs, fs, c.mode, c.rows, W.b, ret_h,
-                                Retain{c.retain ? ret_h : nullptr, c.ret_src, c.ret_dst}, cf.dtype, m->ws + L.Xh, fs,
-                                st));
+    HIPCHK(launch_gemm(gu, 2 * fs, d, cf.dtype, m->ws + L.Xn + (size_t)sxrow0 * d * es, d, sM,
+                       P + (size_t)sxrow0 * 2 * fs, 2 * fs, st_gu, g_sgu, st));
+    HIPCHK(launch_swiglu_finish(P, st_gu, g_sgu.S, 2 * fs, fs, smode, srows, W.b, ret_h,
+                                Retain{c.retain && !cm ? ret_h : nullptr, c.ret_src, c.ret_dst}, cf.dtype,
+                                m->ws + L.Xh, fs, st));
     WSegs sd{{W.s_down, nullptr, nullptr}, {d, 0, 0}};
-    HIPCHK(launch_gemm(sd, d, fs, cf.dtype, m->ws + L.Xh + (size_t)xrow0 * fs * es, fs, M, P + (size_t)xrow0 * d, d,
-                       stride, g_sd, st));
+    HIPCHK(launch_gemm(sd, d, fs, cf.dtype, m->ws + L.Xh + (size_t)sxrow0 * fs * es, fs, sM, P + (size_t)sxrow0 * d,
+                       d, stride, g_sd, st));
     S_sh = g_sd.S;
   }
   const float *g_next = nullptr;
@@ -447,8 +456,9 @@ dbt_status run_moe_mlp(dbt_model *m, int l, const LayerCall &c, hipStream_t st) 
   cb.stride = stride;
   cb.S_sh = S_sh;
   cb.c = W.c;
-  cb.M1_in = ret_m;
+  cb.M1_in = ret_m;  // compute-matched: the kept G1
   cb.ret = Retain{c.retain ? ret_m : nullptr, c.ret_src, c.ret_dst};
+  cb.gG = cm ? W.g_shared_copy : nullptr;
   cb.S = S;
   cb.g_next = g_next;
   cb.eps = cf.rms_eps;
@@ -477,11 +487,23 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
   float *ret_q = m->at<float>(L.ret_q) + rq * dq;
   float *ret_h = m->at<float>(L.ret_h) + rq * f;
   float *ret_m = m->at<float>(L.ret_m) + rq * d;
+  // Compute-matched variant (App. B.3): attention runs on the primary rows
+  // only and the branch takes g_A * A1 in the residual step.
+  const bool cm = cf.compute_matched != 0;
+  float *ret_a = cm ? m->at<float>(L.ret_a) + rq * d : nullptr;
+  if (cm && c.mode == MODE_BRANCH) {
+    HIPCHK(launch_resid_norm(P, 0, 0, d, S, W.mlp_norm, cf.rms_eps, d, cf.dtype, c.rows, Xn, d, st,
+                             GatedCopy{W.g_attn_copy, ret_a, Retain{}}));
+    return run_moe_mlp(m, l, c, st);
+  }
+  const Rows arows = cm ? Rows{c.rows.B, c.rows.Bp, 0, 1} : c.rows;
+  const int amode = cm ? (int)MODE_PRIMARY : c.mode;
+  const int axrow0 = arows.p0 * arows.Bp, aM = arows.np * arows.Bp;
 
   // 1. stacked QKV projection (branch rows need only W_Q)
   WSegs qkv{};
   int nq;
-  if (c.mode == MODE_BRANCH) {
+  if (amode == MODE_BRANCH) {
     qkv = WSegs{{W.wq, nullptr, nullptr}, {dq, 0, 0}};
     nq = dq;
   } else {
@@ -491,7 +513,7 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
   long long stride = (long long)c.rows_layout * nq;
   {
     Timed tm(m, DBT_STAGE_QKV, st);
-    HIPCHK(launch_gemm(qkv, nq, d, cf.dtype, Xn + (size_t)xrow0 * d * es, d, M, P + (size_t)xrow0 * nq, nq,
+    HIPCHK(launch_gemm(qkv, nq, d, cf.dtype, Xn + (size_t)axrow0 * d * es, d, aM, P + (size_t)axrow0 * nq, nq,
                        stride, g_qkv, st));
   }
   QKVFinish qf{};
@@ -502,15 +524,15 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
   qf.n_q = cf.n_q_heads;
   qf.n_kv = cf.n_kv_heads;
   qf.d_h = cf.head_dim;
-  qf.rows = c.rows;
-  qf.mode = c.mode;
+  qf.rows = arows;
+  qf.mode = amode;
   qf.rope = m->at<float2>(L.rope);
   qf.pos_arr = c.prefill ? nullptr : m->at<int>(L.pos);
   qf.seq_fixed = c.seq;
   qf.a = W.a;
   qf.Q = Q;
   qf.Q1_in = ret_q;
-  qf.ret = Retain{c.retain ? ret_q : nullptr, c.ret_src, c.ret_dst};
+  qf.ret = Retain{c.retain && !cm ? ret_q : nullptr, c.ret_src, c.ret_dst};
   qf.kv = kvl;
   qf.dtype = cf.dtype;
   HIPCHK(launch_qkv_finish(qf, st));
@@ -523,7 +545,7 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
     aa.Q = Q;
     aa.kv = kvl;
     aa.pos_arr = m->at<int>(L.pos);
-    aa.rows = c.rows;
+    aa.rows = arows;
     aa.n_q = cf.n_q_heads;
     aa.pages_per_split = cf.dtype == DBT_BF16 ? kSplitTargetBf16 : kSplitTargetF32;
     aa.max_splits = L.max_splits;
@@ -542,10 +564,12 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
   stride = (long long)c.rows_layout * d;
   {
     Timed tm(m, DBT_STAGE_WO, st);
-    HIPCHK(launch_gemm(wo, d, dq, cf.dtype, O + (size_t)xrow0 * dq * es, dq, M, P + (size_t)xrow0 * d, d,
+    HIPCHK(launch_gemm(wo, d, dq, cf.dtype, O + (size_t)axrow0 * dq * es, dq, aM, P + (size_t)axrow0 * d, d,
                        stride, g_o, st));
   }
-  HIPCHK(launch_resid_norm(P, stride, S_o, d, S, W.mlp_norm, cf.rms_eps, d, cf.dtype, c.rows, Xn, d, st));
+  const GatedCopy gca = cm ? GatedCopy{W.g_attn_copy, ret_a, Retain{c.retain ? ret_a : nullptr, c.ret_src, c.ret_dst}}
+                           : GatedCopy{};
+  HIPCHK(launch_resid_norm(P, stride, S_o, d, S, W.mlp_norm, cf.rms_eps, d, cf.dtype, c.rows, Xn, d, st, gca));
 
   if (L.moe) return run_moe_mlp(m, l, c, st);
 
@@ -749,6 +773,8 @@ dbt_status dbt_create(const dbt_config *cfg, const dbt_weights *w, void *workspa
       return fail(DBT_ERR_ARG, "layer %d has a NULL expert parameter", l);
     if (cfg->n_experts > 0 && cfg->d_ff_shared > 0 && (!L.s_gate || !L.s_up || !L.s_down || !L.b))
       return fail(DBT_ERR_ARG, "layer %d has a NULL shared-expert parameter", l);
+    if (cfg->compute_matched && (!L.g_attn_copy || !L.g_shared_copy))
+      return fail(DBT_ERR_ARG, "layer %d has a NULL gate of the compute-matched variant", l);
   }
   dbt_model *m = new (std::nothrow) dbt_model();
   if (!m) return fail(DBT_ERR_ARG, "out of host memory");

@@ -214,15 +214,37 @@ __global__ void k_qkv_finish(QKVFinish f) {
 }
 
 // After the attention output projection: S_bar = S + A (in place), then the
-// MLP input RMSNorm.
+// MLP input RMSNorm.  Compute-matched variant (App. B.3): a branch row adds
+// g_A * A1, A1 being the primary row's projection output (both paths in the
+// call) or the kept A1 (branch-only call); primary rows can keep A1.
 template <typename T>
 __global__ void k_resid_norm(const float *part, long long stride, int S, int ldp, float *Sres,
-                             const float *g, float eps, int d, Rows rows, T *Xn, int ldx) {
+                             const float *g, float eps, int d, Rows rows, T *Xn, int ldx, GatedCopy gc) {
   __shared__ float red[16];
-  const int row = phys_row(rows, rows.p0 + blockIdx.y, blockIdx.x);
+  const int b = blockIdx.x, path = rows.p0 + blockIdx.y;
+  const int row = phys_row(rows, path, b);
   float *s = Sres + (size_t)row * d;
-  for (int i = threadIdx.x; i < d / 4; i += blockDim.x)
-    ((float4 *)s)[i] = add4(((float4 *)s)[i], psum4(part, stride, S, ((size_t)row * ldp) / 4 + i));
+  if (!gc.g) {
+    for (int i = threadIdx.x; i < d / 4; i += blockDim.x)
+      ((float4 *)s)[i] = add4(((float4 *)s)[i], psum4(part, stride, S, ((size_t)row * ldp) / 4 + i));
+  } else if (path == 0) {
+    const bool keep = gc.ret.ptr && (gc.ret.src_row < 0 || gc.ret.src_row == b);
+    float4 *kept = keep ? (float4 *)(gc.ret.ptr + (size_t)(gc.ret.src_row < 0 ? b : gc.ret.dst_row) * d) : nullptr;
+    for (int i = threadIdx.x; i < d / 4; i += blockDim.x) {
+      const float4 a1 = psum4(part, stride, S, ((size_t)row * ldp) / 4 + i);
+      ((float4 *)s)[i] = add4(((float4 *)s)[i], a1);
+      if (keep) kept[i] = a1;
+    }
+  } else {
+    const int r1 = phys_row(rows, 0, b);
+    for (int i = threadIdx.x; i < d / 4; i += blockDim.x) {
+      const float4 a1 = rows.np == 2 ? psum4(part, stride, S, ((size_t)r1 * ldp) / 4 + i)
+                                     : ((const float4 *)(gc.in + (size_t)b * d))[i];
+      const float4 ga = ((const float4 *)gc.g)[i];
+      const float4 v = ((float4 *)s)[i];
+      ((float4 *)s)[i] = make_float4(v.x + ga.x * a1.x, v.y + ga.y * a1.y, v.z + ga.z * a1.z, v.w + ga.w * a1.w);
+    }
+  }
   __syncthreads();
   norm_row<T>(s, g, eps, d, Xn + (size_t)row * ldx, red);
 }
@@ -551,14 +573,14 @@ hipError_t launch_qkv_finish(const QKVFinish &f, hipStream_t st) {
 
 hipError_t launch_resid_norm(const float *part, long long stride, int S, int ldp, float *Sres,
                              const float *g, float eps, int d, int dtype, Rows rows, void *Xn, int ldx,
-                             hipStream_t st) {
+                             hipStream_t st, const GatedCopy &gc) {
   dim3 grid(rows.B, rows.np);
   if (dtype == 1)
     hipLaunchKernelGGL(k_resid_norm<uint16_t>, grid, dim3(row_threads(d)), 0, st, part, stride, S, ldp, Sres, g, eps, d,
-                       rows, (uint16_t *)Xn, ldx);
+                       rows, (uint16_t *)Xn, ldx, gc);
   else
     hipLaunchKernelGGL(k_resid_norm<float>, grid, dim3(row_threads(d)), 0, st, part, stride, S, ldp, Sres, g, eps, d,
-                       rows, (float *)Xn, ldx);
+                       rows, (float *)Xn, ldx, gc);
   return hipGetLastError();
 }
 

@@ -117,9 +117,16 @@ struct QKVFinish {
 };
 hipError_t launch_qkv_finish(const QKVFinish &f, hipStream_t st);
 
+// Compute-matched variant (App. B.3): a branch row takes g * (the primary
+// row's value) instead of its own.  g == NULL: the standard model.
+struct GatedCopy {
+  const float *g;   // [d]
+  const float *in;  // [B][d] primary values (branch-only calls)
+  Retain ret;       // keep the primary values for a later branch-only call
+};
 hipError_t launch_resid_norm(const float *part, long long split_stride, int S, int ldp, float *Sres,
-                             const float *g, float eps, int d, int dtype, Rows rows, void *Xn,
-                             int ldx, hipStream_t st);
+                             const float *g, float eps, int d, int dtype, Rows rows, void *Xn, int ldx,
+                             hipStream_t st, const GatedCopy &gc = GatedCopy{});
 
 hipError_t launch_swiglu_finish(const float *part, long long split_stride, int S, int ldp, int f,
                                 int mode, Rows rows, const float *bvec, const float *H1_in,
@@ -219,8 +226,9 @@ struct MoeCombine {
   long long stride;
   int S_sh;
   const float *c;
-  const float *M1_in;
-  Retain ret;
+  const float *M1_in;  // compute-matched: G1 (primary shared-expert output) instead
+  Retain ret;          // compute-matched: keeps G1
+  const float *gG;     // compute-matched variant (App. B.3): branch M2 = R2 + gG * G1; NULL otherwise
   float *S;
   const float *g_next;
   float eps;

@@ -16,6 +16,8 @@
 // 4. k_moe_gemm<DOWN>: the expert down projections of the same rows.
 // 5. k_moe_combine: M_i = sum over selected experts (ascending id) of
 //    w_e * Expert_e(U_i) + shared expert; M2 += c * M1; S += M; next norm.
+//    Compute-matched variant (App. B.3): the shared expert runs on the
+//    primary rows only and M2 = R2 + g_G * G1.
 // Experts no row selected are never read.
 #include "common.h"
 #include "kernels.h"
@@ -431,7 +433,7 @@ __global__ void k_moe_combine(MoeCombine a) {
   float4 *s2 = (float4 *)(a.S + (size_t)r2 * d);
   const bool keep = a.ret.ptr && (a.ret.src_row < 0 || a.ret.src_row == b);
   float4 *kept = keep ? (float4 *)(a.ret.ptr + (size_t)(a.ret.src_row < 0 ? b : a.ret.dst_row) * d) : nullptr;
-  auto routed = [&](int p, int k, int row, int i) {
+  auto experts = [&](int p, int k, int i) {  // routed experts, ascending id
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     for (int j = 0; j < k; ++j) {
       const float4 y = ((const float4 *)(a.Yexp + (size_t)sl[p][j] * d))[i];
@@ -441,6 +443,9 @@ __global__ void k_moe_combine(MoeCombine a) {
       acc.z += w * y.z;
       acc.w += w * y.w;
     }
+    return acc;
+  };
+  auto shared = [&](int row, int i) {  // shared-expert slabs in split order
     float4 sh = make_float4(0.f, 0.f, 0.f, 0.f);
     for (int q = 0; q < a.S_sh; ++q) {
       const float4 v = ((const float4 *)(a.part + q * a.stride + (size_t)row * d))[i];
@@ -449,24 +454,34 @@ __global__ void k_moe_combine(MoeCombine a) {
       sh.z += v.z;
       sh.w += v.w;
     }
-    return make_float4(acc.x + sh.x, acc.y + sh.y, acc.z + sh.z, acc.w + sh.w);
+    return sh;
   };
+  const bool cm = a.gG != nullptr;  // compute-matched variant (App. B.3)
   for (int i = threadIdx.x; i < d4; i += blockDim.x) {
-    float4 m1;
+    float4 m1, g1;  // primary MoE output; primary shared-expert output
     if (prim) {
-      m1 = routed(0, a.k1, r1, i);
+      const float4 r = experts(0, a.k1, i);
+      g1 = shared(r1, i);
+      m1 = make_float4(r.x + g1.x, r.y + g1.y, r.z + g1.z, r.w + g1.w);
       const float4 s = s1[i];
       s1[i] = make_float4(s.x + m1.x, s.y + m1.y, s.z + m1.z, s.w + m1.w);
-      if (keep) kept[i] = m1;
+      if (keep) kept[i] = cm ? g1 : m1;
     } else {
-      m1 = ((const float4 *)(a.M1_in + (size_t)b * d))[i];
+      m1 = g1 = ((const float4 *)(a.M1_in + (size_t)b * d))[i];
     }
     if (br) {
-      const float4 m2 = routed(1, a.k2, r2, i);
-      const float4 c = ((const float4 *)a.c)[i];
+      const float4 r = experts(1, a.k2, i);
       const float4 s = s2[i];
-      s2[i] = make_float4(s.x + (m2.x + c.x * m1.x), s.y + (m2.y + c.y * m1.y), s.z + (m2.z + c.z * m1.z),
-                          s.w + (m2.w + c.w * m1.w));
+      if (cm) {  // M2 = R2 + g_G * G1
+        const float4 gg = ((const float4 *)a.gG)[i];
+        s2[i] = make_float4(s.x + (r.x + gg.x * g1.x), s.y + (r.y + gg.y * g1.y), s.z + (r.z + gg.z * g1.z),
+                            s.w + (r.w + gg.w * g1.w));
+      } else {   // M2 = R2 + shared expert of the branch + c * M1
+        const float4 g2 = shared(r2, i);
+        const float4 c = ((const float4 *)a.c)[i];
+        s2[i] = make_float4(s.x + ((r.x + g2.x) + c.x * m1.x), s.y + ((r.y + g2.y) + c.y * m1.y),
+                            s.z + ((r.z + g2.z) + c.z * m1.z), s.w + ((r.w + g2.w) + c.w * m1.w));
+      }
     }
   }
   if (!a.g_next) return;
