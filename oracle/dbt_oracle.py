@@ -302,8 +302,9 @@ class Oracle:
     # ---------------- pieces of one layer ----------------
 
     def embed(self, tok, path):
-        """Eq. (7): RMSNorm of the path's own embedding row."""
-        table = "E1" if path == 0 else "E2"
+        """Eq. (7): RMSNorm of the path's own embedding row (path j >= 1 is
+        decode branch j, table E_{j+1}; App. C.1 for j >= 2)."""
+        table = f"E{path + 1}"
         e = np.asarray(self.P[table][tok]).astype(self.ft)
         return rmsnorm(e, self.w("g_emb"), self.s.rms_eps)
 
@@ -416,11 +417,19 @@ class Oracle:
     # ---------------- one sequence, one position ----------------
 
     def _inputs(self, b, token, h1, h2):
+        """Residual inputs of one position: S1, and S2 (one branch) or a list
+        of branch states (more branches; h2 then [n_branches][d])."""
+        nb = self.s.n_branches
         if token is not None:
-            return self.embed(token, 0), self.embed(token, 1)
+            if nb == 1:
+                return self.embed(token, 0), self.embed(token, 1)
+            return self.embed(token, 0), [self.embed(token, j) for j in range(1, nb + 1)]
         S1 = np.asarray(h1).astype(self.ft)
-        S2 = None if h2 is None else np.asarray(h2).astype(self.ft)
-        return S1, S2
+        if h2 is None:
+            return S1, None
+        if nb == 1:
+            return S1, np.asarray(h2).astype(self.ft)
+        return S1, [np.asarray(h2[j]).astype(self.ft) for j in range(nb)]
 
     def step_one(self, b, token=None, h1=None, h2=None, branch_on=True, grouped=True, readout=True):
         """Continuation step of Sec. 4.4 for sequence b at t = current length.
@@ -433,26 +442,37 @@ class Oracle:
         S1, S2 = self._inputs(b, token, h1, h2)
         if not branch_on:
             S2 = None
+        many = isinstance(S2, list)          # more decode branches (App. C.1)
+        Sb = S2 if many else ([S2] if S2 is not None else [])
         per_layer = []
-        if grouped or S2 is None:
+        if grouped or not Sb:
             for l in range(s.n_layers):
                 S1, inter = self.primary_layer(l, b, S1, pos)
                 rec = dict(inter)
-                if S2 is not None:
-                    S2, bo = self.branch_layer(l, b, S2, pos, inter)
-                    rec.update(bo)
+                bos = []
+                for j in range(len(Sb)):     # every branch reads the same primary state
+                    Sb[j], bo = self.branch_layer(l, b, Sb[j], pos, inter)
+                    bos.append(bo)
+                if bos:
+                    rec.update(bos[0])
+                    rec["branches"] = bos
                 per_layer.append(rec)
         else:
             inters = []
             for l in range(s.n_layers):
                 S1, inter = self.primary_layer(l, b, S1, pos)
                 inters.append(inter)
-            for l in range(s.n_layers):
-                S2, bo = self.branch_layer(l, b, S2, pos, inters[l])
-                rec = dict(inters[l])
-                rec.update(bo)
-                per_layer.append(rec)
-        out = dict(h1=S1, h2=S2, layers=per_layer, pos=pos, branch_on=S2 is not None)
+            recs = [dict(inters[l]) for l in range(s.n_layers)]
+            for j in range(len(Sb)):
+                for l in range(s.n_layers):
+                    Sb[j], bo = self.branch_layer(l, b, Sb[j], pos, inters[l])
+                    if j == 0:
+                        recs[l].update(bo)
+                    recs[l].setdefault("branches", []).append(bo)
+            per_layer = recs
+        out = dict(h1=S1, h2=Sb[0] if Sb else None, layers=per_layer, pos=pos, branch_on=bool(Sb))
+        if many:
+            out["hb"] = Sb
         if readout:
             self._readout([out])
         return out
@@ -469,10 +489,14 @@ class Oracle:
         for i, o in enumerate(outs):
             z1 = Z1[i]
             z2 = None
+            zb = None
             if o["h2"] is not None:
                 z2 = Z2[j]
                 j += 1
-            alpha, m, nxt = mixture_readout(z1, z2, branch_on=z2 is not None)
+                if "hb" in o:   # more branches: q is the mean branch softmax (App. C.1)
+                    zb = [z2] + [self.logits(h) for h in o["hb"][1:]]
+                    o["zb"] = zb
+            alpha, m, nxt = mixture_readout(z1, z2, branch_on=z2 is not None, z_branches=zb)
             o.update(z1=z1, z2=z2, alpha=alpha, m=m, next=nxt)
 
     # ---------------- batched entry points ----------------
@@ -489,7 +513,7 @@ class Oracle:
                 b,
                 token=None if tokens is None else int(tokens[b]),
                 h1=None if h1 is None else h1[b],
-                h2=None if h2 is None else h2[b],
+                h2=None if h2 is None else (h2[b] if self.s.n_branches == 1 else [h[b] for h in h2]),
                 branch_on=branch_on, grouped=grouped, readout=False))
         self._readout(outs)
         return outs
@@ -524,19 +548,28 @@ class Oracle:
         step 2), using the retained primary intermediates; writes no cache."""
         ret = self.retained[b]
         pos = ret["pos"]
-        S2 = self.embed(ret["token"], 1)
+        nb = self.s.n_branches
+        Sb = [self.embed(ret["token"], j) for j in range(1, nb + 1)]
         per_layer = []
         for l in range(self.s.n_layers):
-            S2, bo = self.branch_layer(l, b, S2, pos, ret["layers"][l])
             rec = dict(ret["layers"][l])
-            rec.update(bo)
+            bos = []
+            for j in range(nb):
+                Sb[j], bo = self.branch_layer(l, b, Sb[j], pos, ret["layers"][l])
+                bos.append(bo)
+            rec.update(bos[0])
+            rec["branches"] = bos
             per_layer.append(rec)
-        out = dict(h1=ret["h1"], h2=S2, layers=per_layer, pos=pos)
+        out = dict(h1=ret["h1"], h2=Sb[0], layers=per_layer, pos=pos)
+        if nb > 1:
+            out["hb"] = Sb
         if self.s.vocab > 0:
             z1 = ret["z1"]
-            z2 = self.logits(S2)
-            alpha, m, nxt = mixture_readout(z1, z2, branch_on=True)
-            out.update(z1=z1, z2=z2, alpha=alpha, m=m, next=nxt)
+            zb = [self.logits(h) for h in Sb]
+            alpha, m, nxt = mixture_readout(z1, zb[0], branch_on=True, z_branches=zb if nb > 1 else None)
+            out.update(z1=z1, z2=zb[0], alpha=alpha, m=m, next=nxt)
+            if nb > 1:
+                out["zb"] = zb
         return out
 
     # ---------------- full-sequence (masked matrix) form ----------------

@@ -13,6 +13,7 @@ even) and both sides receive exactly those values: the device gets the
 
 Tensor ids (fixed, documented order):
     0 E1 (primary embedding)   1 E2 (branch embedding)   2 W_out (LM head)
+    10 + j: E_j, the embedding of decode branch j - 1 for j >= 3 (more branches)
     per layer l, base = 1000 + 100*l:
     +0 W_Q  +1 W_K  +2 W_V  +3 W_O  +4 W_gate  +5 W_up  +6 W_down
     +7 a    +8 b    +9 c    +10 W_router
@@ -190,6 +191,8 @@ def make_weights(shape: ModelShape, seed: int = 0, coupling_std=None, skip_lm_he
     if s.has_embeddings:
         w._matrix("E1", seed, 0, (s.vocab, s.d_model), s.std)
         w._matrix("E2", seed, 1, (s.vocab, s.d_model), s.std)
+        for j in range(3, s.n_branches + 2):
+            w._matrix(f"E{j}", seed, 10 + j, (s.vocab, s.d_model), s.std)
         w._ones("g_emb", s.d_model)
     if s.vocab > 0:
         if not skip_lm_head:

@@ -117,6 +117,18 @@ def test_mixture_readout_golden():
         assert abs(np.sum(m) - 1.0) < 1e-12
 
 
+def test_mixture_with_several_branches_golden():
+    """App. C.1: hand-worked cases of the averaged branch distribution."""
+    for c in _golden("mixture_branches_cases.json")["cases"]:
+        z1 = np.log(c["p"])
+        zb = [np.log(q) for q in c["q"]]
+        alpha, m, nxt = mixture_readout(z1, zb[0], z_branches=zb)
+        assert abs(alpha - c["alpha"]) < 1e-12
+        np.testing.assert_allclose(np.mean([softmax(z) for z in zb], axis=0), c["q_bar"], rtol=1e-12)
+        np.testing.assert_allclose(m, c["m"], rtol=1e-12, atol=1e-15)
+        assert nxt == c["next"]
+
+
 def test_mixture_readout_limits():
     V = 1000
     # near one-hot primary: alpha -> 1, prediction -> p
@@ -515,3 +527,72 @@ def test_expert_assignments_brute():
     got = expert_assignments(idx1, idx2, 4)
     assert got == [[(0, 0), (1, 0), (1, 1)], [(0, 1), (1, 1)], [(1, 0), (1, 1)],
                    [(0, 0), (0, 1), (1, 0)]]
+
+
+def test_more_branches_identical_tables_give_the_one_branch_model():
+    """App. C.1: two decode branches whose embeddings are equal (E3 := E2)
+    compute the same state; their mean distribution is that branch's own, so
+    every output of the one-branch model is reproduced exactly."""
+    one = tiny_shape(n_layers=2)
+    two = with_shape(one, n_branches=2)
+    P1 = params(one)
+    P2 = dict(params(two))
+    P2["E3"] = P2["E2"]
+    x = synth.make_tokens(1, 3, (9,), one.vocab)
+    o1, o2 = Oracle(one, P1), Oracle(two, P2)
+    b1 = o1.prefill([x])[0]
+    b2 = o2.prefill([x])[0]
+    for key in ("z1", "z2", "alpha", "next"):
+        np.testing.assert_array_equal(b1[key], b2[key])
+    tok = b1["next"]
+    for _ in range(3):
+        s1 = o1.decode_step(tokens=[tok])[0]
+        s2 = o2.decode_step(tokens=[tok])[0]
+        np.testing.assert_array_equal(s2["hb"][0], s2["hb"][1])
+        for key in ("h1", "h2", "z1", "z2", "alpha", "next"):
+            np.testing.assert_array_equal(s1[key], s2[key])
+        np.testing.assert_allclose(s1["m"], s2["m"], rtol=1e-15, atol=0)
+        tok = s1["next"]
+
+
+def test_more_branches_each_branch_is_the_one_branch_model_with_its_table():
+    """App. C.1: branch j has its own embedding and the shared couplings and
+    reads only the primary: branch 2 of a three-path model equals the single
+    branch of the model whose E2 is that branch's table; the primary is the
+    same in all of them."""
+    two = tiny_shape(n_layers=2, n_branches=2)
+    P2 = params(two)
+    one = with_shape(two, n_branches=1)
+    P1 = dict(P2)
+    P1["E2"] = P2["E3"]
+    P1.pop("E3")
+    x = synth.make_tokens(1, 4, (7,), two.vocab)
+    o1, o2 = Oracle(one, P1), Oracle(two, P2)
+    o1.prefill([x], run_boundary=False)
+    o2.prefill([x], run_boundary=False)
+    for tok in (5, 11):
+        s1 = o1.decode_step(tokens=[tok])[0]
+        s2 = o2.decode_step(tokens=[tok])[0]
+        np.testing.assert_array_equal(s1["h1"], s2["h1"])
+        np.testing.assert_array_equal(s1["h2"], s2["hb"][1])
+        np.testing.assert_array_equal(s1["z2"], s2["zb"][1])
+
+
+def test_more_branches_leave_the_primary_and_cache_untouched():
+    """Adding decode branches changes nothing on the primary path or in the
+    cache (Sec. 4.4 for each branch; App. C.1)."""
+    ref = None
+    for nb in (1, 2, 3):
+        shape = tiny_shape(n_layers=2, n_branches=nb)
+        orc = Oracle(shape, params(shape))
+        x = synth.make_tokens(1, 5, (6,), shape.vocab)
+        orc.prefill([x])
+        outs = [orc.decode_step(tokens=[t])[0] for t in (3, 9)]
+        got = ([o["h1"] for o in outs], [o["z1"] for o in outs], [np.array(orc.K[l][0]) for l in range(2)])
+        if ref is None:
+            ref = got
+        else:
+            for a, b in zip(ref, got):
+                for u, v in zip(a, b):
+                    np.testing.assert_array_equal(u, v)
+
