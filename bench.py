@@ -237,9 +237,10 @@ def time_workload(name, steps, warmup, **shape_kw):
         (_, kb), (_, vb) = synth.make_kv(shape, 0, b, L, seed=3)
         sess.reserve_fill(b, [kb], [vb])
     del W
-    h = synth.make_hidden(shape, B, step=0, seed=2)
+    nb = max(1, shape.n_branches)
+    h = synth.make_hidden(shape, B, step=0, seed=2, paths=1 + nb)
     h1d = torch.from_numpy(np.ascontiguousarray(h[0])).cuda()
-    h2d = torch.from_numpy(np.ascontiguousarray(h[1])).cuda()
+    h2d = torch.from_numpy(np.ascontiguousarray(h[1] if nb == 1 else h[1:])).cuda()
     from paper_2608_12385_amd import binding
     res = {}
     for mode in ("grouped", "primary"):
@@ -263,14 +264,17 @@ def time_workload(name, steps, warmup, **shape_kw):
     kv = sum(L + 1 for L in lengths) * 2 * dkv * 2
     rec = {"workload": name, "batch": B, "grouped_us": res["grouped"] * 1e6, "primary_only_us": res["primary"] * 1e6,
            "branch_overhead_pct": 100 * (res["grouped"] - res["primary"]) / res["primary"]}
+    if nb > 1:
+        rec["n_branches"] = nb
     if shape.is_moe:
         rec["k1"], rec["k2"] = shape.top_k1, shape.top_k2
         rec["compute_matched"] = bool(shape.compute_matched)
         rec["note"] = "bytes depend on the touched experts; see profiles"
     else:
         mlp = 3 * d * shape.d_ff * 2
-        rec["algorithmic_MB"] = (attn_w + mlp + kv) / 1e6
-        rec["GBps"] = (attn_w + mlp + kv) / res["grouped"] / 1e9
+        head = shape.vocab * d * 2
+        rec["algorithmic_MB"] = (attn_w + mlp + head + kv) / 1e6
+        rec["GBps"] = (attn_w + mlp + head + kv) / res["grouped"] / 1e9
     return rec
 
 
@@ -337,9 +341,11 @@ def main():
     ap.add_argument("--grouped-only", action="store_true",
                     help="time only the grouped step (counter runs: every dispatch after the calibration "
                          "copies belongs to a grouped step)")
-    ap.add_argument("--only", metavar="WORKLOAD", choices=("longctx_bf16", "moe_bf16", "full24_bf16"),
+    ap.add_argument("--only", metavar="WORKLOAD", choices=("layer8b_bf16", "longctx_bf16", "moe_bf16", "full24_bf16"),
                     help="time only this other workload (one JSON line of its fields)")
     ap.add_argument("--top-k2", type=int, default=4, help="branch fan-out of --only moe_bf16")
+    ap.add_argument("--branches", type=int, default=1,
+                    help="--only layer8b_bf16/longctx_bf16: decode branches (App. C.1 of the paper)")
     ap.add_argument("--compute-matched", action="store_true",
                     help="--only moe_bf16: the compute-matched variant (App. B.3 of the paper)")
     ap.add_argument("--kernel-table", metavar="DB", help="print the kernel-duration table of a rocprofv3 database")
@@ -366,7 +372,8 @@ def main():
         print(json.dumps(time_full24(0)))
         return
     if args.only:
-        kw = {"top_k2": args.top_k2, "compute_matched": args.compute_matched} if args.only == "moe_bf16" else {}
+        kw = ({"top_k2": args.top_k2, "compute_matched": args.compute_matched} if args.only == "moe_bf16"
+              else {"n_branches": args.branches})
         print(json.dumps(time_workload(args.only, args.steps, args.warmup, **kw)))
         return
     w = synth.workload("layer8b_bf16")
@@ -453,6 +460,8 @@ def main():
         for k2 in (2, 4, 8):
             extra.append(time_workload("moe_bf16", args.steps, args.warmup, top_k2=k2))
         extra.append(time_workload("moe_bf16", args.steps, args.warmup, top_k2=2, compute_matched=True))
+        for nb in (2, 3):
+            extra.append(time_workload("layer8b_bf16", args.steps, args.warmup, n_branches=nb))
         line["other_workloads"] = extra
     print(json.dumps(line))
 

@@ -81,11 +81,17 @@ enum { DBT_F32 = 0, DBT_BF16 = 1 };
  * routed experts plus g_G * G(N1) (the layer weights g_attn_copy,
  * g_shared_copy; a and b are unused, and c too).  vocab = 0: no output
  * matrix (layer-only models return residual states).  has_embeddings = 0:
- * steps take residual-state inputs instead of tokens. */
+ * steps take residual-state inputs instead of tokens.  n_branches > 1
+ * (App. C.1): branch j has its own embedding table and shares the couplings
+ * a, b, c and every weight; each branch reads only the primary (its Q1, H1,
+ * M1 and cache); the mixture's q is the mean of the branch softmaxes.  The
+ * branch tables, inputs and outputs below are then stacked [n_branches][...]
+ * in branch order.  Needs (1 + n_branches) * n_q_heads / n_kv_heads <= 16. */
 typedef struct {
   int32_t n_layers, d_model, n_q_heads, n_kv_heads, head_dim, d_ff, vocab;
   int32_t n_experts, d_ff_expert, d_ff_shared, top_k1, top_k2, replay;
   int32_t compute_matched; /* 0 or 1 (App. B.3) */
+  int32_t n_branches;      /* decode branches, 0..3 (0 reads as 1; > 1: App. C.1, dense only) */
   int32_t dtype;          /* DBT_F32 or DBT_BF16 */
   int32_t has_embeddings; /* 1: token inputs through E1/E2 */
   int32_t max_batch;      /* sequences per call */
@@ -118,7 +124,8 @@ typedef struct {
 } dbt_layer_weights;
 
 typedef struct {
-  const void *emb1, *emb2;   /* [vocab][d]: primary and branch embeddings, Eq. (7) */
+  const void *emb1;          /* [vocab][d]: primary embedding, Eq. (7) */
+  const void *emb2;          /* [n_branches][vocab][d]: branch embeddings, Eq. (7) */
   const float *emb_norm;     /* [d] gain of the embedding RMSNorm */
   const float *final_norm;   /* [d] */
   const void *lm_head;       /* [vocab][d]: shared output matrix (Sec. 4.2) */
@@ -129,17 +136,19 @@ typedef struct {
 typedef struct {
   const int32_t *tokens; /* [batch] (models with embeddings), else NULL */
   const float *h1_in;    /* [batch][d] primary residual input (layer-only models) */
-  const float *h2_in;    /* [batch][d] branch residual input (layer-only models) */
+  const float *h2_in;    /* [n_branches][batch][d] branch residual inputs (layer-only models) */
   int32_t batch;
 } dbt_step_in;
 
 /* Outputs of a step; any pointer may be NULL.  Routing arrays are
  * [n_layers][batch][top_k] in the order selected (logit descending). */
 typedef struct {
-  float *logits1, *logits2; /* [batch][vocab] */
+  float *logits1;           /* [batch][vocab] */
+  float *logits2;           /* [n_branches][batch][vocab] */
   float *alpha;             /* [batch] mixture weight (1 with the branch off) */
   int32_t *next_token;      /* [batch] greedy token of the mixture */
-  float *h1_out, *h2_out;   /* [batch][d] final residual states */
+  float *h1_out;            /* [batch][d] final primary residual state */
+  float *h2_out;            /* [n_branches][batch][d] final branch residual states */
   int32_t *route_idx1, *route_idx2;
   float *route_w1, *route_w2;
 } dbt_step_out;

@@ -32,7 +32,7 @@ class dbt_config(ctypes.Structure):
     _fields_ = [(n, I32) for n in (
         "n_layers", "d_model", "n_q_heads", "n_kv_heads", "head_dim", "d_ff", "vocab",
         "n_experts", "d_ff_expert", "d_ff_shared", "top_k1", "top_k2", "replay", "compute_matched",
-        "dtype", "has_embeddings", "max_batch", "max_pos", "max_prompt")] + [
+        "n_branches", "dtype", "has_embeddings", "max_batch", "max_pos", "max_prompt")] + [
         ("rms_eps", ctypes.c_float), ("rope_theta", ctypes.c_float)]
 
 
@@ -216,6 +216,8 @@ class Session:
         E1, E2, g_emb, g_final, W_out,
         L{l}.g_attn, L{l}.W_Q, L{l}.W_K, L{l}.W_V, L{l}.W_O, L{l}.g_mlp,
         L{l}.W_gate, L{l}.W_up, L{l}.W_down, L{l}.a, L{l}.b, L{l}.c.
+    With n_branches > 1 the branch tables E2, E3, ... are stacked in branch
+    order, and branch outputs/inputs are [n_branches][batch][...].
     """
 
     def __init__(self, shape, device_params, max_batch, max_pos, max_prompt=0, num_pages=None,
@@ -231,12 +233,19 @@ class Session:
             d_ff_expert=s.d_ff_expert, d_ff_shared=s.d_ff_shared * max(0, s.n_shared_experts),
             top_k1=s.top_k1, top_k2=s.top_k2,
             replay=int(s.replay), compute_matched=int(s.compute_matched),
+            n_branches=int(getattr(s, "n_branches", 1)),
             dtype=DBT_BF16 if s.dtype == "bf16" else DBT_F32,
             has_embeddings=int(s.has_embeddings), max_batch=max_batch, max_pos=max_pos,
             max_prompt=max_prompt, rms_eps=s.rms_eps, rope_theta=s.rope_theta)
+        self.n_branches = max(1, int(getattr(s, "n_branches", 1)))
         self._keep = {}
         for name, arr in device_params.items():
+            if self.n_branches > 1 and name.startswith("E") and name[1:].isdigit() and name != "E1":
+                continue
             self._keep[name] = self._upload(arr)
+        if self.n_branches > 1 and "E2" in device_params:
+            self._keep["E2"] = self._upload(np.stack(
+                [device_params[f"E{j + 2}"] for j in range(self.n_branches)]))
         self._layers = (dbt_layer_weights * s.n_layers)()
         names = dict(attn_norm="g_attn", wq="W_Q", wk="W_K", wv="W_V", wo="W_O", mlp_norm="g_mlp",
                      w_gate="W_gate", w_up="W_up", w_down="W_down", a="a", b="b", c="c",
@@ -274,6 +283,10 @@ class Session:
             a = a.view(np.int16)
         return torch.from_numpy(a).to(self.device)
 
+    def _br(self, *shape):
+        """Shape of a branch output: [n_branches] leads only with several."""
+        return shape if self.n_branches == 1 else (self.n_branches,) + shape
+
     @property
     def stream(self):
         return self.torch.cuda.current_stream().cuda_stream
@@ -299,13 +312,13 @@ class Session:
         t = {}
         if logits and s.vocab > 0:
             t["logits1"] = torch.empty(batch, s.vocab, dtype=torch.float32, device=self.device)
-            t["logits2"] = torch.empty(batch, s.vocab, dtype=torch.float32, device=self.device)
+            t["logits2"] = torch.empty(*self._br(batch, s.vocab), dtype=torch.float32, device=self.device)
         if s.vocab > 0:
             t["alpha"] = torch.empty(batch, dtype=torch.float32, device=self.device)
             t["next_token"] = torch.empty(batch, dtype=torch.int32, device=self.device)
         if hidden:
             t["h1_out"] = torch.empty(batch, s.d_model, dtype=torch.float32, device=self.device)
-            t["h2_out"] = torch.empty(batch, s.d_model, dtype=torch.float32, device=self.device)
+            t["h2_out"] = torch.empty(*self._br(batch, s.d_model), dtype=torch.float32, device=self.device)
         if routing and s.n_experts > 0:
             k2 = s.top_k1 if s.replay else s.top_k2
             L = s.n_layers

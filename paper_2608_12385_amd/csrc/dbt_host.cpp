@@ -51,6 +51,8 @@ constexpr int kMixChunk = 4096;
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 int round16(int x) { return (x + 15) / 16 * 16; }
+// Decode branches (App. C.1 for more than one); 0 reads as one branch.
+int n_branches(const dbt_config &c) { return c.n_branches > 1 ? c.n_branches : 1; }
 
 // Offsets (bytes) of every workspace buffer.
 struct Layout {
@@ -96,8 +98,11 @@ dbt_status check_config(const dbt_config *c) {
   if (c->has_embeddings && c->vocab <= 0) return fail(DBT_ERR_SHAPE, "token inputs need a vocabulary");
   if (c->max_prompt > 0 && !c->has_embeddings) return fail(DBT_ERR_SHAPE, "prefill needs token inputs");
   if (!(c->rms_eps >= 0.f) || !(c->rope_theta > 0.f)) return fail(DBT_ERR_ARG, "bad rms_eps/rope_theta");
-  const int G = c->n_q_heads / c->n_kv_heads;
-  if (2 * G > 16) return fail(DBT_ERR_UNSUPPORTED, "more than 8 query heads per KV head");
+  if (c->n_branches < 0 || c->n_branches > 3) return fail(DBT_ERR_ARG, "n_branches must be in [0, 3]");
+  if (c->n_branches > 1 && c->n_experts > 0)
+    return fail(DBT_ERR_UNSUPPORTED, "more than one decode branch runs with dense MLPs only");
+  const int G = c->n_q_heads / c->n_kv_heads, P = 1 + n_branches(*c);
+  if (P * G > 16) return fail(DBT_ERR_UNSUPPORTED, "(1 + n_branches) * query heads per KV head exceeds 16");
   if (c->head_dim > 128) return fail(DBT_ERR_UNSUPPORTED, "head_dim > 128");
   if (c->dtype == DBT_BF16) {
     const int dq = c->n_q_heads * c->head_dim, dkv = c->n_kv_heads * c->head_dim;
@@ -117,7 +122,7 @@ Layout make_layout(const dbt_config *c) {
   L.fs = L.moe ? c->d_ff_shared : 0;
   L.f = L.moe ? std::max(L.fs, 128) : c->d_ff;
   L.Bp_max = round16(c->max_batch);
-  L.R_max = 2 * L.Bp_max;
+  L.R_max = (1 + n_branches(*c)) * L.Bp_max;
   L.rows_max = std::max(L.R_max, c->max_prompt);
   L.max_in = std::max(std::max(d, dq), L.f);
   L.nqkv = dq + 2 * dkv;
@@ -323,7 +328,7 @@ struct LayerCall {
   int ret_src, ret_dst;
   bool prefill;
   int seq;           // prefill: the sequence
-  int rows_layout;   // prefill: T; decode: 2*Bp
+  int rows_layout;   // prefill: T; decode: (1 + n_branches)*Bp
   bool last_norm;    // apply the next norm after the layer
   const dbt_step_out *out;  // routing outputs (MoE), may be NULL
 };
@@ -649,7 +654,8 @@ dbt_status readout(dbt_model *m, int B, int Bp, bool branch, dbt_step_out *out, 
   MixArgs mx{};
   mx.logits = m->at<float>(L.logits);
   mx.V = cf.vocab;
-  mx.rows = Rows{B, Bp, 0, branch ? 2 : 1};
+  const int nb = n_branches(cf);
+  mx.rows = Rows{B, Bp, 0, branch ? 1 + nb : 1};
   mx.chunk = kMixChunk;
   mx.stats = m->at<float>(L.mstats);
   mx.stats_ready = gemm_stats_tiles(cf.vocab, L.g_lm, cf.dtype) > 0;
@@ -664,7 +670,18 @@ dbt_status readout(dbt_model *m, int B, int Bp, bool branch, dbt_step_out *out, 
   if (out && out->logits1)
     HIPCHK(hipMemcpyAsync(out->logits1, m->at<float>(L.logits), (size_t)B * cf.vocab * 4, hipMemcpyDeviceToDevice, st));
   if (out && out->logits2 && branch)
-    HIPCHK(hipMemcpyAsync(out->logits2, m->at<float>(L.logits) + (size_t)Bp * cf.vocab, (size_t)B * cf.vocab * 4,
+    for (int j = 0; j < nb; ++j)
+      HIPCHK(hipMemcpyAsync(out->logits2 + (size_t)j * B * cf.vocab, m->at<float>(L.logits) + (size_t)(1 + j) * Bp * cf.vocab,
+                            (size_t)B * cf.vocab * 4, hipMemcpyDeviceToDevice, st));
+  return DBT_OK;
+}
+
+// Final residual states of the branches: [n_branches][B][d].
+dbt_status copy_branch_rows(dbt_model *m, float *dst, int B, int Bp, hipStream_t st) {
+  if (!dst) return DBT_OK;
+  const int d = m->cfg.d_model;
+  for (int j = 0; j < n_branches(m->cfg); ++j)
+    HIPCHK(hipMemcpyAsync(dst + (size_t)j * B * d, m->at<float>(m->L.S) + (size_t)(1 + j) * Bp * d, (size_t)B * d * 4,
                           hipMemcpyDeviceToDevice, st));
   return DBT_OK;
 }
@@ -721,13 +738,14 @@ dbt_status copy_rows(float *dst, const float *src, int B, int d, hipStream_t st)
 dbt_status branch_pass(dbt_model *m, dbt_kv *kv, int B, int Bp, hipStream_t st, const dbt_step_out *out = nullptr) {
   LayerCall lc{};
   lc.out = out;
-  lc.rows = Rows{B, Bp, 1, 1};
+  const int nb = n_branches(m->cfg);
+  lc.rows = Rows{B, Bp, 1, nb};
   lc.mode = MODE_BRANCH;
   lc.retain = false;
   lc.ret_src = -1;
   lc.ret_dst = 0;
   lc.prefill = false;
-  lc.rows_layout = 2 * Bp;
+  lc.rows_layout = (1 + nb) * Bp;
   lc.last_norm = true;
   for (int l = 0; l < m->cfg.n_layers; ++l) {
     dbt_status s = run_layer(m, kv, l, lc, st);
@@ -912,7 +930,8 @@ dbt_status dbt_decode_step(dbt_model *m, dbt_kv *kv, const dbt_step_in *in, int3
   StepBegin sb;
   if ((s = flush(kv, pos.data(), B, st, &sb))) return s;
   const bool on = branch_on != 0;
-  const Rows rows{B, Bp, 0, on ? 2 : 1};
+  const int nb = n_branches(cf);
+  const Rows rows{B, Bp, 0, on ? 1 + nb : 1};
   if ((s = load_inputs(m, kv, in, in->tokens, rows, st, &sb))) return s;
   LayerCall lc{};
   lc.rows = rows;
@@ -920,7 +939,7 @@ dbt_status dbt_decode_step(dbt_model *m, dbt_kv *kv, const dbt_step_in *in, int3
   lc.retain = false;
   lc.ret_src = -1;
   lc.prefill = false;
-  lc.rows_layout = 2 * Bp;
+  lc.rows_layout = (1 + nb) * Bp;
   lc.last_norm = true;
   lc.out = out;
   for (int l = 0; l < cf.n_layers; ++l)
@@ -930,7 +949,7 @@ dbt_status dbt_decode_step(dbt_model *m, dbt_kv *kv, const dbt_step_in *in, int3
   if (out) {
     if ((s = readout(m, B, Bp, on, out, st))) return s;
     if ((s = copy_rows(out->h1_out, m->at<float>(m->L.S), B, cf.d_model, st))) return s;
-    if (on && (s = copy_rows(out->h2_out, m->at<float>(m->L.S) + (size_t)Bp * cf.d_model, B, cf.d_model, st))) return s;
+    if (on && (s = copy_branch_rows(m, out->h2_out, B, Bp, st))) return s;
   }
   return DBT_OK;
 }
@@ -958,21 +977,21 @@ dbt_status dbt_decode_step_ungrouped(dbt_model *m, dbt_kv *kv, const dbt_step_in
   lc.retain = true;
   lc.ret_src = -1;
   lc.prefill = false;
-  lc.rows_layout = 2 * Bp;
+  lc.rows_layout = (1 + n_branches(cf)) * Bp;
   lc.last_norm = true;
   lc.out = out;
   for (int l = 0; l < cf.n_layers; ++l)
     if ((s = run_layer(m, kv, l, lc, st))) return s;
   if (cf.vocab > 0 && (s = lm_head(m, prim, st))) return s;
   // pass 2: every branch layer
-  const Rows br{B, Bp, 1, 1};
+  const Rows br{B, Bp, 1, n_branches(cf)};
   if ((s = load_inputs(m, kv, in, in->tokens, br, st))) return s;
   if ((s = branch_pass(m, kv, B, Bp, st, out))) return s;
   for (int b = 0; b < B; ++b) kv->len[b] += 1;
   if (out) {
     if ((s = readout(m, B, Bp, true, out, st))) return s;
     if ((s = copy_rows(out->h1_out, m->at<float>(m->L.S), B, cf.d_model, st))) return s;
-    if ((s = copy_rows(out->h2_out, m->at<float>(m->L.S) + (size_t)Bp * cf.d_model, B, cf.d_model, st))) return s;
+    if ((s = copy_branch_rows(m, out->h2_out, B, Bp, st))) return s;
   }
   return DBT_OK;
 }
@@ -1060,14 +1079,14 @@ dbt_status dbt_boundary(dbt_model *m, dbt_kv *kv, int32_t batch, dbt_step_out *o
   std::vector<int> pos(B);
   for (int b = 0; b < B; ++b) pos[b] = kv->len[b] - 1;
   if ((s = flush(kv, pos.data(), B, st))) return s;
-  const Rows br{B, Bp, 1, 1};
+  const Rows br{B, Bp, 1, n_branches(cf)};
   HIPCHK(launch_embed(m->at<int>(L.btok), cf.vocab, m->w.emb1, m->w.emb2, m->w.emb_norm, m->layers[0].attn_norm, cf.rms_eps,
                       cf.d_model, cf.dtype, br, m->at<float>(L.S), m->ws + L.Xn, cf.d_model, st));
   if ((s = branch_pass(m, kv, B, Bp, st))) return s;
   m->bnd_kv = nullptr;
   if (out) {
     if ((s = readout(m, B, Bp, true, out, st))) return s;
-    if ((s = copy_rows(out->h2_out, m->at<float>(L.S) + (size_t)Bp * cf.d_model, B, cf.d_model, st))) return s;
+    if ((s = copy_branch_rows(m, out->h2_out, B, Bp, st))) return s;
   }
   return DBT_OK;
 }

@@ -102,7 +102,8 @@ __global__ void k_embed(const int *tokens, int vocab, const T *e1, const T *e2, 
   const int row = phys_row(rows, path, b);
   const int tok = tokens[b];
   const bool valid = tok >= 0 && tok < vocab;
-  const T *e = (path == 0 ? e1 : e2) + (size_t)(valid ? tok : 0) * d;
+  // decode branch j >= 1 reads table j of the branch tables (App. C.1 for j >= 2)
+  const T *e = (path == 0 ? e1 : e2 + (size_t)(path - 1) * vocab * d) + (size_t)(valid ? tok : 0) * d;
   float *s = S + (size_t)row * d;
   float ss = 0.f;
   for (int i = threadIdx.x; i < d / 4; i += blockDim.x) {
@@ -125,7 +126,7 @@ __global__ void k_load_hidden(const float *h1, const float *h2, const float *g_n
   apply_step_begin(sb, pos_arr, page_table, mpps);
   const int b = blockIdx.x, path = rows.p0 + blockIdx.y;
   const int row = phys_row(rows, path, b);
-  const float *h = (path == 0 ? h1 : h2) + (size_t)b * d;
+  const float *h = (path == 0 ? h1 : h2 + (size_t)(path - 1) * rows.B * d) + (size_t)b * d;
   float *s = S + (size_t)row * d;
   for (int i = threadIdx.x; i < d / 4; i += blockDim.x) ((float4 *)s)[i] = ((const float4 *)h)[i];
   __syncthreads();
@@ -156,7 +157,8 @@ __global__ void k_qkv_finish(QKVFinish f) {
   const int pos = f.pos_arr ? f.pos_arr[b] : b;
   const int seq = f.pos_arr ? b : f.seq_fixed;
   const int dq = f.n_q * f.d_h, dkv = f.n_kv * f.d_h;
-  const int r1 = phys_row(f.rows, 0, b), r2 = phys_row(f.rows, 1, b);
+  const int r1 = phys_row(f.rows, 0, b);
+  const int pb0 = f.rows.p0 > 1 ? f.rows.p0 : 1, pb1 = f.rows.p0 + f.rows.np;  // branch paths of the call
   const int i = pi % half;
   const float2 cs = f.rope[(size_t)pos * half + i];
   if (pi < nqp) {
@@ -178,14 +180,16 @@ __global__ void k_qkv_finish(QKVFinish f) {
       q1a = f.Q1_in[(size_t)b * dq + c0];
       q1b = f.Q1_in[(size_t)b * dq + c1];
     }
-    if (br) {
-      const float y0 = psum(f.part, f.split_stride, f.S, (size_t)r2 * f.ldp + c0);
-      const float y1 = psum(f.part, f.split_stride, f.S, (size_t)r2 * f.ldp + c1);
-      const float q2a = y0 * cs.x - y1 * cs.y;
-      const float q2b = y0 * cs.y + y1 * cs.x;
-      f.Q[(size_t)r2 * dq + c0] = q2a + f.a[c0] * q1a;
-      f.Q[(size_t)r2 * dq + c1] = q2b + f.a[c1] * q1b;
-    }
+    if (br)
+      for (int p = pb0; p < pb1; ++p) {  // every branch couples to Q1 with the shared a
+        const int r2 = phys_row(f.rows, p, b);
+        const float y0 = psum(f.part, f.split_stride, f.S, (size_t)r2 * f.ldp + c0);
+        const float y1 = psum(f.part, f.split_stride, f.S, (size_t)r2 * f.ldp + c1);
+        const float q2a = y0 * cs.x - y1 * cs.y;
+        const float q2b = y0 * cs.y + y1 * cs.x;
+        f.Q[(size_t)r2 * dq + c0] = q2a + f.a[c0] * q1a;
+        f.Q[(size_t)r2 * dq + c1] = q2b + f.a[c1] * q1b;
+      }
     return;
   }
   // keys and values (primary only): cache slot of position pos
@@ -238,7 +242,7 @@ __global__ void k_resid_norm(const float *part, long long stride, int S, int ldp
   } else {
     const int r1 = phys_row(rows, 0, b);
     for (int i = threadIdx.x; i < d / 4; i += blockDim.x) {
-      const float4 a1 = rows.np == 2 ? psum4(part, stride, S, ((size_t)r1 * ldp) / 4 + i)
+      const float4 a1 = rows.p0 == 0 ? psum4(part, stride, S, ((size_t)r1 * ldp) / 4 + i)
                                      : ((const float4 *)(gc.in + (size_t)b * d))[i];
       const float4 ga = ((const float4 *)gc.g)[i];
       const float4 v = ((float4 *)s)[i];
@@ -259,7 +263,8 @@ __global__ void k_swiglu_finish(const float *part, long long stride, int S, int 
   const int j = blockIdx.x * blockDim.x + threadIdx.x;
   if (j >= f) return;
   const bool prim = mode != MODE_BRANCH, br = mode != MODE_PRIMARY;
-  const int r1 = phys_row(rows, 0, b), r2 = phys_row(rows, 1, b);
+  const int r1 = phys_row(rows, 0, b);
+  const int pb0 = rows.p0 > 1 ? rows.p0 : 1, pb1 = rows.p0 + rows.np;
   float h1;
   if (prim) {
     const float gt = psum(part, stride, S, (size_t)r1 * ldp + j);
@@ -271,12 +276,14 @@ __global__ void k_swiglu_finish(const float *part, long long stride, int S, int 
   } else {
     h1 = H1_in[(size_t)b * f + j];
   }
-  if (br) {
-    const float gt = psum(part, stride, S, (size_t)r2 * ldp + j);
-    const float up = psum(part, stride, S, (size_t)r2 * ldp + f + j);
-    const float h2 = gt / (1.0f + expf(-gt)) * up;
-    st<T>(Xh, (size_t)r2 * ldh + j, h2 + bvec[j] * h1);
-  }
+  if (br)
+    for (int p = pb0; p < pb1; ++p) {
+      const int r2 = phys_row(rows, p, b);
+      const float gt = psum(part, stride, S, (size_t)r2 * ldp + j);
+      const float up = psum(part, stride, S, (size_t)r2 * ldp + f + j);
+      const float h2 = gt / (1.0f + expf(-gt)) * up;
+      st<T>(Xh, (size_t)r2 * ldh + j, h2 + bvec[j] * h1);
+    }
 }
 
 // After the MLP down projection: M1, M2 = M2' + c * M1 (Eq. (15)),
@@ -289,9 +296,9 @@ __global__ void k_down_finish(const float *part, long long stride, int S, int ld
   __shared__ float red[16];
   const int b = blockIdx.x;
   const bool prim = mode != MODE_BRANCH, br = mode != MODE_PRIMARY;
-  const int r1 = phys_row(rows, 0, b), r2 = phys_row(rows, 1, b);
+  const int r1 = phys_row(rows, 0, b);
+  const int pb0 = rows.p0 > 1 ? rows.p0 : 1, pb1 = rows.p0 + rows.np;
   float4 *s1 = (float4 *)(Sres + (size_t)r1 * d);
-  float4 *s2 = (float4 *)(Sres + (size_t)r2 * d);
   const bool keep = ret.ptr && (ret.src_row < 0 || ret.src_row == b);
   float4 *kept = keep ? (float4 *)(ret.ptr + (size_t)(ret.src_row < 0 ? b : ret.dst_row) * d) : nullptr;
   for (int i = threadIdx.x; i < d / 4; i += blockDim.x) {
@@ -303,20 +310,25 @@ __global__ void k_down_finish(const float *part, long long stride, int S, int ld
     } else {
       m1 = ((const float4 *)(M1_in + (size_t)b * d))[i];
     }
-    if (br) {
-      const float4 m2 = psum4(part, stride, S, ((size_t)r2 * ldp) / 4 + i);
-      const float4 c = ((const float4 *)cvec)[i];
-      const float4 t = make_float4(m2.x + c.x * m1.x, m2.y + c.y * m1.y, m2.z + c.z * m1.z, m2.w + c.w * m1.w);
-      s2[i] = add4(s2[i], t);
-    }
+    if (br)
+      for (int p = pb0; p < pb1; ++p) {
+        const int r2 = phys_row(rows, p, b);
+        float4 *s2 = (float4 *)(Sres + (size_t)r2 * d);
+        const float4 m2 = psum4(part, stride, S, ((size_t)r2 * ldp) / 4 + i);
+        const float4 c = ((const float4 *)cvec)[i];
+        const float4 t = make_float4(m2.x + c.x * m1.x, m2.y + c.y * m1.y, m2.z + c.z * m1.z, m2.w + c.w * m1.w);
+        s2[i] = add4(s2[i], t);
+      }
   }
   if (!g_next) return;
   __syncthreads();
   if (prim) norm_row<T>((const float *)s1, g_next, eps, d, Xn + (size_t)r1 * ldx, red);
-  if (br) {
-    __syncthreads();
-    norm_row<T>((const float *)s2, g_next, eps, d, Xn + (size_t)r2 * ldx, red);
-  }
+  if (br)
+    for (int p = pb0; p < pb1; ++p) {
+      const int r2 = phys_row(rows, p, b);
+      __syncthreads();
+      norm_row<T>(Sres + (size_t)r2 * d, g_next, eps, d, Xn + (size_t)r2 * ldx, red);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -423,44 +435,61 @@ __device__ void merged_stats(const MixArgs &m, int row, float &lse, float &p2) {
   p2 = y / (z * z);
 }
 
+// With several decode branches (App. C.1) q is the mean of the branch
+// softmaxes: (1 - alpha) / n_b * sum_j q_j, branches summed in order.
 __global__ void k_mix_argmax(MixArgs m) {
+  constexpr int MAXB = 3;  // decode branches
   __shared__ float rv[16];
   __shared__ int ri[16];
-  __shared__ float sh[3];
+  __shared__ float sh[2 + MAXB];
   const int c = blockIdx.x, b = blockIdx.y;
-  const bool on = m.rows.np == 2;
-  const int nch = (m.V + m.chunk - 1) / m.chunk;
-  const int r1 = phys_row(m.rows, 0, b), r2 = phys_row(m.rows, 1, b);
+  const int nb = m.rows.np - 1;  // branches (0: branch off)
+  const bool on = nb > 0;
+  const int r1 = phys_row(m.rows, 0, b);
   if (on && threadIdx.x < 64) {
     float lse1, p2, lse2, dummy;
     merged_stats(m, r1, lse1, p2);
-    merged_stats(m, r2, lse2, dummy);
     if (threadIdx.x == 0) {
       sh[0] = lse1;
       sh[1] = fminf(1.f, fmaxf(0.5f, p2));
-      sh[2] = lse2;
+    }
+    for (int j = 0; j < nb; ++j) {
+      merged_stats(m, phys_row(m.rows, 1 + j, b), lse2, dummy);
+      if (threadIdx.x == 0) sh[2 + j] = lse2;
     }
   }
   __syncthreads();
-  const float lse1 = on ? sh[0] : 0.f, alpha = on ? sh[1] : 1.f, lse2 = on ? sh[2] : 0.f;
+  const float lse1 = on ? sh[0] : 0.f, alpha = on ? sh[1] : 1.f;
+  const float wq = on ? (1.f - alpha) / (float)nb : 0.f;
   const int lo = c * m.chunk, hi = min(m.V, lo + m.chunk);
   const float *z1 = m.logits + (size_t)r1 * m.V;
-  const float *z2 = m.logits + (size_t)r2 * m.V;
   float best = -INFINITY;
   int bi = 0x7fffffff;
   constexpr int PER = 16;  // chunk = PER * blockDim.x
-  float a1[PER], a2[PER];
+  float a1[PER], qs[PER];
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
     const int v = lo + threadIdx.x + k * blockDim.x;
     a1[k] = v < hi ? z1[v] : -INFINITY;
-    a2[k] = (on && v < hi) ? z2[v] : -INFINITY;
+    qs[k] = 0.f;
+  }
+  for (int j = 0; j < nb; ++j) {
+    const float *z2 = m.logits + (size_t)phys_row(m.rows, 1 + j, b) * m.V;
+    const float lse2 = sh[2 + j];
+    float a2[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int v = lo + threadIdx.x + k * blockDim.x;
+      a2[k] = v < hi ? z2[v] : -INFINITY;
+    }
+#pragma unroll
+    for (int k = 0; k < PER; ++k) qs[k] += expf(a2[k] - lse2);
   }
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
     const int v = lo + threadIdx.x + k * blockDim.x;
     if (v < hi) {
-      const float val = on ? alpha * expf(a1[k] - lse1) + (1.f - alpha) * expf(a2[k] - lse2) : a1[k];
+      const float val = on ? alpha * expf(a1[k] - lse1) + wq * qs[k] : a1[k];
       argmax_merge(best, bi, val, v);
     }
   }
@@ -475,6 +504,7 @@ __global__ void k_mix_argmax(MixArgs m) {
   __syncthreads();
   if (threadIdx.x == 0) {
     for (int k = 1; k < (int)(blockDim.x >> 6); ++k) argmax_merge(best, bi, rv[k], ri[k]);
+    const int nch = (m.V + m.chunk - 1) / m.chunk;
     float *o = m.cand + ((size_t)b * nch + c) * 2;
     o[0] = best;
     o[1] = __int_as_float(bi);

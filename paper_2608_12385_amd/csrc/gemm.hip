@@ -205,9 +205,10 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
         if (rt.ptr && (rt.src_row < 0 || rt.src_row == b))
           rt.ptr[(size_t)(rt.src_row < 0 ? b : rt.dst_row) * ep.f + n] = h;
       } else {
-        // H2~ = H2 + b * H1: the primary row of the same sequence is in this
-        // tile (both paths, M <= 16*MB) or comes from the retained H1
-        const float h1 = ep.rows.np == 2 ? hb[(mm - Bp) * HC + cc] : ep.H1_in[(size_t)b * ep.f + n];
+        // H2~ = H2 + b * H1 for every branch: the primary row of the same
+        // sequence is this tile's row b (primary and branches in one tile,
+        // M <= 16*MB, m0 = 0) or comes from the retained H1
+        const float h1 = ep.rows.p0 == 0 ? hb[b * HC + cc] : ep.H1_in[(size_t)b * ep.f + n];
         out = h + ep.bvec[n] * h1;
       }
       ep.Xh[(size_t)(row0 + gm) * ep.ldh + n] = f2bf(out);

@@ -163,9 +163,9 @@ hipError_t launch_kv_fill(KVRef kv, int seq, int start, int count, const void *k
 
 // ---- mixture readout (Sec. 4.2) ----
 struct MixArgs {
-  const float *logits;  // [2Bp][V]
+  const float *logits;  // [(1 + n_b) Bp][V]
   int V;
-  Rows rows;            // np = 2 with the branch on, 1 (primary) otherwise
+  Rows rows;            // np = 1 + n_b with the branches on (n_b <= 3), 1 (primary) otherwise
   int chunk;            // vocabulary entries per argmax chunk
   float *stats;         // [2Bp][nstat][3] per-tile (max, sum e^(z-max), sum e^(2(z-max)))
   int nstat;            // tiles per row in stats

@@ -1,0 +1,180 @@
+"""GPU parity of several decode branches (App. C.1): the HIP path through the
+C ABI against the oracle with two and three branches.
+
+Branch j has its own embedding table, shares every weight and the couplings
+a, b, c, and reads only the primary (its Q1, H1, M1 and cache); the mixture's
+q is the mean of the branch softmaxes.  Bars as for one branch: fp32 1e-5,
+bf16 2e-2 max relative error per row; greedy tokens equal except at certified
+near-ties of the oracle's mixture; primary outputs and the cache bit-identical
+with the branches on or off; the grouped step equals the two-pass step bit
+for bit.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import Oracle
+from tests.gpu_util import check_readout, fill_cache, make_session, row_err, to_np
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+F32_TOL = 1e-5
+BF16_TOL = 2e-2
+
+
+def _check(t, outs, tol, tag, nb):
+    """Primary logits, alpha and tokens, then every branch's logits."""
+    check_readout(t, outs, tol, tag, branch=False)
+    l2 = to_np(t["logits2"])
+    assert l2.shape[0] == nb, (tag, l2.shape)
+    for j in range(nb):
+        zj = np.stack([o["zb"][j] for o in outs])
+        err = row_err(l2[j], zj)
+        assert err.max() <= tol, (tag, j, err)
+
+
+def _check_states(t, outs, tol, tag, nb):
+    assert row_err(to_np(t["h1_out"]), np.stack([o["h1"] for o in outs])).max() <= tol, tag
+    h2 = to_np(t["h2_out"])
+    for j in range(nb):
+        hj = np.stack([o["hb"][j] for o in outs])
+        assert row_err(h2[j], hj).max() <= tol, (tag, j)
+
+
+@pytest.mark.parametrize("nb", [2, 3])
+def test_tiny_f32_branches_prefill_boundary_steps(nb):
+    w = synth.workload("tiny_f32")
+    shape = dataclasses.replace(w["shape"], n_branches=nb)
+    W = synth.make_weights(shape, seed=0)
+    prompt = synth.make_tokens(1, 0, (w["prompt_len"],), shape.vocab)
+    orc = Oracle(shape, W.values)
+    ob = orc.prefill([prompt], run_boundary=True)
+    sess = make_session(shape, W, max_batch=1, max_pos=w["prompt_len"] + 9, max_prompt=w["prompt_len"])
+    t = sess.prefill([prompt], run_boundary=True)
+    _check(t, ob, F32_TOL, "boundary", nb)
+    tok = ob[0]["next"]
+    for step in range(8):
+        o = orc.decode_step(tokens=[tok])
+        t = sess.decode(tokens=[tok])
+        _check(t, o, F32_TOL, f"step {step}", nb)
+        _check_states(t, o, F32_TOL, f"step {step}", nb)
+        assert int(to_np(t["next_token"])[0]) == o[0]["next"], step
+        tok = o[0]["next"]
+
+
+def _small_bf16(**kw):
+    base = dict(n_layers=2, d_model=512, n_q_heads=8, n_kv_heads=2, head_dim=128, d_ff=1024,
+                vocab=1024, dtype="bf16", has_embeddings=True, std=0.05, coupling_std=0.5)
+    base.update(kw)
+    return synth.ModelShape(**base)
+
+
+def test_small_bf16_three_branches_ragged_prompts():
+    """Four query rows per path and KV head (16 with three branches), ragged
+    prompts, the boundary and three grouped steps."""
+    shape = _small_bf16(n_branches=3)
+    W = synth.make_weights(shape, seed=0)
+    lens = [37, 100, 529, 1, 16]
+    prompts = [synth.make_tokens(1, 10 + i, (L,), shape.vocab) for i, L in enumerate(lens)]
+    orc = Oracle(shape, W.values)
+    obs = orc.prefill(prompts, run_boundary=True)
+    sess = make_session(shape, W, max_batch=5, max_pos=600, max_prompt=529)
+    t = sess.prefill(prompts, run_boundary=True)
+    _check(t, obs, BF16_TOL, "boundary", 3)
+    toks = [o["next"] for o in obs]
+    for step in range(3):
+        outs = orc.decode_step(tokens=toks)
+        t = sess.decode(tokens=toks)
+        _check(t, outs, BF16_TOL, f"step {step}", 3)
+        _check_states(t, outs, BF16_TOL, f"step {step}", 3)
+        toks = [o["next"] for o in outs]
+
+
+def test_three_branches_primary_bitwise_and_grouped_equals_ungrouped():
+    lengths = [3, 40, 530, 16]
+    B = len(lengths)
+    res = {}
+    for mode in ("on", "off", "ungrouped"):
+        shape = _small_bf16(n_layers=1, vocab=512, has_embeddings=False, n_branches=3)
+        W = synth.make_weights(shape, seed=0)
+        sess = make_session(shape, W, max_batch=B, max_pos=600)
+        sess.k_pages.fill_(0)   # unused slots compare equal across sessions
+        sess.v_pages.fill_(0)
+        fill_cache(sess, None, shape, lengths)
+        h = synth.make_hidden(shape, B, step=0, seed=2, paths=4)
+        if mode == "ungrouped":
+            t = sess.decode(h1=h[0], h2=h[1:], grouped=False)
+        else:
+            t = sess.decode(h1=h[0], h2=h[1:], branch_on=(mode == "on"))
+        res[mode] = {k: to_np(v).copy() for k, v in t.items()}
+        res[mode]["k"] = to_np(sess.k_pages).copy()
+        res[mode]["v"] = to_np(sess.v_pages).copy()
+        sess.close()
+    on, off, ug = res["on"], res["off"], res["ungrouped"]
+    for k in ("h1_out", "logits1", "k", "v"):
+        np.testing.assert_array_equal(on[k], off[k], err_msg=k)
+    assert np.all(off["alpha"] == 1.0)
+    np.testing.assert_array_equal(off["next_token"], np.argmax(off["logits1"], axis=1))
+    for k in ("h1_out", "h2_out", "logits1", "logits2", "alpha", "next_token", "k", "v"):
+        np.testing.assert_array_equal(on[k], ug[k], err_msg=k)
+
+
+def test_equal_tables_give_identical_branches():
+    """Two branches with the same embedding table are the same computation:
+    their logits and final states agree bit for bit, and the mixture is the
+    one-branch mixture of that table (oracle, within the bf16 bar)."""
+    shape = _small_bf16(n_branches=2)
+    W = synth.make_weights(shape, seed=0)
+    W.values["E3"] = W.values["E2"]
+    W.bits["E3"] = W.bits["E2"]
+    lens = [20, 70, 3]
+    prompts = [synth.make_tokens(1, 30 + i, (L,), shape.vocab) for i, L in enumerate(lens)]
+    sess = make_session(shape, W, max_batch=3, max_pos=80, max_prompt=70)
+    t = sess.prefill(prompts, run_boundary=True)
+    toks = to_np(t["next_token"]).tolist()
+    t = sess.decode(tokens=toks)
+    l2, h2 = to_np(t["logits2"]), to_np(t["h2_out"])
+    np.testing.assert_array_equal(l2[0], l2[1])
+    np.testing.assert_array_equal(h2[0], h2[1])
+    one = dataclasses.replace(shape, n_branches=1)
+    orc = Oracle(one, {k: v for k, v in W.values.items() if k != "E3"})
+    orc.prefill(prompts, run_boundary=True)
+    outs = orc.decode_step(tokens=toks)
+    check_readout({"logits1": t["logits1"], "logits2": l2[0], "alpha": t["alpha"],
+                   "next_token": t["next_token"]}, outs, BF16_TOL, "equal tables")
+
+
+# ----------------------------------------------------------------------------
+# one 8B-shape layer + LM head, batch 32, cache 4096, three branches: the
+# primary and branch rows fill one 128-row tile of the fused gate/up epilogue
+# ----------------------------------------------------------------------------
+
+@pytest.mark.slow
+def test_layer8b_three_branches_full_size_sampled():
+    w = synth.workload("layer8b_bf16")
+    shape = dataclasses.replace(w["shape"], n_branches=3)
+    B, L = w["batch"], w["cache_len"]
+    W = synth.make_weights(shape, seed=0)
+    sess = make_session(shape, W, max_batch=B, max_pos=L + 16)
+    fill_cache(sess, None, shape, [L] * B)
+    h = synth.make_hidden(shape, B, step=0, seed=2, paths=4)
+    t = sess.decode(h1=h[0], h2=h[1:])
+    t = {k: to_np(v).copy() for k, v in t.items()}
+    sess.close()
+    sample = [0, 21, 31]
+    orc = Oracle(shape, W.values)
+    for b in sample:
+        (kv_, _), (vv_, _) = synth.make_kv(shape, 0, b, L, seed=3)
+        orc.kv_fill(b, L, [kv_], [vv_])
+    outs = [orc.step_one(b, h1=h[0, b], h2=[h[1 + j, b] for j in range(3)], readout=False) for b in sample]
+    orc._readout(outs)
+    sub = {k: (v[:, sample] if k in ("logits2", "h2_out") else v[sample]) for k, v in t.items()}
+    _check(sub, outs, BF16_TOL, "layer8b three branches", 3)
+    _check_states(sub, outs, BF16_TOL, "layer8b three branches", 3)
+    a = t["alpha"]
+    assert np.all((a >= 0.5) & (a <= 1.0))
+    nt = t["next_token"]
+    assert np.all((nt >= 0) & (nt < shape.vocab))
