@@ -47,9 +47,10 @@ constexpr int kLdsRow = kChunk + 8;  // padded LDS row of a staged activation ch
 // channels (row strides are powers of two).  The order is a function of the
 // row tile and the split only.
 //
-// GLU: the workgroup owns 32*RB rows of segment 0 (gate, waves 0-1) and the
-// same rows of segment 1 (up, waves 2-3); instead of storing Y it finishes
-// the MLP intermediate in its epilogue (see GluEpi).
+// GLU: the workgroup owns NW/2*16*RB rows of segment 0 (gate, the first
+// half of the waves) and the same rows of segment 1 (up, the second half);
+// instead of storing Y it finishes the MLP intermediate in its epilogue (see
+// GluEpi).
 template <int MB, int RB, int PD, int NW, bool GLU = false>
 __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const uint16_t *__restrict__ X, int ldx,
                                                        int M, float *__restrict__ Y, int ldy,
@@ -75,10 +76,11 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
   int nloc = blockIdx.x * ROWS;
   const uint16_t *Wseg = (const uint16_t *)segs.w[0];
   int segrows = segs.rows[0];
+  constexpr int HW = NW / 2, TC = HW * 16 * RB;  // GLU: waves per half, gate (= up) rows per tile
   if (GLU) {
-    static_assert(!GLU || NW == 4, "GLU tiles are 4 waves");
-    nloc = blockIdx.x * 32 * RB - (wave & 2) * 16 * RB;  // + wave*16*RB below: rows (wave&1)*16*RB of the tile
-    if (wave >= 2) {
+    static_assert(!GLU || NW % 2 == 0, "GLU tiles split the waves in two halves");
+    nloc = blockIdx.x * TC - (wave >= HW ? TC : 0);  // + wave*16*RB below: rows (wave%HW)*16*RB of the tile
+    if (wave >= HW) {
       Wseg = (const uint16_t *)segs.w[1];
       segrows = segs.rows[1];
     }
@@ -163,13 +165,13 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
     if (c0 + u < nch) step(c0 + u, u);
   // lane holds D[n = rb*16 + 4*gq + i][m = cb*16 + r]: Y[m][n .. n+3]
   if constexpr (GLU) {
-    // hb[m][c]: the tile's 32*RB gate/up columns c for activation row m
+    // hb[m][c]: the tile's TC gate/up columns c for activation row m
     // (reuses the activation slots: the loop's last barrier has passed)
-    constexpr int HC = 32 * RB + 1;
+    constexpr int HC = TC + 1;
     static_assert(XR * HC * 4 <= (int)sizeof(xs), "GLU staging exceeds the activation slots");
     float *hb = (float *)&xs[0][0];
-    const int c0 = (wave & 1) * 16 * RB;
-    if (wave >= 2)
+    const int c0 = (wave % HW) * 16 * RB;
+    if (wave >= HW)
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
@@ -177,7 +179,7 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
 #pragma unroll
           for (int i = 0; i < 4; ++i) hb[(cb * 16 + r) * HC + c0 + rb * 16 + 4 * gq + i] = acc[rb][cb][i];
     __syncthreads();
-    if (wave < 2)
+    if (wave < HW)
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
@@ -190,13 +192,13 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
           }
     __syncthreads();
     const int Bp = ep.rows.Bp, row0 = ep.rows.p0 * Bp;
-    for (int e = t; e < XR * 32 * RB; e += NW * 64) {
-      const int mm = e / (32 * RB), cc = e % (32 * RB);
+    for (int e = t; e < XR * TC; e += NW * 64) {
+      const int mm = e / TC, cc = e % TC;
       const int gm = m0 + mm;  // row of this call (relative to its first row)
       if (gm >= M) continue;
       const int path = ep.rows.p0 + gm / Bp, b = gm % Bp;
       if (b >= ep.rows.B) continue;
-      const int n = blockIdx.x * 32 * RB + cc;
+      const int n = blockIdx.x * TC + cc;
       const float h = hb[mm * HC + cc];
       float out;
       if (path == 0) {
@@ -349,16 +351,24 @@ GemmConfig gemm_config(int n_full, int K, int dtype, int seg_gran, int max_rows)
   } else if (n_full >= 16384 && seg_gran % 128 == 0) {
     g = GemmConfig{2, 2, 1, 4};    // MLP up projections
   } else {
-    // thin matrices: split the reduction so about one workgroup per compute
-    // unit runs; the fp32 slabs of up to max_rows stacked rows never exceed
-    // the weight bytes, and every split keeps at least one chunk
-    g = GemmConfig{1, 2, 1, 4};
-    const int tiles = std::max(1, n_full / 64);  // n_full may be 0 (no output matrix)
+    // thin matrices: split the reduction so that at most one workgroup per
+    // compute unit runs (a second round of workgroups costs a whole round);
+    // the fp32 slabs of up to max_rows stacked rows never exceed the weight
+    // bytes, and every split keeps at least one chunk.  Tiles of 64 rows
+    // (4 waves) unless 128-row tiles (8 waves) keep more compute units busy;
+    // fewer splits also mean fewer slabs for the consumer to add.
     const int nc = K / kChunk;
-    int S = (256 + tiles / 2) / tiles;
-    S = std::min(S, std::max(1, K / (2 * std::max(max_rows, 1))));
-    S = std::min({S, 16, std::max(nc, 1)});
-    g.S = std::max(S, 1);
+    auto splits = [&](int tiles) {
+      int S = 256 / tiles;
+      S = std::min(S, std::max(1, K / (2 * std::max(max_rows, 1))));
+      return std::max(std::min({S, 16, std::max(nc, 1)}), 1);
+    };
+    const int t4 = std::max(1, n_full / 64), t8 = std::max(1, n_full / 128);
+    const int s4 = splits(t4), s8 = splits(t8);
+    if (seg_gran % 128 == 0 && t8 * s8 > t4 * s4)
+      g = GemmConfig{1, 2, s8, 8};
+    else
+      g = GemmConfig{1, 2, s4, 4};
   }
   return g;
 }
@@ -368,8 +378,12 @@ template <int MB>
 void launch_mb(const GemmConfig &g, dim3 grid, hipStream_t st, const WSegs &segs, int K, const uint16_t *X, int ldx,
                int M, float *Y, int ldy, long long yss, float *rs) {
   const GluEpi none{};
-  if (g.NW == 8)
+  if (g.NW == 16)
+    hipLaunchKernelGGL((k_gemm_bf16<MB, 1, 2, 16>), grid, dim3(1024), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs, none);
+  else if (g.NW == 8 && g.RB == 4)
     hipLaunchKernelGGL((k_gemm_bf16<MB, 4, 1, 8>), grid, dim3(512), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs, none);
+  else if (g.NW == 8)
+    hipLaunchKernelGGL((k_gemm_bf16<MB, 1, 2, 8>), grid, dim3(512), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs, none);
   else if (g.RB == 2)
     hipLaunchKernelGGL((k_gemm_bf16<MB, 2, 2, 4>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs, none);
   else
@@ -379,7 +393,7 @@ void launch_mb(const GemmConfig &g, dim3 grid, hipStream_t st, const WSegs &segs
 template <int MB>
 void launch_glu_mb(dim3 grid, hipStream_t st, const WSegs &segs, int K, const uint16_t *X, int ldx, int M,
                    const GluEpi &ep) {
-  hipLaunchKernelGGL((k_gemm_bf16<MB, 2, 2, 4, true>), grid, dim3(256), 0, st, segs, K, X, ldx, M, nullptr, 0, 0LL,
+  hipLaunchKernelGGL((k_gemm_bf16<MB, 1, 2, 8, true>), grid, dim3(512), 0, st, segs, K, X, ldx, M, nullptr, 0, 0LL,
                      nullptr, ep);
 }
 }  // namespace
