@@ -65,7 +65,7 @@ struct Layout {
   size_t moe_idx = 0, moe_logits = 0, moe_w = 0, moe_aslot = 0, moe_counts = 0, moe_offsets = 0, moe_arow = 0, moe_h = 0,
          moe_y = 0, ret_idx = 0;
   size_t rope = 0, pos = 0, S = 0, Xn = 0, Xh = 0, Q = 0, O = 0, P = 0, apart = 0, astat = 0,
-         logits = 0, mstats = 0, mcand = 0, ret_q = 0, ret_h = 0, ret_m = 0, ret_a = 0, btok = 0, slast = 0,
+         logits = 0, mstats = 0, ret_q = 0, ret_h = 0, ret_m = 0, ret_a = 0, btok = 0, slast = 0,
          total = 0;
 };
 
@@ -160,7 +160,6 @@ Layout make_layout(const dbt_config *c) {
   L.nstat = gemm_stats_tiles(std::max(c->vocab, 1), L.g_lm, c->dtype);
   if (L.nstat == 0) L.nstat = std::max(L.nch, 1);
   L.mstats = take((size_t)L.R_max * L.nstat * 3 * 4);
-  L.mcand = take((size_t)c->max_batch * std::max(L.nch, 1) * 2 * 4);
   L.ret_q = take((size_t)c->n_layers * L.Bp_max * dq * 4);
   L.ret_h = take((size_t)c->n_layers * L.Bp_max * L.f * 4);
   L.ret_m = take((size_t)c->n_layers * L.Bp_max * d * 4);
@@ -659,8 +658,8 @@ dbt_status readout(dbt_model *m, int B, int Bp, bool branch, dbt_step_out *out, 
   mx.chunk = kMixChunk;
   mx.stats = m->at<float>(L.mstats);
   mx.stats_ready = gemm_stats_tiles(cf.vocab, L.g_lm, cf.dtype) > 0;
+  mx.tile_w = mx.stats_ready ? gemm_tile_rows(L.g_lm) : kMixChunk;
   mx.nstat = L.nstat;
-  mx.cand = m->at<float>(L.mcand);
   mx.alpha = out ? out->alpha : nullptr;
   mx.next = out ? out->next_token : nullptr;
   if (mx.alpha || mx.next) {

@@ -397,100 +397,176 @@ __global__ void k_mix_stats(MixArgs m) {
   }
 }
 
-// Merge the per-tile statistics of one row with one wave (fixed-order tree).
-// Up to 16 tiles per lane are loaded at once (one memory round trip).
-__device__ void merged_stats(const MixArgs &m, int row, float &lse, float &p2) {
-  const int lane = threadIdx.x & 63;
-  const float *st = m.stats + (size_t)row * m.nstat * 3;
-  constexpr int PER = 16;
-  float tm[PER], t1[PER], t2[PER];
+// Greedy token of the mixture (Eqs. (17)-(18)); with several decode branches
+// (App. C.1) q is the mean of the branch softmaxes, (1 - alpha) / n_b *
+// sum_j q_j, branches summed in order.  One wave per sequence, NP = 1 + n_b
+// path rows (1: branches off).
+//
+// The per-tile statistics (max, sum e^(z-max), sum e^(2(z-max))) of the
+// output projection give lse of each row and sum p^2 (alpha).  Not every
+// entry is then read: a tile T (row maxima max1_T, max2j_T) holds no mixture
+// value above
+//   ub_T = alpha e^(max1_T - lse1) + (1 - alpha)/n_b sum_j e^(max2j_T - lse2j),
+// while the token attaining a tile maximum proves the lower bound
+//   lb = max_T max(alpha e^(max1_T - lse1), (1 - alpha)/n_b e^(max2j_T - lse2j))
+// on the largest value.  Only tiles with ub_T >= lb (1 - 2^-10) are scanned
+// (the margin exceeds the fp32 rounding of both sides, so a skipped entry can
+// never be the fp32 argmax), and every entry of a kept tile is evaluated.
+// With the branches off the value is the primary logit itself and only tiles
+// attaining the row maximum are scanned.  The lowest index wins ties.  The
+// kernel is short: one memory round trip for the statistics and one per kept
+// tile, and little code (a cold instruction cache is a large part of such a
+// kernel's time).
+template <int NP>
+__global__ __launch_bounds__(256) void k_mix_select(MixArgs m) {
+  constexpr int SB = 8, MAXT = 4096;
+  __shared__ float red[NP][3][4];
+  __shared__ float lb_s[4];
+  __shared__ int list[MAXT];
+  __shared__ int cnt_s[4];
+  __shared__ float rv[4];
+  __shared__ int ri[4];
+  const int b = blockIdx.x, t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const float *st[NP];
+  const float *z[NP];
 #pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int c = lane + 64 * k;
-    const bool ok = c < m.nstat;
-    tm[k] = ok ? st[c * 3] : -INFINITY;
-    t1[k] = ok ? st[c * 3 + 1] : 0.f;
-    t2[k] = ok ? st[c * 3 + 2] : 0.f;
+  for (int j = 0; j < NP; ++j) {
+    st[j] = m.stats + (size_t)(j * m.rows.Bp + b) * m.nstat * 3;
+    z[j] = m.logits + (size_t)(j * m.rows.Bp + b) * m.V;
   }
-  float mx = -INFINITY;
+  // 1. lse and sum p^2: each thread merges its tiles t + 256k online, then
+  //    the workgroup merges the threads (fixed tree); the maxima of the last
+  //    round stay in registers
+  float M[NP], Z[NP], Y[NP], x[NP];
 #pragma unroll
-  for (int k = 0; k < PER; ++k) mx = fmaxf(mx, tm[k]);
-  for (int c = lane + 64 * PER; c < m.nstat; c += 64) mx = fmaxf(mx, st[c * 3]);
-  mx = wave_max(mx);
-  float z = 0.f, y = 0.f;
+  for (int j = 0; j < NP; ++j) {
+    M[j] = -INFINITY;
+    Z[j] = Y[j] = 0.f;
+  }
+  for (int T = t; T - t < m.nstat; T += 256) {
+    float s1[NP], s2[NP];
 #pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const float e = expf(tm[k] - mx);
-    z += t1[k] * e;
-    y += t2[k] * e * e;
-  }
-  for (int c = lane + 64 * PER; c < m.nstat; c += 64) {
-    const float e = expf(st[c * 3] - mx);
-    z += st[c * 3 + 1] * e;
-    y += st[c * 3 + 2] * e * e;
-  }
-  z = wave_sum(z);
-  y = wave_sum(y);
-  lse = mx + logf(z);
-  p2 = y / (z * z);
-}
-
-// With several decode branches (App. C.1) q is the mean of the branch
-// softmaxes: (1 - alpha) / n_b * sum_j q_j, branches summed in order.
-__global__ void k_mix_argmax(MixArgs m) {
-  constexpr int MAXB = 3;  // decode branches
-  __shared__ float rv[16];
-  __shared__ int ri[16];
-  __shared__ float sh[2 + MAXB];
-  const int c = blockIdx.x, b = blockIdx.y;
-  const int nb = m.rows.np - 1;  // branches (0: branch off)
-  const bool on = nb > 0;
-  const int r1 = phys_row(m.rows, 0, b);
-  if (on && threadIdx.x < 64) {
-    float lse1, p2, lse2, dummy;
-    merged_stats(m, r1, lse1, p2);
-    if (threadIdx.x == 0) {
-      sh[0] = lse1;
-      sh[1] = fminf(1.f, fmaxf(0.5f, p2));
+    for (int j = 0; j < NP; ++j) {
+      x[j] = T < m.nstat ? st[j][T * 3] : -INFINITY;
+      s1[j] = T < m.nstat ? st[j][T * 3 + 1] : 0.f;
+      s2[j] = T < m.nstat ? st[j][T * 3 + 2] : 0.f;
     }
-    for (int j = 0; j < nb; ++j) {
-      merged_stats(m, phys_row(m.rows, 1 + j, b), lse2, dummy);
-      if (threadIdx.x == 0) sh[2 + j] = lse2;
+#pragma unroll
+    for (int j = 0; j < NP; ++j) {
+      const float Mn = fmaxf(M[j], x[j]);
+      if (Mn == -INFINITY) continue;
+      const float fo = __expf(M[j] - Mn), fn = __expf(x[j] - Mn);
+      Z[j] = Z[j] * fo + s1[j] * fn;
+      Y[j] = Y[j] * fo * fo + s2[j] * fn * fn;
+      M[j] = Mn;
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < NP; ++j) {
+    const float Mw = wave_max(M[j]);
+    const float f = M[j] == -INFINITY ? 0.f : __expf(M[j] - Mw);
+    const float Zw = wave_sum(Z[j] * f), Yw = j == 0 ? wave_sum(Y[j] * f * f) : 0.f;
+    if (lane == 0) {
+      red[j][0][wave] = Mw;
+      red[j][1][wave] = Zw;
+      red[j][2][wave] = Yw;
     }
   }
   __syncthreads();
-  const float lse1 = on ? sh[0] : 0.f, alpha = on ? sh[1] : 1.f;
-  const float wq = on ? (1.f - alpha) / (float)nb : 0.f;
-  const int lo = c * m.chunk, hi = min(m.V, lo + m.chunk);
-  const float *z1 = m.logits + (size_t)r1 * m.V;
+  float lse[NP], p2 = 0.f;
+#pragma unroll
+  for (int j = 0; j < NP; ++j) {
+    float Mb = -INFINITY, Zb = 0.f, Yb = 0.f;
+    for (int w = 0; w < 4; ++w) Mb = fmaxf(Mb, red[j][0][w]);
+    for (int w = 0; w < 4; ++w) {
+      const float f = red[j][0][w] == -INFINITY ? 0.f : __expf(red[j][0][w] - Mb);
+      Zb += red[j][1][w] * f;
+      Yb += red[j][2][w] * f * f;
+    }
+    lse[j] = Mb + __logf(Zb);
+    if (j == 0) p2 = Yb / (Zb * Zb);
+  }
+  const float alpha = NP > 1 ? fminf(1.f, fmaxf(0.5f, p2)) : 1.f;
+  const float wq = NP > 1 ? (1.f - alpha) / (float)(NP - 1) : 0.f;
+  // 2. bounds; tile maxima from registers in the last round, else reloaded
+  const int lastT = (m.nstat - 1) / 256 * 256 + t;
+  auto bounds = [&](int T, float &ub, float &lo) {
+    float xt[NP];
+#pragma unroll
+    for (int j = 0; j < NP; ++j) xt[j] = T == lastT ? x[j] : (T < m.nstat ? st[j][T * 3] : -INFINITY);
+    if (T >= m.nstat) {
+      ub = lo = -INFINITY;
+      return;
+    }
+    if (NP == 1) {
+      ub = lo = xt[0];
+      return;
+    }
+    const float p1 = alpha * __expf(xt[0] - lse[0]);
+    float q = 0.f;
+    lo = p1;
+#pragma unroll
+    for (int j = 1; j < NP; ++j) {
+      const float e = __expf(xt[j] - lse[j]);
+      q += e;
+      lo = fmaxf(lo, wq * e);
+    }
+    ub = p1 + wq * q;
+  };
+  float lb = -INFINITY;
+  for (int T = t; T - t < m.nstat; T += 256) {
+    float ub, lo;
+    bounds(T, ub, lo);
+    lb = fmaxf(lb, lo);
+  }
+  lb = wave_max(lb);
+  if (lane == 0) lb_s[wave] = lb;
+  __syncthreads();
+  lb = fmaxf(fmaxf(lb_s[0], lb_s[1]), fmaxf(lb_s[2], lb_s[3]));
+  const float thr = NP > 1 ? lb * (1.f - 1.f / 1024.f) : lb;
+  // 3. kept tiles into the list (rounds of 256, ballot per wave), then one
+  //    flattened scan, SB entries per thread per memory round trip (any
+  //    order: the merge keeps the largest value, then the lowest index)
+  int nkeep = 0;
+  for (int T = t; T - t < m.nstat; T += 256) {
+    float ub, lo;
+    bounds(T, ub, lo);
+    const bool keep = ub >= thr;
+    const unsigned long long bal = __ballot(keep);
+    if (lane == 0) cnt_s[wave] = __popcll(bal);
+    __syncthreads();
+    int off = nkeep;
+    for (int w = 0; w < wave; ++w) off += cnt_s[w];
+    if (keep && off + __popcll(bal & ((1ull << lane) - 1ull)) < MAXT)
+      list[off + __popcll(bal & ((1ull << lane) - 1ull))] = T;
+    nkeep += cnt_s[0] + cnt_s[1] + cnt_s[2] + cnt_s[3];
+    __syncthreads();
+  }
+  nkeep = min(nkeep, MAXT);
+  const int tw = m.tile_w, total = nkeep * tw;
   float best = -INFINITY;
   int bi = 0x7fffffff;
-  constexpr int PER = 16;  // chunk = PER * blockDim.x
-  float a1[PER], qs[PER];
+  for (int e0 = 0; e0 < total; e0 += 256 * SB) {
+    int vi[SB];
+    float a[NP][SB];
 #pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int v = lo + threadIdx.x + k * blockDim.x;
-    a1[k] = v < hi ? z1[v] : -INFINITY;
-    qs[k] = 0.f;
-  }
-  for (int j = 0; j < nb; ++j) {
-    const float *z2 = m.logits + (size_t)phys_row(m.rows, 1 + j, b) * m.V;
-    const float lse2 = sh[2 + j];
-    float a2[PER];
+    for (int i = 0; i < SB; ++i) {
+      const int e = e0 + t + 256 * i;
+      vi[i] = e < total ? list[e / tw] * tw + e % tw : m.V;
 #pragma unroll
-    for (int k = 0; k < PER; ++k) {
-      const int v = lo + threadIdx.x + k * blockDim.x;
-      a2[k] = v < hi ? z2[v] : -INFINITY;
+      for (int j = 0; j < NP; ++j) a[j][i] = vi[i] < m.V ? z[j][vi[i]] : -INFINITY;
     }
 #pragma unroll
-    for (int k = 0; k < PER; ++k) qs[k] += expf(a2[k] - lse2);
-  }
+    for (int i = 0; i < SB; ++i) {
+      if (vi[i] >= m.V) continue;
+      float val = a[0][i];
+      if (NP > 1) {
+        float qs = 0.f;
 #pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int v = lo + threadIdx.x + k * blockDim.x;
-    if (v < hi) {
-      const float val = on ? alpha * expf(a1[k] - lse1) + wq * qs[k] : a1[k];
-      argmax_merge(best, bi, val, v);
+        for (int j = 1; j < NP; ++j) qs += __expf(a[j][i] - lse[j]);
+        val = alpha * __expf(a[0][i] - lse[0]) + wq * qs;
+      }
+      argmax_merge(best, bi, val, vi[i]);
     }
   }
 #pragma unroll
@@ -499,31 +575,16 @@ __global__ void k_mix_argmax(MixArgs m) {
     const int i2 = __shfl_xor(bi, o, 64);
     argmax_merge(best, bi, v2, i2);
   }
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  if (lane == 0) { rv[w] = best; ri[w] = bi; }
+  if (lane == 0) {
+    rv[wave] = best;
+    ri[wave] = bi;
+  }
   __syncthreads();
-  if (threadIdx.x == 0) {
-    for (int k = 1; k < (int)(blockDim.x >> 6); ++k) argmax_merge(best, bi, rv[k], ri[k]);
-    const int nch = (m.V + m.chunk - 1) / m.chunk;
-    float *o = m.cand + ((size_t)b * nch + c) * 2;
-    o[0] = best;
-    o[1] = __int_as_float(bi);
-    if (c == 0 && m.alpha) m.alpha[b] = alpha;
+  if (t == 0) {
+    for (int w = 1; w < 4; ++w) argmax_merge(best, bi, rv[w], ri[w]);
+    if (m.next) m.next[b] = bi;
+    if (m.alpha) m.alpha[b] = alpha;
   }
-}
-
-// Merge the chunk candidates of each sequence in chunk order.
-__global__ void k_mix_final(MixArgs m) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= m.rows.B) return;
-  const int nch = (m.V + m.chunk - 1) / m.chunk;
-  float best = -INFINITY;
-  int bi = 0x7fffffff;
-  for (int c = 0; c < nch; ++c) {
-    const float *o = m.cand + ((size_t)b * nch + c) * 2;
-    argmax_merge(best, bi, o[0], __float_as_int(o[1]));
-  }
-  if (m.next) m.next[b] = bi;
 }
 
 }  // namespace
@@ -654,10 +715,19 @@ hipError_t launch_kv_fill(KVRef kv, int seq, int start, int count, const void *k
 }
 
 hipError_t launch_mixture(const MixArgs &m, hipStream_t st) {
-  const int nch = (m.V + m.chunk - 1) / m.chunk;
-  if (!m.stats_ready) hipLaunchKernelGGL(k_mix_stats, dim3(nch, m.rows.np * m.rows.B), dim3(256), 0, st, m);
-  hipLaunchKernelGGL(k_mix_argmax, dim3(nch, m.rows.B), dim3(256), 0, st, m);
-  hipLaunchKernelGGL(k_mix_final, dim3((m.rows.B + 63) / 64), dim3(64), 0, st, m);
+  // k_mix_select keeps the list of kept tiles (at most 4096) in LDS
+  if (m.nstat < 1 || m.nstat > 4096 || m.rows.np < 1 || m.rows.np > 4 || m.tile_w < 1) return hipErrorInvalidValue;
+  if (!m.stats_ready) {
+    const int nch = (m.V + m.chunk - 1) / m.chunk;
+    hipLaunchKernelGGL(k_mix_stats, dim3(nch, m.rows.np * m.rows.B), dim3(256), 0, st, m);
+  }
+  const dim3 grid(m.rows.B), block(256);
+  switch (m.rows.np) {
+    case 1: hipLaunchKernelGGL(k_mix_select<1>, grid, block, 0, st, m); break;
+    case 2: hipLaunchKernelGGL(k_mix_select<2>, grid, block, 0, st, m); break;
+    case 3: hipLaunchKernelGGL(k_mix_select<3>, grid, block, 0, st, m); break;
+    default: hipLaunchKernelGGL(k_mix_select<4>, grid, block, 0, st, m); break;
+  }
   return hipGetLastError();
 }
 

@@ -400,6 +400,8 @@ void launch_glu_mb(dim3 grid, hipStream_t st, const WSegs &segs, int K, const ui
 
 static int gemm_rows_per_wg(const GemmConfig &g) { return g.NW * 16 * g.RB; }
 
+int gemm_tile_rows(const GemmConfig &g) { return gemm_rows_per_wg(g); }
+
 int gemm_stats_tiles(int N, const GemmConfig &g, int dtype) {
   return (dtype == 1 && g.S == 1) ? (N + gemm_rows_per_wg(g) - 1) / gemm_rows_per_wg(g) : 0;
 }

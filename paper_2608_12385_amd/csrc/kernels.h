@@ -74,6 +74,7 @@ hipError_t launch_gemm(const WSegs &segs, int N, int K, int dtype, const void *X
 // Tiles per row of the statistics the output projection writes when given
 // row_stats (0: this shape does not produce them).
 int gemm_stats_tiles(int N, const GemmConfig &g, int dtype);
+int gemm_tile_rows(const GemmConfig &g);  // weight rows (output columns) per workgroup
 
 // ---- row-wise and elementwise stages ----
 struct StepBegin {
@@ -166,11 +167,11 @@ struct MixArgs {
   const float *logits;  // [(1 + n_b) Bp][V]
   int V;
   Rows rows;            // np = 1 + n_b with the branches on (n_b <= 3), 1 (primary) otherwise
-  int chunk;            // vocabulary entries per argmax chunk
-  float *stats;         // [2Bp][nstat][3] per-tile (max, sum e^(z-max), sum e^(2(z-max)))
+  int chunk;            // vocabulary entries per statistics chunk when the projection wrote none
+  float *stats;         // [(1 + n_b) Bp][nstat][3] per tile (max, sum e^(z-max), sum e^(2(z-max)))
   int nstat;            // tiles per row in stats
-  int stats_ready;      // 1: the output projection already wrote stats (tiles of 256)
-  float *cand;          // [B][nchunks][2] (value, index as float bits)
+  int tile_w;           // vocabulary entries per tile (the projection's rows per workgroup, or chunk)
+  int stats_ready;      // 1: the output projection already wrote stats
   float *alpha;         // [B] or NULL
   int *next;            // [B] or NULL
 };

@@ -300,3 +300,81 @@ def test_layer8b_full_size_modes_bitwise(layer8b):
     for k in ("h1_out", "h2_out", "logits1", "logits2", "alpha", "next_token"):
         np.testing.assert_array_equal(on[k], ug[k], err_msg=k)
     assert bool((on["k"] == ug["k"]).all()) and bool((on["v"] == ug["v"]).all())
+
+
+# ----------------------------------------------------------------------------
+# mixture selection: the greedy token reads only tiles whose bound can reach
+# the maximum; it must equal the full scan of the mixture
+# ----------------------------------------------------------------------------
+
+def _host_mixture(z1, z2):
+    """Eqs. (17)-(18) in float64 on given logits: alpha, m, lowest argmax."""
+    z1 = np.asarray(z1, np.float64)
+    z2 = np.asarray(z2, np.float64)
+    p = np.exp(z1 - z1.max(axis=1, keepdims=True))
+    p /= p.sum(axis=1, keepdims=True)
+    q = np.exp(z2 - z2.max(axis=1, keepdims=True))
+    q /= q.sum(axis=1, keepdims=True)
+    alpha = np.clip((p * p).sum(axis=1), 0.5, 1.0)
+    m = alpha[:, None] * p + (1 - alpha[:, None]) * q
+    return alpha, m, np.argmax(m, axis=1)
+
+
+def _check_select(t, tag):
+    alpha, m, nxt = _host_mixture(_np(t["logits1"]), _np(t["logits2"]))
+    np.testing.assert_allclose(_np(t["alpha"]), alpha, rtol=1e-5, err_msg=tag)
+    got = _np(t["next_token"])
+    for i in range(len(nxt)):
+        if got[i] != nxt[i]:   # only a value within fp32 rounding of the maximum
+            assert m[i, got[i]] >= m[i].max() * (1 - 1e-5), (tag, i, got[i], nxt[i])
+
+
+@pytest.mark.slow
+def test_layer8b_mixture_select_equals_full_scan(layer8b):
+    """All 32 sequences at full size (251 tiles of 512 entries per row)."""
+    shape, W, sess, B, L = layer8b
+    for step in range(2):
+        h = synth.make_hidden(shape, B, step=step, seed=5)
+        t = sess.decode(h1=h[0], h2=h[1])
+        _truncate_all(sess, B, L)
+        _check_select(t, f"step {step}")
+
+
+@pytest.mark.parametrize("pattern", ["equal_rows", "staircase"])
+def test_mixture_select_degenerate_heads(pattern):
+    """Output matrices whose logits tie everywhere (equal rows: every tile is
+    kept) or rise by tiny steps across the vocabulary (many tiles within
+    rounding of the maximum); the token must be the full scan's, or within
+    fp32 rounding of its value."""
+    shape = _small_bf16(n_layers=1, vocab=1024, has_embeddings=False)
+    W = synth.make_weights(shape, seed=0)
+    V, d = shape.vocab, shape.d_model
+    base = W.values["W_out"][0].astype(np.float64)
+    if pattern == "equal_rows":
+        wo = np.tile(base, (V, 1))
+    else:
+        wo = np.outer(1.0 + np.arange(V) / (4.0 * V), base)
+    bits = synth.bf16_bits(wo.astype(np.float32))
+    W.values["W_out"] = synth.bf16_values(bits)
+    W.bits["W_out"] = bits
+    lengths = [5, 40, 17]
+    sess = make_session(shape, W, max_batch=3, max_pos=64)
+    fill_cache(sess, None, shape, lengths)
+    from paper_2608_12385_amd import binding
+    for branch_on in (True, False):
+        h = synth.make_hidden(shape, 3, step=0, seed=2)
+        t = sess.decode(h1=h[0], h2=h[1], branch_on=branch_on)
+        for b, L in enumerate(lengths):
+            binding.dbt_kv_truncate(sess.kv, b, L)
+        if branch_on:
+            _check_select(t, pattern)
+        else:
+            z1 = _np(t["logits1"])
+            np.testing.assert_array_equal(_np(t["next_token"]), np.argmax(z1, axis=1))
+        if pattern == "equal_rows":
+            # every entry of a row is the same product up to the summation
+            # order of its tile (each tile starts at its own chunk)
+            z1 = _np(t["logits1"]).astype(np.float64)
+            spread = (z1.max(axis=1) - z1.min(axis=1)) / np.abs(z1).max(axis=1)
+            assert spread.max() <= 1e-5, spread
+    sess.close()
