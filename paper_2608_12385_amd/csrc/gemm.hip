@@ -32,11 +32,12 @@ constexpr int kLdsRow = kChunk + 8;  // padded LDS row of a staged activation ch
 // in MFMA operand layout, so larger workgroups re-read the activations from
 // L2 less often per weight byte.
 //
-// Pipeline: the weights and the activations of chunk c+PD are loaded together
-// while chunk c is multiplied; the activation chunk c+1, loaded PD chunks
-// earlier, is then written to the other of two LDS slots.  Vector loads
-// complete in issue order, so that write only waits for loads that are
-// already consumed and the PD chunks of weights behind it stay in flight.
+// Pipeline: while chunk c is multiplied, the activations of chunk c+2 and
+// the weights of chunk c+PD are loaded; the activation chunk c+1, loaded one
+// step earlier, is then written to the other of two LDS slots.  Vector loads
+// complete in issue order, so that write never waits for the loads just
+// issued (whatever the weight depth PD), and the weights behind it stay in
+// flight.
 // Loads are never predicated (rows past M re-read row M-1, chunks past the
 // end re-read the last one), and the loop body always runs PD chunks, so the
 // compiler's wait counts stay exact across the loop's back edge.
@@ -114,13 +115,18 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
 #pragma unroll
     for (int cb = 0; cb < MB; ++cb) acc[rb][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  u32x4 a[PD][RB][4], stg[PD][PPT];
-  auto load = [&](int slot, int c) {  // logical chunk c (clamped) of this workgroup's rotated order
+  u32x4 a[PD][RB][4], stg[2][PPT];
+  auto koff = [&](int c) {  // logical chunk c (clamped) of this workgroup's rotated order
     c = min(c, nch - 1) + crot;
-    c = c >= nch ? c - nch : c;
-    const int ko = c * kChunk;
+    return (c >= nch ? c - nch : c) * kChunk;
+  };
+  auto xload = [&](int slot, int c) {
+    const int ko = koff(c);
 #pragma unroll
     for (int j = 0; j < PPT; ++j) stg[slot][j] = *(const u32x4 *)(xsrc[j] + ko);
+  };
+  auto wload = [&](int slot, int c) {
+    const int ko = koff(c);
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
@@ -131,8 +137,11 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
     for (int j = 0; j < PPT; ++j)
       if (PIECES % (NW * 64) == 0 || xdst[j] >= 0) *(u32x4 *)(&xs[lds][xdst[j]]) = stg[slot][j];
   };
-  auto step = [&](int c, int u) {  // multiply chunk c (ring slot u), refill, stage chunk c+1
-    const uint16_t *xl = xs[c & 1];
+  // multiply chunk c (weight ring slot w, activation slot par = c & 1); load
+  // the activations of chunk c+2 and the weights of chunk c+PD; stage chunk
+  // c+1 (loaded one step ago).  w and par are compile-time at every call.
+  auto step = [&](int c, int w, int par) {
+    const uint16_t *xl = xs[par];
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
       u32x4 bx[MB];
@@ -142,27 +151,34 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
       for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
         for (int cb = 0; cb < MB; ++cb)
-          acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a[u][rb][s]),
+          acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a[w][rb][s]),
                                                                 __builtin_bit_cast(bf16x8, bx[cb]), acc[rb][cb], 0, 0,
                                                                 0);
     }
-    load(u, c + PD);
-    xstore((c + 1) & 1, (u + 1) % PD);
+    xload(par, c + 2);
+    wload(w, c + PD);
+    xstore(par ^ 1, par ^ 1);
     __syncthreads();
   };
 
+  xload(0, 0);
+  xload(1, 1);
 #pragma unroll
-  for (int u = 0; u < PD; ++u) load(u, u);
+  for (int u = 0; u < PD; ++u) wload(u, u);
   xstore(0, 0);
   __syncthreads();
+  // rounds of P2 chunks (a multiple of PD and of 2, so both ring positions
+  // are constants); the round's loads are the same every time, which keeps
+  // the wait counts exact across the loop's back edge
+  constexpr int P2 = PD % 2 == 0 ? PD : 2 * PD;
   int c0 = 0;
-  for (; c0 + PD <= nch; c0 += PD) {
+  for (; c0 + P2 <= nch; c0 += P2) {
 #pragma unroll
-    for (int u = 0; u < PD; ++u) step(c0 + u, u);
+    for (int u = 0; u < P2; ++u) step(c0 + u, u % PD, u & 1);
   }
 #pragma unroll
-  for (int u = 0; u + 1 < PD; ++u)
-    if (c0 + u < nch) step(c0 + u, u);
+  for (int u = 0; u + 1 < P2; ++u)
+    if (c0 + u < nch) step(c0 + u, u % PD, u & 1);
   // lane holds D[n = rb*16 + 4*gq + i][m = cb*16 + r]: Y[m][n .. n+3]
   if constexpr (GLU) {
     // hb[m][c]: the tile's TC gate/up columns c for activation row m
