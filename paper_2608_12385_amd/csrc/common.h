@@ -40,6 +40,26 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// Sum of S split-K partial slabs (stride apart) at idx, in split order.
+__device__ __forceinline__ float psum(const float *part, long long stride, int S, size_t idx) {
+  float v[16];
+#pragma unroll
+  for (int k = 0; k < 16; ++k) v[k] = k < S ? part[k * stride + idx] : 0.f;
+  float s = 0.f;
+#pragma unroll
+  for (int k = 0; k < 16; ++k)
+    if (k < S) s += v[k];
+  return s;
+}
+
+// RoPE of the pair (x0, x1) = (v_i, v_{i+d_h/2}) by the angle with (cos, sin)
+// = cs, and the query coupling q2 + a * q1, written with explicit fused
+// multiply-adds so that every kernel computing them rounds identically.
+__device__ __forceinline__ float2 rope_pair(float x0, float x1, float2 cs) {
+  return make_float2(fmaf(x0, cs.x, -(x1 * cs.y)), fmaf(x0, cs.y, x1 * cs.x));
+}
+__device__ __forceinline__ float couple(float a, float q1, float q2) { return fmaf(a, q1, q2); }
+
 // Sum over a block of up to 1024 threads in a fixed order (deterministic).
 // `red` must hold 16 floats; every thread gets the result.
 __device__ __forceinline__ float block_sum(float v, float *red) {

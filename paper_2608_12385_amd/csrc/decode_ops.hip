@@ -19,16 +19,6 @@ namespace {
 __device__ __forceinline__ int phys_row(const Rows &r, int path, int b) { return path * r.Bp + b; }
 
 // Sum of the split-K partial slabs in split order (S <= 16).
-__device__ __forceinline__ float psum(const float *part, long long stride, int S, size_t idx) {
-  float v[16];
-#pragma unroll
-  for (int k = 0; k < 16; ++k) v[k] = k < S ? part[k * stride + idx] : 0.f;
-  float s = 0.f;
-#pragma unroll
-  for (int k = 0; k < 16; ++k)
-    if (k < S) s += v[k];
-  return s;
-}
 
 // ---------------------------------------------------------------------------
 
@@ -165,10 +155,10 @@ __global__ void k_qkv_finish(QKVFinish f) {
     const int c0 = (pi / half) * f.d_h + i, c1 = c0 + half;
     float q1a = 0.f, q1b = 0.f;
     if (prim) {
-      const float x0 = psum(f.part, f.split_stride, f.S, (size_t)r1 * f.ldp + c0);
-      const float x1 = psum(f.part, f.split_stride, f.S, (size_t)r1 * f.ldp + c1);
-      q1a = x0 * cs.x - x1 * cs.y;
-      q1b = x0 * cs.y + x1 * cs.x;
+      const float2 q1 = rope_pair(psum(f.part, f.split_stride, f.S, (size_t)r1 * f.ldp + c0),
+                                  psum(f.part, f.split_stride, f.S, (size_t)r1 * f.ldp + c1), cs);
+      q1a = q1.x;
+      q1b = q1.y;
       f.Q[(size_t)r1 * dq + c0] = q1a;
       f.Q[(size_t)r1 * dq + c1] = q1b;
       if (f.ret.ptr && (f.ret.src_row < 0 || f.ret.src_row == b)) {
@@ -183,12 +173,10 @@ __global__ void k_qkv_finish(QKVFinish f) {
     if (br)
       for (int p = pb0; p < pb1; ++p) {  // every branch couples to Q1 with the shared a
         const int r2 = phys_row(f.rows, p, b);
-        const float y0 = psum(f.part, f.split_stride, f.S, (size_t)r2 * f.ldp + c0);
-        const float y1 = psum(f.part, f.split_stride, f.S, (size_t)r2 * f.ldp + c1);
-        const float q2a = y0 * cs.x - y1 * cs.y;
-        const float q2b = y0 * cs.y + y1 * cs.x;
-        f.Q[(size_t)r2 * dq + c0] = q2a + f.a[c0] * q1a;
-        f.Q[(size_t)r2 * dq + c1] = q2b + f.a[c1] * q1b;
+        const float2 q2 = rope_pair(psum(f.part, f.split_stride, f.S, (size_t)r2 * f.ldp + c0),
+                                    psum(f.part, f.split_stride, f.S, (size_t)r2 * f.ldp + c1), cs);
+        f.Q[(size_t)r2 * dq + c0] = couple(f.a[c0], q1a, q2.x);
+        f.Q[(size_t)r2 * dq + c1] = couple(f.a[c1], q1b, q2.y);
       }
     return;
   }
@@ -201,11 +189,11 @@ __global__ void k_qkv_finish(QKVFinish f) {
   if (j < nkp) {
     const int g = j / half;
     const int c0 = dq + g * f.d_h + i;
-    const float x0 = psum(f.part, f.split_stride, f.S, (size_t)r1 * f.ldp + c0);
-    const float x1 = psum(f.part, f.split_stride, f.S, (size_t)r1 * f.ldp + c0 + half);
+    const float2 k = rope_pair(psum(f.part, f.split_stride, f.S, (size_t)r1 * f.ldp + c0),
+                               psum(f.part, f.split_stride, f.S, (size_t)r1 * f.ldp + c0 + half), cs);
     const size_t base = (((size_t)page * f.n_kv + g) * 16 + slot) * f.d_h;
-    st<T>(kp, base + i, x0 * cs.x - x1 * cs.y);
-    st<T>(kp, base + i + half, x0 * cs.y + x1 * cs.x);
+    st<T>(kp, base + i, k.x);
+    st<T>(kp, base + i + half, k.y);
   } else {
     const int g = (j - nkp) / half;
     const int c0 = dq + dkv + g * f.d_h + i;
