@@ -88,7 +88,7 @@ def traffic_summary(fetch_path, write_path):
     the 256 MiB device-to-device copies bench.py --calib-copy launches (the only
     copies of that size in the run).  The runs use --grouped-only, so every
     dispatch after the last calibration copy belongs to a grouped step; steps
-    are counted by the mixture's final kernel (one launch per step)."""
+    are counted by the mixture kernel (one launch per step)."""
     lines, steps = [], []
     res, step_bytes = {}, {}
     for counter, path in (("FETCH_SIZE", fetch_path), ("WRITE_SIZE", write_path)):
@@ -102,7 +102,7 @@ def traffic_summary(fetch_path, write_path):
         lm = [v for k, v in after if _short(k) == LMHEAD_KERNEL]
         if not lm:
             raise SystemExit(f"{counter}: no {LMHEAD_KERNEL} dispatches")
-        n_steps = sum(1 for k, _ in after if _short(k) == "k_mix_final")
+        n_steps = sum(1 for k, _ in after if _short(k).startswith("k_mix_select"))
         kib = sum(lm) / len(lm)
         res[counter] = kib * 1024 * factor
         step_bytes[counter] = sum(v for _, v in after) * 1024 * factor / max(n_steps, 1)
