@@ -42,13 +42,9 @@ __device__ __forceinline__ float wave_max(float v) {
 
 // Sum of S split-K partial slabs (stride apart) at idx, in split order.
 __device__ __forceinline__ float psum(const float *part, long long stride, int S, size_t idx) {
-  float v[16];
-#pragma unroll
-  for (int k = 0; k < 16; ++k) v[k] = k < S ? part[k * stride + idx] : 0.f;
   float s = 0.f;
-#pragma unroll
-  for (int k = 0; k < 16; ++k)
-    if (k < S) s += v[k];
+#pragma unroll 4
+  for (int k = 0; k < S; ++k) s += part[k * stride + idx];
   return s;
 }
 

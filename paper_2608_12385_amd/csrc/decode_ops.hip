@@ -60,13 +60,9 @@ __device__ __forceinline__ float4 mul4(float4 a, float s, float4 g) {
   return make_float4(a.x * s * g.x, a.y * s * g.y, a.z * s * g.z, a.w * s * g.w);
 }
 __device__ __forceinline__ float4 psum4(const float *part, long long stride, int S, size_t idx4) {
-  float4 v[16];
-#pragma unroll
-  for (int k = 0; k < 16; ++k) v[k] = k < S ? ((const float4 *)(part + k * stride))[idx4] : make_float4(0.f, 0.f, 0.f, 0.f);
   float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-  for (int k = 0; k < 16; ++k)
-    if (k < S) s = add4(s, v[k]);
+#pragma unroll 4
+  for (int k = 0; k < S; ++k) s = add4(s, ((const float4 *)(part + k * stride))[idx4]);
   return s;
 }
 
