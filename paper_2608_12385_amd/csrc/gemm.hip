@@ -362,8 +362,9 @@ GemmConfig gemm_config(int n_full, int K, int dtype, int seg_gran, int max_rows)
   if (dtype != 1) return g;
   if (n_full >= 65536 && seg_gran == n_full && n_full % 64 == 0) {
     // output-matrix shapes (one segment): 16 waves x 32 rows = 512 rows per
-    // workgroup, so each staged activation chunk serves 512 weight rows
-    g = GemmConfig{2, 1, 1, 16};
+    // workgroup, so each staged activation chunk serves 512 weight rows; above
+    // 96 stacked rows (its accumulators would spill at 16 waves) 8 waves x 32
+    g = max_rows <= 96 ? GemmConfig{2, 1, 1, 16} : GemmConfig{2, 1, 1, 8};
   } else if (n_full >= 16384 && seg_gran % 128 == 0) {
     g = GemmConfig{2, 2, 1, 4};    // MLP up projections
   } else {
@@ -396,8 +397,8 @@ void launch_mb(const GemmConfig &g, dim3 grid, hipStream_t st, const WSegs &segs
   const GluEpi none{};
   if (g.NW == 16)
     hipLaunchKernelGGL((k_gemm_bf16<MB, 2, 1, 16>), grid, dim3(1024), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs, none);
-  else if (g.NW == 8 && g.RB == 4)
-    hipLaunchKernelGGL((k_gemm_bf16<MB, 4, 1, 8>), grid, dim3(512), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs, none);
+  else if (g.NW == 8 && g.RB == 2)
+    hipLaunchKernelGGL((k_gemm_bf16<MB, 2, 1, 8>), grid, dim3(512), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs, none);
   else if (g.NW == 8)
     hipLaunchKernelGGL((k_gemm_bf16<MB, 1, 2, 8>), grid, dim3(512), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs, none);
   else if (g.RB == 2)
