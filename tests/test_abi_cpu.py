@@ -72,6 +72,26 @@ def test_config_checks():
         assert B.dbt_workspace_bytes(hid) > 0, mb
 
 
+def test_branch_count_checks():
+    """More decode branches (App. C.1): 0..3 (0 reads as one), dense MLPs only,
+    and every branch's query heads of a KV group must fit the attention tile
+    ((1 + n_branches) * n_q / n_kv <= 16)."""
+    bf = dict(dtype=B.DBT_BF16, d_model=512, n_q_heads=8, n_kv_heads=2, head_dim=128, d_ff=1024, vocab=512)
+    one = B.dbt_workspace_bytes(_cfg(**bf, n_branches=1))
+    assert one > 0 and B.dbt_workspace_bytes(_cfg(**bf, n_branches=0)) == one
+    # three branches: 4 paths x 4 query heads per KV head = 16 rows; more rows need more workspace
+    assert B.dbt_workspace_bytes(_cfg(**bf, n_branches=3)) > one
+    w, _keep = _fake_weights(_cfg())
+    for bad, status in [(dict(bf, n_branches=4), 1), (dict(bf, n_branches=-1), 1),
+                        (dict(bf, n_branches=3, n_q_heads=16, n_kv_heads=2), 5),
+                        (dict(bf, n_branches=2, n_experts=4, d_ff_expert=128, top_k1=2, top_k2=2,
+                              d_model=512, d_ff=0), 5)]:
+        assert B.dbt_workspace_bytes(_cfg(**bad)) == 0, bad
+        with pytest.raises(B.DbtError) as e:
+            B.dbt_create(_cfg(**bad), w, FAKE)
+        assert e.value.status == status, (bad, e.value)
+
+
 def test_create_rejects_null_and_misaligned():
     cfg = _cfg()
     w, _keep = _fake_weights(cfg)
