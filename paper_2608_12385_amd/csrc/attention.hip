@@ -54,13 +54,20 @@ __device__ __forceinline__ u32x4 mask8(u32x4 v, int first, int nvalid) {
 }
 
 // Requires d_h == 128, np*G <= 16 and pages_per_split <= 128.
-__global__ __launch_bounds__(256) void k_attn_decode_bf16(AttnArgs a) {
+// NW = 4: one split of the sequence per workgroup, partials merged by
+// k_attn_combine.  NW = 8 (a.single): the whole sequence in one workgroup of
+// eight waves (at most 1024 pages, page ids staged in LDS), the waves merged
+// in LDS and the normalised rows written to a.O directly.
+template <int NW>
+__global__ __launch_bounds__(NW * 64) void k_attn_decode_bf16(AttnArgs a) {
   constexpr int DH = 128;
+  constexpr bool SINGLE = NW == 8;
   const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int len = a.pos_arr[b] + 1;
   const int npages = (len + 15) >> 4;
-  int pb, pe;
-  if (!split_range(npages, a.pages_per_split, split, &pb, &pe)) return;
+  int pb = 0, pe = npages;
+  if (SINGLE && npages > 1024) return;  // excluded by the host
+  if (!SINGLE && !split_range(npages, a.pages_per_split, split, &pb, &pe)) return;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r = lane & 15, gq = lane >> 4;
   const int n_kv = a.kv.n_kv;
@@ -70,9 +77,19 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(AttnArgs a) {
   const float scale = kLog2e / sqrtf((float)DH);
   // page ids of the split: lane i holds pages pb + i and pb + 64 + i
   const int *ptab = a.kv.page_table + (size_t)b * a.kv.mpps;
-  const int myid0 = (pb + lane < pe) ? ptab[pb + lane] : 0;
-  const int myid1 = (pb + 64 + lane < pe) ? ptab[pb + 64 + lane] : 0;
-  auto page_id = [&](int j) { return __shfl(j < 64 ? myid0 : myid1, j & 63, 64); };
+  __shared__ int pid_s[SINGLE ? 1024 : 1];
+  int myid0 = 0, myid1 = 0;
+  if constexpr (SINGLE) {
+    for (int i = threadIdx.x; i < npages; i += NW * 64) pid_s[i] = ptab[i];
+    __syncthreads();
+  } else {
+    myid0 = (pb + lane < pe) ? ptab[pb + lane] : 0;
+    myid1 = (pb + 64 + lane < pe) ? ptab[pb + 64 + lane] : 0;
+  }
+  auto page_id = [&](int j) {
+    if constexpr (SINGLE) return pid_s[j];
+    else return __shfl(j < 64 ? myid0 : myid1, j & 63, 64);
+  };
 
   // Query operand: lane (query r, group gq) holds Q[r][s*32 + gq*8 .. +8].
   u32x4 qf[4];
@@ -104,7 +121,7 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(AttnArgs a) {
   const int kpage = r >> 3, kpos = 8 * ((r >> 2) & 1) + (r & 3);
   const int vpage = gq >> 1, vpos = 8 * (gq & 1);
   const int npairs = (pe - pb + 1) >> 1;
-  for (int q = wave; q < npairs; q += 4) {
+  for (int q = wave; q < npairs; q += NW) {
     const int pg0 = pb + 2 * q;                 // first page of the pair
     const int last = pe - pb - 1;               // a missing second page re-reads the first (masked)
     const int phys0 = page_id(2 * q);
@@ -177,9 +194,9 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(AttnArgs a) {
   l_run += __shfl_xor(l_run, 16, 64);
   l_run += __shfl_xor(l_run, 32, 64);
 
-  // merge the four waves: acc holds O^T[dh = 16c + 4gq + i][query r]
-  __shared__ float so[4][DH][17];
-  __shared__ float sm[4][16], sl[4][16];
+  // merge the waves: acc holds O^T[dh = 16c + 4gq + i][query r]
+  __shared__ float so[NW][DH][17];
+  __shared__ float sm[NW][16], sl[NW][16];
 #pragma unroll
   for (int c = 0; c < 8; ++c)
 #pragma unroll
@@ -190,24 +207,29 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(AttnArgs a) {
   }
   __syncthreads();
   const size_t obase = (((size_t)b * n_kv + g) * a.max_splits + split) * 16;
-  for (int e = threadIdx.x; e < nrows * DH; e += 256) {
+  for (int e = threadIdx.x; e < nrows * DH; e += NW * 64) {
     const int qr = e / DH, dh = e % DH;
     float mx = -INFINITY;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) mx = fmaxf(mx, sm[w][qr]);
+    for (int w = 0; w < NW; ++w) mx = fmaxf(mx, sm[w][qr]);
     float o = 0.f, l = 0.f;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
+    for (int w = 0; w < NW; ++w) {
       if (sm[w][qr] != -INFINITY) {
         const float f = exp2f(sm[w][qr] - mx);
         o += so[w][dh][qr] * f;
         l += sl[w][qr] * f;
       }
     }
-    a.opart[(obase + qr) * DH + dh] = o;
-    if (dh == 0) {
-      a.ostat[(obase + qr) * 2 + 0] = mx;
-      a.ostat[(obase + qr) * 2 + 1] = l;
+    if constexpr (SINGLE) {
+      const int path = a.rows.p0 + qr / G, head = g * G + qr % G;
+      ((uint16_t *)a.O)[(size_t)(path * a.rows.Bp + b) * a.ldo + head * DH + dh] = f2bf(o / l);
+    } else {
+      a.opart[(obase + qr) * DH + dh] = o;
+      if (dh == 0) {
+        a.ostat[(obase + qr) * 2 + 0] = mx;
+        a.ostat[(obase + qr) * 2 + 1] = l;
+      }
     }
   }
 }
@@ -527,8 +549,10 @@ hipError_t launch_attn_decode(const AttnArgs &a, hipStream_t st) {
   // the bf16 kernel holds two page ids per lane, the fp32 one 1024 positions in LDS
   if (a.pages_per_split < 1 || a.pages_per_split > (a.dtype == 1 ? 128 : 64)) return hipErrorInvalidValue;
   dim3 grid(a.max_splits, a.kv.n_kv, a.rows.B);
-  if (a.dtype == 1)
-    hipLaunchKernelGGL(k_attn_decode_bf16, grid, dim3(256), 0, st, a);
+  if (a.dtype == 1 && a.single)
+    hipLaunchKernelGGL(k_attn_decode_bf16<8>, dim3(1, a.kv.n_kv, a.rows.B), dim3(512), 0, st, a);
+  else if (a.dtype == 1)
+    hipLaunchKernelGGL(k_attn_decode_bf16<4>, grid, dim3(256), 0, st, a);
   else
     hipLaunchKernelGGL(k_attn_decode_f32, grid, dim3(256), 0, st, a);
   return hipGetLastError();

@@ -556,11 +556,19 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
     aa.opart = m->at<float>(L.apart);
     aa.ostat = m->at<float>(L.astat);
     aa.dtype = cf.dtype;
+    // When the batch fills the chip (B x n_kv >= 256 workgroups), each
+    // (sequence, KV head) is read by one eight-wave workgroup and no partials
+    // are merged.  The choice depends on the batch, never on the branch.
+    int maxlen = 0;
+    for (int b = 0; b < c.rows.B; ++b) maxlen = std::max(maxlen, kv->len[b] + 1);
+    aa.single = cf.dtype == DBT_BF16 && c.rows.B * cf.n_kv_heads >= 256 && (maxlen + kPage - 1) / kPage <= 1024;
+    aa.O = O;
+    aa.ldo = dq;
     {
       Timed tm(m, DBT_STAGE_ATTN, st);
       HIPCHK(launch_attn_decode(aa, st));
     }
-    HIPCHK(launch_attn_combine(aa, O, dq, st));
+    if (!aa.single) HIPCHK(launch_attn_combine(aa, O, dq, st));
   }
 
   // 3. output projection + residual + MLP norm

@@ -150,6 +150,12 @@ struct AttnArgs {
   float *opart;  // [B][n_kv][max_splits][16][d_h]
   float *ostat;  // [B][n_kv][max_splits][16][2]
   int dtype;
+  // bf16, every sequence at most 1024 pages: one workgroup of eight waves per
+  // (sequence, KV head) writes the normalised rows to O (bf16, row stride
+  // ldo); no partials and no combine launch
+  int single;
+  void *O;
+  int ldo;
 };
 hipError_t launch_attn_decode(const AttnArgs &a, hipStream_t st);
 hipError_t launch_attn_combine(const AttnArgs &a, void *O, int ldo, hipStream_t st);
