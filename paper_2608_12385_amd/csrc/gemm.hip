@@ -266,7 +266,7 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
         if (rvalid[rb])
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            const float e = expf(acc[rb][cb][i] - mx);
+            const float e = __expf(acc[rb][cb][i] - mx);  // fast exp: lse and alpha need ~1e-6
             e1 += e;
             e2 += e * e;
           }
