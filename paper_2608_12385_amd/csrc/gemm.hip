@@ -383,7 +383,7 @@ GemmConfig gemm_config(int n_full, int K, int dtype, int seg_gran, int max_rows)
     const int t4 = std::max(1, n_full / 64), t8 = std::max(1, n_full / 128);
     const int s4 = splits(t4), s8 = splits(t8);
     if (seg_gran % 128 == 0 && t8 * s8 > t4 * s4)
-      g = GemmConfig{1, 2, s8, 8};
+      g = GemmConfig{1, 1, s8, 8};
     else
       g = GemmConfig{1, 2, s4, 4};
   }
@@ -400,7 +400,7 @@ void launch_mb(const GemmConfig &g, dim3 grid, hipStream_t st, const WSegs &segs
   else if (g.NW == 8 && g.RB == 2)
     hipLaunchKernelGGL((k_gemm_bf16<MB, 2, 1, 8>), grid, dim3(512), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs, none);
   else if (g.NW == 8)
-    hipLaunchKernelGGL((k_gemm_bf16<MB, 1, 2, 8>), grid, dim3(512), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs, none);
+    hipLaunchKernelGGL((k_gemm_bf16<MB, 1, 1, 8>), grid, dim3(512), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs, none);
   else if (g.RB == 2)
     hipLaunchKernelGGL((k_gemm_bf16<MB, 2, 2, 4>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs, none);
   else
@@ -410,7 +410,7 @@ void launch_mb(const GemmConfig &g, dim3 grid, hipStream_t st, const WSegs &segs
 template <int MB>
 void launch_glu_mb(dim3 grid, hipStream_t st, const WSegs &segs, int K, const uint16_t *X, int ldx, int M,
                    const GluEpi &ep) {
-  hipLaunchKernelGGL((k_gemm_bf16<MB, 1, 2, 8, true>), grid, dim3(512), 0, st, segs, K, X, ldx, M, nullptr, 0, 0LL,
+  hipLaunchKernelGGL((k_gemm_bf16<MB, 1, 1, 8, true>), grid, dim3(512), 0, st, segs, K, X, ldx, M, nullptr, 0, 0LL,
                      nullptr, ep);
 }
 }  // namespace
