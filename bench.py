@@ -354,6 +354,8 @@ def main():
     ap.add_argument("--only", metavar="WORKLOAD", choices=("layer8b_bf16", "longctx_bf16", "moe_bf16", "full24_bf16"),
                     help="time only this other workload (one JSON line of its fields)")
     ap.add_argument("--top-k2", type=int, default=4, help="branch fan-out of --only moe_bf16")
+    ap.add_argument("--full24-steps", type=int, default=0,
+                    help="--only full24_bf16: greedy steps per mode (0: the workload's 256)")
     ap.add_argument("--branches", type=int, default=1,
                     help="--only layer8b_bf16/longctx_bf16: decode branches (App. C.1 of the paper)")
     ap.add_argument("--compute-matched", action="store_true",
@@ -379,7 +381,7 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     if args.only == "full24_bf16":
-        print(json.dumps(time_full24(0)))
+        print(json.dumps(time_full24(args.full24_steps)))
         return
     if args.only:
         kw = ({"top_k2": args.top_k2, "compute_matched": args.compute_matched} if args.only == "moe_bf16"
