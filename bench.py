@@ -121,10 +121,14 @@ def traffic_summary(fetch_path, write_path):
 
 
 def _sources_sha():
+    """Hash of the kernel sources a decode step runs (the prompt-only kernels
+    in csrc/prefill_*.hip never run in a decode step)."""
     import hashlib
     import glob
     h = hashlib.sha256()
     for f in sorted(glob.glob(os.path.join(ROOT, "paper_2608_12385_amd", "csrc", "*"))):
+        if os.path.basename(f).startswith("prefill_"):
+            continue
         with open(f, "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()

@@ -26,25 +26,6 @@ namespace dbt {
 
 namespace {
 
-constexpr float kLog2e = 1.4426950408889634f;
-
-// Two floats to packed bf16 with the hardware conversion (round to nearest
-// even, the same bits as f2bf for every non-NaN input).
-__device__ __forceinline__ uint32_t pack2(float lo, float hi) {
-  return __builtin_bit_cast(uint32_t, bf16x2{(__bf16)lo, (__bf16)hi});
-}
-
-// Maximum over lanes l, l^16, l^32 and l^48 (one column of a 16x16 MFMA
-// result held by four 16-lane rows), with the row-swap permutes: no LDS
-// round trip.
-__device__ __forceinline__ float rows4_max(float x) {
-  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
-  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
-}
-
-// Zero the bf16 lanes of v (positions first .. first+7) at positions >= nvalid.
 // Split s of a sequence of npages pages: pages [*pb, *pe); false when the
 // sequence has fewer splits.
 __device__ __forceinline__ bool split_range(int npages, int target, int s, int *pb, int *pe) {
@@ -54,15 +35,6 @@ __device__ __forceinline__ bool split_range(int npages, int target, int s, int *
   *pb = s * pps;
   *pe = min(npages, *pb + pps);
   return *pb < *pe;
-}
-
-__device__ __forceinline__ u32x4 mask8(u32x4 v, int first, int nvalid) {
-#pragma unroll
-  for (int w = 0; w < 4; ++w) {
-    if (first + 2 * w >= nvalid) v[w] &= 0xffff0000u;
-    if (first + 2 * w + 1 >= nvalid) v[w] &= 0x0000ffffu;
-  }
-  return v;
 }
 
 // Requires d_h == 128, np*G <= 16 and pages_per_split <= 128.
@@ -350,413 +322,6 @@ __global__ void k_attn_combine(AttnArgs a, T *O, int ldo) {
   st<T>(O, out + 3, o.w / l);
 }
 
-// Causal attention over the prompt of one sequence on MFMA (bf16 cache,
-// d_h = 128; Sec. 4.4, prefill through the primary path).  A workgroup owns
-// 16 consecutive query positions and one KV head; wave w is query head
-// g*G + w, so the G waves read the same K/V pages.  Each wave walks the page
-// pairs up to its last position with the decode kernel's permuted score rows
-// (lane: eight consecutive key positions of one page for one query), masks
-// keys after the query (causal) and cache slots past the prompt, and keeps an
-// online softmax per query row.  Tiles are issued longest first.
-__global__ __launch_bounds__(1024) void k_attn_prefill_bf16(const float *Q, int ldq, int T, KVRef kv, int seq,
-                                                           int n_q, uint16_t *O, int ldo) {
-  constexpr int DH = 128;
-  const int ntiles = (T + 15) >> 4;
-  const int q0 = (ntiles - 1 - (int)blockIdx.x) * 16;  // longest tiles first
-  const int g = blockIdx.y;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int r = lane & 15, gq = lane >> 4;
-  const int n_kv = kv.n_kv;
-  const int G = n_q / n_kv;
-  const int head = g * G + wave;
-  const float scale = kLog2e / sqrtf((float)DH);
-  const int qpos = q0 + r;  // query position of this lane's column
-  const int qlast = min(q0 + 15, T - 1);
-
-  u32x4 qf[4];
-  {
-    const bool valid = qpos < T;
-    const float *qp = Q + (size_t)(valid ? qpos : 0) * ldq + head * DH + gq * 8;
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      float x[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) x[e] = valid ? qp[s * 32 + e] : 0.f;
-      qf[s] = u32x4{pack2(x[0], x[1]), pack2(x[2], x[3]), pack2(x[4], x[5]), pack2(x[6], x[7])};
-    }
-  }
-  const uint16_t *kbase = (const uint16_t *)kv.k;
-  const uint16_t *vbase = (const uint16_t *)kv.v;
-  const int *ptab = kv.page_table + (size_t)seq * kv.mpps;
-  float m_run = -INFINITY, l_run = 0.f;
-  floatx4 acc[8];
-#pragma unroll
-  for (int c = 0; c < 8; ++c) acc[c] = floatx4{0.f, 0.f, 0.f, 0.f};
-  const int kpage = r >> 3, kpos = 8 * ((r >> 2) & 1) + (r & 3);
-  const int vpage = gq >> 1, vpos = 8 * (gq & 1);
-  const int npg = (qlast >> 4) + 1;  // pages holding keys 0..qlast
-  const int npairs = (npg + 1) >> 1;
-  int nid0 = ptab[0], nid1 = ptab[min(1, npg - 1)];
-  for (int q = 0; q < npairs; ++q) {
-    const int pg0 = 2 * q;
-    const int phys0 = nid0, phys1 = nid1;
-    if (q + 1 < npairs) {  // page ids of the next pair
-      nid0 = ptab[pg0 + 2];
-      nid1 = ptab[min(pg0 + 3, npg - 1)];
-    }
-    const int kphys = kpage ? phys1 : phys0;
-    const int vphys = vpage ? phys1 : phys0;
-    const uint16_t *kp = kbase + ((size_t)kphys * n_kv + g) * 16 * DH + kpos * DH + gq * 8;
-    const uint16_t *vp = vbase + ((size_t)vphys * n_kv + g) * DH * 16 + r * 16 + vpos;
-    u32x4 ka[4], kb[4], vf[8];
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      ka[s] = *(const u32x4 *)(kp + s * 32);
-      kb[s] = *(const u32x4 *)(kp + 4 * DH + s * 32);
-    }
-#pragma unroll
-    for (int c = 0; c < 8; ++c) vf[c] = *(const u32x4 *)(vp + c * 16 * 16);
-    floatx4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ka[s]),
-                                                   __builtin_bit_cast(bf16x8, qf[s]), s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kb[s]),
-                                                   __builtin_bit_cast(bf16x8, qf[s]), s1, 0, 0, 0);
-    }
-    // key position of this lane's first score; keys after the query are masked
-    const int kp0 = (pg0 + vpage) * 16 + vpos;
-    const bool page_ok = pg0 + vpage < npg;
-    float sc[8];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      sc[i] = (page_ok && kp0 + i <= qpos) ? s0[i] * scale : -INFINITY;
-      sc[4 + i] = (page_ok && kp0 + 4 + i <= qpos) ? s1[i] * scale : -INFINITY;
-    }
-    float mt = sc[0];
-#pragma unroll
-    for (int i = 1; i < 8; ++i) mt = fmaxf(mt, sc[i]);
-    mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
-    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-    const float m_new = fmaxf(m_run, mt);
-    // a query row with no key yet in this pair keeps m = -inf: use 0 as the base
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    float p[8];
-    float ps = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      p[i] = exp2f(sc[i] - m_use);
-      ps += p[i];
-    }
-    if (__any(m_new > m_run)) {
-      const float corr = m_run == -INFINITY ? 0.f : exp2f(m_run - m_new);
-      l_run *= corr;
-#pragma unroll
-      for (int c = 0; c < 8; ++c) acc[c] = acc[c] * corr;
-    }
-    l_run += ps;
-    m_run = m_new;
-    const u32x4 pf = u32x4{pack2(p[0], p[1]), pack2(p[2], p[3]), pack2(p[4], p[5]), pack2(p[6], p[7])};
-    // cache slots past the prompt (or a missing second page) may hold stale values
-    const int nv = page_ok ? min(16, T - (pg0 + vpage) * 16) : 0;
-    if (__any(nv < 16)) {
-#pragma unroll
-      for (int c = 0; c < 8; ++c) vf[c] = mask8(vf[c], vpos, nv);
-    }
-#pragma unroll
-    for (int c = 0; c < 8; ++c)
-      acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vf[c]),
-                                                       __builtin_bit_cast(bf16x8, pf), acc[c], 0, 0, 0);
-  }
-  l_run += __shfl_xor(l_run, 16, 64);
-  l_run += __shfl_xor(l_run, 32, 64);
-  if (qpos < T) {
-    const float inv = 1.f / l_run;
-    uint16_t *o = O + (size_t)qpos * ldo + head * DH;
-#pragma unroll
-    for (int c = 0; c < 8; ++c) {
-      const int dh = c * 16 + 4 * gq;
-      *(u32x2 *)(o + dh) = u32x2{pack2(acc[c][0] * inv, acc[c][1] * inv), pack2(acc[c][2] * inv, acc[c][3] * inv)};
-    }
-  }
-}
-
-// Longest prompt (in 16-position pages) of the LDS-shared prefill kernel.
-constexpr int kPrefillMaxPages = 1024;
-
-// Causal attention over the prompt of one sequence on MFMA, K/V shared
-// through LDS (bf16 cache, d_h = 128, G = n_q/n_kv dividing 16).  A
-// workgroup of 16 waves covers 256/G positions of all G query heads of KV
-// head g: wave w computes head g*G + (w % G) for positions
-// q0 + 16*(w / G) .. +15.  Each pair of K/V pages (32 keys, 16 KB) is loaded
-// once per workgroup, one 16-byte piece per thread, into one of two padded
-// LDS buffers while the previous pair is multiplied, so every key/value is
-// fetched once for 256 query rows.  The per-wave arithmetic is that of the
-// decode kernel (permuted score rows, online softmax in base 2) with a causal
-// mask per query row; a wave skips pairs that start after its last position.
-// Position tiles are issued longest first.
-template <int G>
-__global__ __launch_bounds__(1024) void k_attn_prefill_wide(const float *Q, int ldq, int T, KVRef kv, int seq,
-                                                            int n_q, uint16_t *O, int ldo) {
-  constexpr int DH = 128, QB = 16 / G, TP = 16 * QB;  // query blocks per head, positions per workgroup
-  constexpr int KR = DH + 8, VR = 16 + 8;            // padded LDS rows (elements)
-  __shared__ uint16_t kl[2][2][16][KR];
-  __shared__ uint16_t vl[2][2][DH][VR];
-  __shared__ int pid_s[kPrefillMaxPages];  // the sequence's page ids
-  const int ntiles = (T + TP - 1) / TP;
-  const int q0 = (ntiles - 1 - (int)blockIdx.x) * TP;  // longest tiles first
-  const int g = blockIdx.y;
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int r = lane & 15, gq = lane >> 4;
-  const int n_kv = kv.n_kv;
-  const int head = g * G + wave % G;
-  const int qw0 = q0 + 16 * (wave / G);    // first position of this wave
-  const int qpos = qw0 + r;                // query position of this lane's column
-  const int qw_last = min(qw0 + 15, T - 1);
-  const int q_last = min(q0 + TP - 1, T - 1);
-  const float scale = kLog2e / sqrtf((float)DH);
-
-  u32x4 qf[4];
-  {
-    // row 0 stands in for positions past the prompt: all loads are issued
-    // unconditionally, then zeroed
-    const bool valid = qpos < T;
-    const float *qp = Q + (size_t)(valid ? qpos : 0) * ldq + head * DH + gq * 8;
-    float4 x[8];
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      x[2 * s] = *(const float4 *)(qp + s * 32);
-      x[2 * s + 1] = *(const float4 *)(qp + s * 32 + 4);
-    }
-    const float z = valid ? 1.f : 0.f;
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      const float4 a = x[2 * s] * z, c = x[2 * s + 1] * z;
-      qf[s] = u32x4{pack2(a.x, a.y), pack2(a.z, a.w), pack2(c.x, c.y), pack2(c.z, c.w)};
-    }
-  }
-  const uint16_t *kbase = (const uint16_t *)kv.k;
-  const uint16_t *vbase = (const uint16_t *)kv.v;
-  const int *ptab = kv.page_table + (size_t)seq * kv.mpps;
-  const int npg = (q_last >> 4) + 1;  // pages holding keys 0..q_last
-  const int npairs = (npg + 1) >> 1;
-  // page ids come from LDS: a page-table load in front of each K/V load
-  // would make every load wait for all loads in flight
-  for (int i = t; i < npg; i += 1024) pid_s[i] = ptab[i];
-  __syncthreads();
-  // this thread's 16-byte piece of a pair: K (threads 0..511) or V (512..1023)
-  const bool is_k = t < 512;
-  const int u = is_k ? t : t - 512;
-  const int pp = u >> 8;  // page of the pair
-  const int k_pos = (u & 255) >> 4, k_d8 = (u & 15) * 8;
-  const int v_dim = (u & 255) >> 1, v_h8 = (u & 1) * 8;
-  auto gload = [&](int p) {  // pair p (a missing second page re-reads the first)
-    const int phys = pid_s[min(2 * p + pp, npg - 1)];
-    return is_k ? *(const u32x4 *)(kbase + (((size_t)phys * n_kv + g) * 16 + k_pos) * DH + k_d8)
-                : *(const u32x4 *)(vbase + (((size_t)phys * n_kv + g) * DH + v_dim) * 16 + v_h8);
-  };
-  // K rows 8..15 hold their 16-byte chunks XOR 4: the score operand reads
-  // rows {0..3, 8..11} (or {4..7, 12..15}) at one chunk, which then fall in
-  // distinct LDS banks
-  auto kchunk = [](int row, int c16) { return (c16 ^ ((row >> 3) << 2)) * 8; };
-  // pair p into LDS buffer buf; value slots at positions >= T (stale cache
-  // slots, or the re-read stand-in for a missing second page) are stored as
-  // zeros, so no wave masks V.  Keys need no such care: a query row only
-  // uses keys at or before its position, which lie in the prompt.
-  auto lstore = [&](int buf, u32x4 v, int p) {
-    if (is_k) {
-      *(u32x4 *)&kl[buf][pp][k_pos][kchunk(k_pos, k_d8 >> 3)] = v;
-    } else {
-      const int kp = (2 * p + pp) * 16 + v_h8;
-      if (kp + 8 > T) v = mask8(v, kp, T);
-      *(u32x4 *)&vl[buf][pp][v_dim][v_h8] = v;
-    }
-  };
-
-  float m_run = -INFINITY, l_run = 0.f;
-  floatx4 acc[8];
-#pragma unroll
-  for (int c = 0; c < 8; ++c) acc[c] = floatx4{0.f, 0.f, 0.f, 0.f};
-  const int kpage = r >> 3, kpos = 8 * ((r >> 2) & 1) + (r & 3);
-  const int vpage = gq >> 1, vpos = 8 * (gq & 1);
-
-  // pairs p+1 .. p+PF in flight in a register ring while pair p is
-  // multiplied from LDS; ring positions are compile-time (rounds of PF)
-  constexpr int PF = 4;
-  u32x4 stg[PF];
-#pragma unroll
-  for (int u = 0; u < PF; ++u) stg[u] = gload(min(u, npairs - 1));
-  lstore(0, stg[0], 0);
-  __syncthreads();
-  auto pair_step = [&](int p, int buf) {
-    const int pg0 = 2 * p;
-    if (pg0 * 16 <= qw_last) {  // some key of the pair at or before this wave's last position
-      u32x4 ka[4], kb[4];
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        ka[s] = *(const u32x4 *)&kl[buf][kpage][kpos][kchunk(kpos, s * 4 + gq)];
-        kb[s] = *(const u32x4 *)&kl[buf][kpage][kpos + 4][kchunk(kpos + 4, s * 4 + gq)];
-      }
-      floatx4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ka[s]),
-                                                     __builtin_bit_cast(bf16x8, qf[s]), s0, 0, 0, 0);
-        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kb[s]),
-                                                     __builtin_bit_cast(bf16x8, qf[s]), s1, 0, 0, 0);
-      }
-      // every key of the pair precedes every query of the wave (uniform
-      // over the wave): no causal mask
-      const bool full = (pg0 + 2) * 16 <= qw0 + 1;
-      // key position of this lane's first score; keys after the query are masked
-      const int kp0 = (pg0 + vpage) * 16 + vpos;
-      float sc[8];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        sc[i] = s0[i];
-        sc[4 + i] = s1[i];
-      }
-      if (!full) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          if (kp0 + i > qpos) sc[i] = -INFINITY;
-          if (kp0 + 4 + i > qpos) sc[4 + i] = -INFINITY;
-        }
-      }
-      float mt = sc[0];
-#pragma unroll
-      for (int i = 1; i < 8; ++i) mt = fmaxf(mt, sc[i]);
-      // scores in base 2: s * scale (scale > 0, so the maximum commutes)
-      const float m_new = fmaxf(m_run, rows4_max(mt) * scale);
-      // a query row with no key yet keeps m = -inf: use 0 as the base
-      const float m_use = m_new == -INFINITY ? 0.f : m_new;
-      float pr[8];
-      float ps = 0.f;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        pr[i] = __builtin_amdgcn_exp2f(fmaf(sc[i], scale, -m_use));
-        ps += pr[i];
-      }
-      if (__any(m_new > m_run)) {
-        const float corr = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
-        l_run *= corr;
-#pragma unroll
-        for (int c = 0; c < 8; ++c) acc[c] = acc[c] * corr;
-      }
-      l_run += ps;
-      m_run = m_new;
-      const u32x4 pf = u32x4{pack2(pr[0], pr[1]), pack2(pr[2], pr[3]), pack2(pr[4], pr[5]), pack2(pr[6], pr[7])};
-      u32x4 vf[8];
-#pragma unroll
-      for (int c = 0; c < 8; ++c) vf[c] = *(const u32x4 *)&vl[buf][vpage][c * 16 + r][vpos];
-#pragma unroll
-      for (int c = 0; c < 8; ++c)
-        acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vf[c]),
-                                                         __builtin_bit_cast(bf16x8, pf), acc[c], 0, 0, 0);
-    }
-  };
-  // Whole rounds, every store and load unconditional: a pair past the last
-  // is skipped by every wave's causal bound, and its stand-in data (the last
-  // pair again, values at positions >= T zeroed) is never read.  Without
-  // conditional paths the wait for a ring slot covers that slot's load only.
-  const int nrounds = (npairs + PF - 1) / PF;
-  for (int p0 = 0; p0 < nrounds * PF; p0 += PF) {
-#pragma unroll
-    for (int u = 0; u < PF; ++u) {
-      const int p = p0 + u;
-      pair_step(p, u & 1);
-      lstore((u + 1) & 1, stg[(u + 1) % PF], p + 1);  // loaded PF - 1 pairs ago
-      stg[u] = gload(min(p + PF, npairs - 1));
-      __syncthreads();
-    }
-  }
-  l_run += __shfl_xor(l_run, 16, 64);
-  l_run += __shfl_xor(l_run, 32, 64);
-  if (qpos < T) {
-    const float inv = 1.f / l_run;
-    uint16_t *o = O + (size_t)qpos * ldo + head * DH;
-#pragma unroll
-    for (int c = 0; c < 8; ++c) {
-      const int dh = c * 16 + 4 * gq;
-      *(u32x2 *)(o + dh) = u32x2{pack2(acc[c][0] * inv, acc[c][1] * inv), pack2(acc[c][2] * inv, acc[c][3] * inv)};
-    }
-  }
-}
-
-// Causal attention over the prompt of one sequence: workgroup per
-// (position t, KV head), keys 0..t in chunks of 256 with an online softmax.
-template <typename T>
-__global__ __launch_bounds__(256) void k_attn_prefill(const float *Q, int ldq, KVRef kv, int seq, int n_q,
-                                                      T *O, int ldo) {
-  constexpr int CH = 256;
-  __shared__ float qs[16][128];
-  __shared__ float sc[16][CH];
-  __shared__ float red[16];
-  const int t = blockIdx.x, g = blockIdx.y;
-  const int n_kv = kv.n_kv, DH = kv.d_h;
-  const int G = n_q / n_kv;
-  const float scale = kLog2e / sqrtf((float)DH);
-  const T *kb = (const T *)kv.k;
-  const T *vb = (const T *)kv.v;
-  const int *ptab = kv.page_table + (size_t)seq * kv.mpps;
-  for (int e = threadIdx.x; e < G * DH; e += blockDim.x)
-    qs[e / DH][e % DH] = Q[(size_t)t * ldq + (g * G + e / DH) * DH + e % DH];
-  float acc[8], mrun[16], lrun[16];
-  for (int k = 0; k < 8; ++k) acc[k] = 0.f;
-  for (int j = 0; j < 16; ++j) { mrun[j] = -INFINITY; lrun[j] = 0.f; }
-  const int nel = G * DH;  // <= 2048: thread owns elements threadIdx.x + 256k
-  for (int c0 = 0; c0 <= t; c0 += CH) {
-    const int nk = min(CH, t + 1 - c0);
-    __syncthreads();
-    if ((int)threadIdx.x < nk) {
-      const int pos = c0 + threadIdx.x;
-      const T *kr = kb + (((size_t)ptab[pos >> 4] * n_kv + g) * 16 + (pos & 15)) * DH;
-      for (int j = 0; j < G; ++j) {
-        float s = 0.f;
-        for (int dh = 0; dh < DH; ++dh) s = fmaf(ld<T>(kr, dh), qs[j][dh], s);
-        sc[j][threadIdx.x] = s * scale;
-      }
-    }
-    __syncthreads();
-    float corr[16];
-    for (int j = 0; j < G; ++j) {
-      float mx = -INFINITY;
-      for (int k = threadIdx.x; k < nk; k += blockDim.x) mx = fmaxf(mx, sc[j][k]);
-      mx = block_max(mx, red);
-      const float mn = fmaxf(mrun[j], mx);
-      corr[j] = exp2f(mrun[j] - mn);
-      float l = 0.f;
-      __syncthreads();
-      for (int k = threadIdx.x; k < nk; k += blockDim.x) {
-        const float pv = exp2f(sc[j][k] - mn);
-        sc[j][k] = pv;
-        l += pv;
-      }
-      l = block_sum(l, red);
-      lrun[j] = lrun[j] * corr[j] + l;
-      mrun[j] = mn;
-    }
-    __syncthreads();
-    for (int k = 0; k < 8; ++k) {
-      const int e = threadIdx.x + 256 * k;
-      if (e >= nel) break;
-      const int j = e / DH, dh = e % DH;
-      float o = acc[k] * corr[j];
-      for (int kk = 0; kk < nk; ++kk) {
-        const int pos = c0 + kk;
-        o = fmaf(sc[j][kk], ld<T>(vb, (((size_t)ptab[pos >> 4] * n_kv + g) * DH + dh) * 16 + (pos & 15)), o);
-      }
-      acc[k] = o;
-    }
-  }
-  for (int k = 0; k < 8; ++k) {
-    const int e = threadIdx.x + 256 * k;
-    if (e >= nel) break;
-    const int j = e / DH, dh = e % DH;
-    st<T>(O, (size_t)t * ldo + (g * G + j) * DH + dh, acc[k] / lrun[j]);
-  }
-}
-
 }  // namespace
 
 hipError_t launch_attn_decode(const AttnArgs &a, hipStream_t st) {
@@ -780,35 +345,6 @@ hipError_t launch_attn_combine(const AttnArgs &a, void *O, int ldo, hipStream_t 
     hipLaunchKernelGGL(k_attn_combine<uint16_t>, grid, dim3(threads), 0, st, a, (uint16_t *)O, ldo);
   else
     hipLaunchKernelGGL(k_attn_combine<float>, grid, dim3(threads), 0, st, a, (float *)O, ldo);
-  return hipGetLastError();
-}
-
-hipError_t launch_attn_prefill(const float *Q, int ldq, int T, KVRef kv, int seq, int n_q, int dtype, void *O,
-                               int ldo, hipStream_t st) {
-  const int G = n_q / kv.n_kv;
-  if (dtype == 1 && kv.d_h == 128 && G >= 1 && G <= 16) {
-    dim3 grid((T + 15) / 16, kv.n_kv);
-    switch ((T + 15) / 16 <= kPrefillMaxPages && ldq % 4 == 0 ? G : 0) {  // K/V shared by 16 waves through LDS when G divides 16
-      case 1: case 2: case 4: case 8: case 16: {
-        const int tp = 256 / G;  // positions per workgroup
-        const dim3 wgrid((T + tp - 1) / tp, kv.n_kv);
-        if (G == 1) hipLaunchKernelGGL(k_attn_prefill_wide<1>, wgrid, dim3(1024), 0, st, Q, ldq, T, kv, seq, n_q, (uint16_t *)O, ldo);
-        else if (G == 2) hipLaunchKernelGGL(k_attn_prefill_wide<2>, wgrid, dim3(1024), 0, st, Q, ldq, T, kv, seq, n_q, (uint16_t *)O, ldo);
-        else if (G == 4) hipLaunchKernelGGL(k_attn_prefill_wide<4>, wgrid, dim3(1024), 0, st, Q, ldq, T, kv, seq, n_q, (uint16_t *)O, ldo);
-        else if (G == 8) hipLaunchKernelGGL(k_attn_prefill_wide<8>, wgrid, dim3(1024), 0, st, Q, ldq, T, kv, seq, n_q, (uint16_t *)O, ldo);
-        else hipLaunchKernelGGL(k_attn_prefill_wide<16>, wgrid, dim3(1024), 0, st, Q, ldq, T, kv, seq, n_q, (uint16_t *)O, ldo);
-        break;
-      }
-      default:
-        hipLaunchKernelGGL(k_attn_prefill_bf16, grid, dim3(64 * G), 0, st, Q, ldq, T, kv, seq, n_q, (uint16_t *)O, ldo);
-    }
-    return hipGetLastError();
-  }
-  dim3 grid(T, kv.n_kv);
-  if (dtype == 1)
-    hipLaunchKernelGGL(k_attn_prefill<uint16_t>, grid, dim3(256), 0, st, Q, ldq, kv, seq, n_q, (uint16_t *)O, ldo);
-  else
-    hipLaunchKernelGGL(k_attn_prefill<float>, grid, dim3(256), 0, st, Q, ldq, kv, seq, n_q, (float *)O, ldo);
   return hipGetLastError();
 }
 

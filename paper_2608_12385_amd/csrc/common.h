@@ -30,6 +30,34 @@ template <typename T> __device__ __forceinline__ void st(T *p, size_t i, float v
 template <> __device__ __forceinline__ void st<float>(float *p, size_t i, float v) { p[i] = v; }
 template <> __device__ __forceinline__ void st<uint16_t>(uint16_t *p, size_t i, float v) { p[i] = f2bf(v); }
 
+constexpr float kLog2e = 1.4426950408889634f;
+
+// Two floats to packed bf16 with the hardware conversion (round to nearest
+// even, the same bits as f2bf for every non-NaN input).
+__device__ __forceinline__ uint32_t pack2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, bf16x2{(__bf16)lo, (__bf16)hi});
+}
+
+// Maximum over lanes l, l^16, l^32 and l^48 (one column of a 16x16 MFMA
+// result held by four 16-lane rows), with the row-swap permutes: no LDS
+// round trip.
+__device__ __forceinline__ float rows4_max(float x) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
+// Zero the bf16 lanes of v (positions first .. first+7) at positions >= nvalid.
+__device__ __forceinline__ u32x4 mask8(u32x4 v, int first, int nvalid) {
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    if (first + 2 * w >= nvalid) v[w] &= 0xffff0000u;
+    if (first + 2 * w + 1 >= nvalid) v[w] &= 0x0000ffffu;
+  }
+  return v;
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);

@@ -484,6 +484,27 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
   float *P = m->at<float>(L.P), *S = m->at<float>(L.S), *Q = m->at<float>(L.Q);
   // prompt-wide rows: no reduction split (plenty of row tiles)
   auto cfg = [&](GemmConfig g) { if (c.prefill) g.S = 1; return g; };
+  // A projection of the active rows: the 256-row tiled kernel over a whole
+  // prompt, the weight-streaming kernel otherwise.
+  auto project = [&](const WSegs &segs, int N, int K, const char *X, int ldx, int rows_M, float *Y, int ldy,
+                     long long y_stride, const GemmConfig &g) -> hipError_t {
+    if (c.prefill && gemm_tile_ok(N, K, rows_M, cf.dtype)) {
+      TileGemm tg{};
+      for (int i = 0; i < 3; ++i) {
+        tg.w[i] = (const uint16_t *)segs.w[i];
+        tg.rows[i] = segs.rows[i];
+      }
+      tg.N = N;
+      tg.K = K;
+      tg.X = (const uint16_t *)X;
+      tg.ldx = ldx;
+      tg.M = rows_M;
+      tg.Y = Y;
+      tg.ldy = ldy;
+      return launch_gemm_tile(tg, false, st);
+    }
+    return launch_gemm(segs, N, K, cf.dtype, X, ldx, rows_M, Y, ldy, y_stride, g, st);
+  };
   const GemmConfig g_qkv = cfg(L.g_qkv), g_o = cfg(L.g_o), g_gu = cfg(L.g_gu), g_d = cfg(L.g_d);
   const int S_qkv = g_qkv.S, S_o = g_o.S, S_gu = g_gu.S, S_d = g_d.S;
   KVRef kvl = kv_layer(kv, l);
@@ -517,8 +538,7 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
   long long stride = (long long)c.rows_layout * nq;
   {
     Timed tm(m, DBT_STAGE_QKV, st);
-    HIPCHK(launch_gemm(qkv, nq, d, cf.dtype, Xn + (size_t)axrow0 * d * es, d, aM, P + (size_t)axrow0 * nq, nq,
-                       stride, g_qkv, st));
+    HIPCHK(project(qkv, nq, d, Xn + (size_t)axrow0 * d * es, d, aM, P + (size_t)axrow0 * nq, nq, stride, g_qkv));
   }
   QKVFinish qf{};
   qf.part = P;
@@ -576,8 +596,7 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
   stride = (long long)c.rows_layout * d;
   {
     Timed tm(m, DBT_STAGE_WO, st);
-    HIPCHK(launch_gemm(wo, d, dq, cf.dtype, O + (size_t)axrow0 * dq * es, dq, aM, P + (size_t)axrow0 * d, d,
-                       stride, g_o, st));
+    HIPCHK(project(wo, d, dq, O + (size_t)axrow0 * dq * es, dq, aM, P + (size_t)axrow0 * d, d, stride, g_o));
   }
   const GatedCopy gca = cm ? GatedCopy{W.g_attn_copy, ret_a, Retain{c.retain ? ret_a : nullptr, c.ret_src, c.ret_dst}}
                            : GatedCopy{};
@@ -588,7 +607,24 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
   // 4. gate/up + SwiGLU + b coupling (fused into the projection's epilogue
   // when the tiles fill the chip)
   const Retain ret_h_keep{c.retain ? ret_h : nullptr, c.ret_src, c.ret_dst};
-  if (gemm_glu_ok(f, M, c.rows.np, cf.dtype)) {
+  if (c.prefill && c.mode == MODE_PRIMARY && c.rows.np == 1 && gemm_tile_ok(f, d, M, cf.dtype)) {
+    TileGemm tg{};
+    tg.w[0] = (const uint16_t *)W.w_gate;
+    tg.w[1] = (const uint16_t *)W.w_up;
+    tg.rows[0] = tg.rows[1] = f;
+    tg.N = f;
+    tg.K = d;
+    tg.X = (const uint16_t *)(Xn + (size_t)xrow0 * d * es);
+    tg.ldx = d;
+    tg.M = M;
+    tg.H = (uint16_t *)(Xh + (size_t)xrow0 * f * es);
+    tg.ldh = f;
+    tg.ret = ret_h_keep.ptr;
+    tg.ret_src = ret_h_keep.src_row;
+    tg.ret_dst = ret_h_keep.dst_row;
+    Timed tm(m, DBT_STAGE_GATEUP, st);
+    HIPCHK(launch_gemm_tile(tg, true, st));
+  } else if (gemm_glu_ok(f, M, c.rows.np, cf.dtype)) {
     const GluEpi ep{c.rows, c.mode, f, W.b, ret_h, ret_h_keep, (uint16_t *)Xh, f};
     Timed tm(m, DBT_STAGE_GATEUP, st);
     HIPCHK(launch_gemm_glu((const uint16_t *)W.w_gate, (const uint16_t *)W.w_up, f, d, Xn + (size_t)xrow0 * d * es,
@@ -610,8 +646,7 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
   stride = (long long)c.rows_layout * d;
   {
     Timed tm(m, DBT_STAGE_DOWN, st);
-    HIPCHK(launch_gemm(wd, d, f, cf.dtype, Xh + (size_t)xrow0 * f * es, f, M, P + (size_t)xrow0 * d, d, stride,
-                       g_d, st));
+    HIPCHK(project(wd, d, f, Xh + (size_t)xrow0 * f * es, f, M, P + (size_t)xrow0 * d, d, stride, g_d));
   }
   const float *g_next = nullptr;
   if (l + 1 < cf.n_layers) g_next = m->layers[l + 1].attn_norm;

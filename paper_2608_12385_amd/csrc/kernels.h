@@ -76,6 +76,28 @@ hipError_t launch_gemm(const WSegs &segs, int N, int K, int dtype, const void *X
 int gemm_stats_tiles(int N, const GemmConfig &g, int dtype);
 int gemm_tile_rows(const GemmConfig &g);  // weight rows (output columns) per workgroup
 
+// Projection of a whole prompt (M >= 256 rows, K a multiple of 64, N a
+// multiple of 16, bf16): 256-row tiles on the matrix cores.  Plain: Y (fp32,
+// [M][ldy]) = X W^T with W the stacked segments w[0..2] (rows[0..2] rows).
+// GLU: w[0] = gate, w[1] = up (N = f rows each); writes H (bf16, [M][ldh]) =
+// silu(X Wg^T) * (X Wu^T), and row ret_src of H in fp32 to ret + ret_dst*N
+// when ret is not NULL (ret_src < 0: every row m to ret + m*N).
+struct TileGemm {
+  const uint16_t *w[3];
+  int rows[3];
+  int N, K;
+  const uint16_t *X;
+  int ldx, M;
+  float *Y;
+  int ldy;
+  uint16_t *H;
+  int ldh;
+  float *ret;
+  int ret_src, ret_dst;
+};
+bool gemm_tile_ok(int N, int K, int M, int dtype);
+hipError_t launch_gemm_tile(const TileGemm &g, bool glu, hipStream_t st);
+
 // ---- row-wise and elementwise stages ----
 struct StepBegin {
   int n_pos, b0;
