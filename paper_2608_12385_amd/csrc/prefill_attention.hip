@@ -8,6 +8,8 @@ namespace dbt {
 
 namespace {
 
+typedef __attribute__((address_space(3))) void lds_void;
+
 // Causal attention over the prompt of one sequence on MFMA (bf16 cache,
 // d_h = 128; Sec. 4.4, prefill through the primary path).  A workgroup owns
 // 16 consecutive query positions and one KV head; wave w is query head
@@ -147,23 +149,30 @@ constexpr int kPrefillMaxPages = 1024;
 // workgroup of 16 waves covers 256/G positions of all G query heads of KV
 // head g: wave w computes head g*G + (w % G) for positions
 // q0 + 16*(w / G) .. +15.  Each pair of K/V pages (32 keys, 16 KB) is loaded
-// once per workgroup, one 16-byte piece per thread, into one of two padded
-// LDS buffers while the previous pair is multiplied, so every key/value is
-// fetched once for 256 query rows.  The per-wave arithmetic is that of the
-// decode kernel (permuted score rows, online softmax in base 2) with a causal
-// mask per query row; a wave skips pairs that start after its last position.
+// once per workgroup straight into LDS (one 1 KB load per wave), two pairs
+// per stage into one of two sets of buffers while the other set is
+// multiplied, so every key/value is fetched once for 256 query rows.  The
+// per-wave arithmetic is that of the decode kernel (permuted score rows,
+// online softmax in base 2) with a causal mask per query row on the pairs
+// that need one; a wave skips pairs that start after its last position.
 // Position tiles are issued longest first.
 template <int G>
 __global__ __launch_bounds__(1024) void k_attn_prefill_wide(const float *Q, int ldq, int T, KVRef kv, int seq,
                                                             int n_q, uint16_t *O, int ldo) {
   constexpr int DH = 128, QB = 16 / G, TP = 16 * QB;  // query blocks per head, positions per workgroup
-  __shared__ uint16_t kl[2][2][16][DH];  // [buffer][page][key][dim], chunks swizzled
-  __shared__ uint16_t vl[2][2][DH][16];  // [buffer][page][dim][position]
+  constexpr int SP = 2;                                // pairs per stage (one barrier per stage)
+  constexpr int PB = 2 * 16 * DH;                      // elements of one pair buffer (two pages)
+  // Two sets of SP pair buffers, separate arrays so that the loads filling
+  // one set are told apart from the reads of the other.  K: [page][key][dim]
+  // with swizzled chunks; V: [page][dim][position].
+  __shared__ __attribute__((aligned(16))) uint16_t kl0[SP * PB], kl1[SP * PB];
+  __shared__ __attribute__((aligned(16))) uint16_t vl0[SP * PB], vl1[SP * PB];
   __shared__ int pid_s[kPrefillMaxPages];  // the sequence's page ids
   const int ntiles = (T + TP - 1) / TP;
   const int q0 = (ntiles - 1 - (int)blockIdx.x) * TP;  // longest tiles first
   const int g = blockIdx.y;
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);  // uniform: per-wave conditions stay scalar branches
   const int r = lane & 15, gq = lane >> 4;
   const int n_kv = kv.n_kv;
   const int head = g * G + wave % G;
@@ -201,35 +210,37 @@ __global__ __launch_bounds__(1024) void k_attn_prefill_wide(const float *Q, int 
   // would make every load wait for all loads in flight
   for (int i = t; i < npg; i += 1024) pid_s[i] = ptab[i];
   __syncthreads();
-  // this thread's 16-byte piece of a pair: K (threads 0..511) or V (512..1023)
-  const bool is_k = t < 512;
-  const int u = is_k ? t : t - 512;
-  const int pp = u >> 8;  // page of the pair
-  const int k_pos = (u & 255) >> 4, k_d8 = (u & 15) * 8;
-  const int v_dim = (u & 255) >> 1, v_h8 = (u & 1) * 8;
-  auto gload = [&](int p) {  // pair p (a missing second page re-reads the first)
-    const int phys = pid_s[min(2 * p + pp, npg - 1)];
-    return is_k ? *(const u32x4 *)(kbase + (((size_t)phys * n_kv + g) * 16 + k_pos) * DH + k_d8)
-                : *(const u32x4 *)(vbase + (((size_t)phys * n_kv + g) * DH + v_dim) * 16 + v_h8);
-  };
+
   // K row j of a page holds its 16-byte chunk c at c ^ 2((j & 3) | ((j >> 3) << 2)):
   // the score operand reads rows {0..3, 8..11} (or {4..7, 12..15}) of both
   // pages at one chunk, which then run at the conflict-free rate (measured on
-  // gfx950; the padded rows used before took 2x as long per read).  V rows
-  // (one dimension, 16 positions, 32 bytes) need neither padding nor swizzle.
-  auto kchunk = [](int row, int c16) { return (c16 ^ (((row & 3) | ((row >> 3) << 2)) << 1)) * 8; };
-  // pair p into LDS buffer buf; value slots at positions >= T (stale cache
-  // slots, or the re-read stand-in for a missing second page) are stored as
-  // zeros, so no wave masks V.  Keys need no such care: a query row only
-  // uses keys at or before its position, which lie in the prompt.
-  auto lstore = [&](int buf, u32x4 v, int p) {
-    if (is_k) {
-      *(u32x4 *)&kl[buf][pp][k_pos][kchunk(k_pos, k_d8 >> 3)] = v;
-    } else {
-      const int kp = (2 * p + pp) * 16 + v_h8;
-      if (kp + 8 > T) v = mask8(v, kp, T);
-      *(u32x4 *)&vl[buf][pp][v_dim][v_h8] = v;
-    }
+  // gfx950).  V rows (one dimension, 16 positions, 32 bytes) need no swizzle.
+  auto kswz = [](int row) { return ((row & 3) | ((row >> 3) << 2)) << 1; };
+  // Loads go straight from global memory into LDS (global_load_lds_dwordx4):
+  // per pair every wave fills 1 KB, lane l the 16 bytes at l * 16 of it.
+  // Waves 0..7: K rows 4 (w & 3) .. + 3 of page w >> 2 (each lane fetches the
+  // chunk the swizzle places in its slot); waves 8..15: V dimensions
+  // 32 ((w - 8) & 3) .. + 31 of page (w - 8) >> 2 (contiguous).
+  const bool ld_k = wave < 8;
+  const int lw = wave & 7, lpp = lw >> 2;
+  uint32_t loff, ldst;  // lane's element offset in the page's head block; wave's offset in a pair buffer
+  if (ld_k) {
+    const int row = 4 * (lw & 3) + (lane >> 4);
+    loff = row * DH + ((lane & 15) ^ kswz(row)) * 8;
+    ldst = (lpp * 16 + 4 * (lw & 3)) * DH;
+  } else {
+    loff = 32 * (lw & 3) * 16 + lane * 8;
+    ldst = (lpp * DH + 32 * (lw & 3)) * 16;
+  }
+  // pair p (a pair past the last, or a missing second page, re-reads the
+  // last page: such data is never used unmasked)
+  auto dma = [&](int p, uint16_t *kb, uint16_t *vb) __attribute__((always_inline)) {
+    const int phys = pid_s[min(2 * min(p, npairs - 1) + lpp, npg - 1)];
+    const size_t blk = ((size_t)phys * n_kv + g) * (16 * DH);  // a page's K or V block of head g
+    if (ld_k)
+      __builtin_amdgcn_global_load_lds((const void *)(kbase + blk + loff), (lds_void *)(kb + ldst), 16, 0, 0);
+    else
+      __builtin_amdgcn_global_load_lds((const void *)(vbase + blk + loff), (lds_void *)(vb + ldst), 16, 0, 0);
   };
 
   float m_run = -INFINITY, l_run = 0.f;
@@ -239,96 +250,121 @@ __global__ __launch_bounds__(1024) void k_attn_prefill_wide(const float *Q, int 
   const int kpage = r >> 3, kpos = 8 * ((r >> 2) & 1) + (r & 3);
   const int vpage = gq >> 1, vpos = 8 * (gq & 1);
 
-  // pairs p+1 .. p+PF in flight in a register ring while pair p is
-  // multiplied from LDS; ring positions are compile-time (rounds of PF)
-  constexpr int PF = 4;
-  u32x4 stg[PF];
+  // Scores of pair p (two MFMA chains over d_h); false when every key of
+  // the pair comes after this wave's last position (uniform over the wave).
+  auto pair_scores = [&](int p, const uint16_t *kb, floatx4 &s0, floatx4 &s1) __attribute__((always_inline)) {
+    if (2 * p * 16 > qw_last) return false;
+    u32x4 ka[4], kc[4];
 #pragma unroll
-  for (int u = 0; u < PF; ++u) stg[u] = gload(min(u, npairs - 1));
-  lstore(0, stg[0], 0);
-  __syncthreads();
-  auto pair_step = [&](int p, int buf) {
+    for (int s = 0; s < 4; ++s) {
+      ka[s] = *(const u32x4 *)&kb[(kpage * 16 + kpos) * DH + ((s * 4 + gq) ^ kswz(kpos)) * 8];
+      kc[s] = *(const u32x4 *)&kb[(kpage * 16 + kpos + 4) * DH + ((s * 4 + gq) ^ kswz(kpos + 4)) * 8];
+    }
+    s0 = floatx4{0.f, 0.f, 0.f, 0.f};
+    s1 = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ka[s]),
+                                                   __builtin_bit_cast(bf16x8, qf[s]), s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kc[s]),
+                                                   __builtin_bit_cast(bf16x8, qf[s]), s1, 0, 0, 0);
+    }
+    return true;
+  };
+  // Online softmax over pair p's scores, then the value MFMAs.
+  auto pair_finish = [&](int p, const uint16_t *vb, const floatx4 &s0, const floatx4 &s1) __attribute__((always_inline)) {
     const int pg0 = 2 * p;
-    if (pg0 * 16 <= qw_last) {  // some key of the pair at or before this wave's last position
-      u32x4 ka[4], kb[4];
+    // value operands first: their LDS reads run under the softmax
+    u32x4 vf[8];
 #pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        ka[s] = *(const u32x4 *)&kl[buf][kpage][kpos][kchunk(kpos, s * 4 + gq)];
-        kb[s] = *(const u32x4 *)&kl[buf][kpage][kpos + 4][kchunk(kpos + 4, s * 4 + gq)];
-      }
-      floatx4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+    for (int c = 0; c < 8; ++c) vf[c] = *(const u32x4 *)&vb[(vpage * DH + c * 16 + r) * 16 + vpos];
+    // every key of the pair precedes every query of the wave (uniform
+    // over the wave): no causal mask
+    const bool full = (pg0 + 2) * 16 <= qw0 + 1;
+    // key position of this lane's first score; keys after the query are masked
+    const int kp0 = (pg0 + vpage) * 16 + vpos;
+    float sc[8];
 #pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ka[s]),
-                                                     __builtin_bit_cast(bf16x8, qf[s]), s0, 0, 0, 0);
-        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kb[s]),
-                                                     __builtin_bit_cast(bf16x8, qf[s]), s1, 0, 0, 0);
-      }
-      // every key of the pair precedes every query of the wave (uniform
-      // over the wave): no causal mask
-      const bool full = (pg0 + 2) * 16 <= qw0 + 1;
-      // key position of this lane's first score; keys after the query are masked
-      const int kp0 = (pg0 + vpage) * 16 + vpos;
-      float sc[8];
+    for (int i = 0; i < 4; ++i) {
+      sc[i] = s0[i];
+      sc[4 + i] = s1[i];
+    }
+    if (!full) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        sc[i] = s0[i];
-        sc[4 + i] = s1[i];
+        if (kp0 + i > qpos) sc[i] = -INFINITY;
+        if (kp0 + 4 + i > qpos) sc[4 + i] = -INFINITY;
       }
-      if (!full) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          if (kp0 + i > qpos) sc[i] = -INFINITY;
-          if (kp0 + 4 + i > qpos) sc[4 + i] = -INFINITY;
-        }
-      }
-      float mt = sc[0];
-#pragma unroll
-      for (int i = 1; i < 8; ++i) mt = fmaxf(mt, sc[i]);
-      // scores in base 2: s * scale (scale > 0, so the maximum commutes)
-      const float m_new = fmaxf(m_run, rows4_max(mt) * scale);
-      // a query row with no key yet keeps m = -inf: use 0 as the base
-      const float m_use = m_new == -INFINITY ? 0.f : m_new;
-      float pr[8];
-      float ps = 0.f;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        pr[i] = __builtin_amdgcn_exp2f(fmaf(sc[i], scale, -m_use));
-        ps += pr[i];
-      }
-      if (__any(m_new > m_run)) {
-        const float corr = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
-        l_run *= corr;
-#pragma unroll
-        for (int c = 0; c < 8; ++c) acc[c] = acc[c] * corr;
-      }
-      l_run += ps;
-      m_run = m_new;
-      const u32x4 pf = u32x4{pack2(pr[0], pr[1]), pack2(pr[2], pr[3]), pack2(pr[4], pr[5]), pack2(pr[6], pr[7])};
-      u32x4 vf[8];
-#pragma unroll
-      for (int c = 0; c < 8; ++c) vf[c] = *(const u32x4 *)&vl[buf][vpage][c * 16 + r][vpos];
-#pragma unroll
-      for (int c = 0; c < 8; ++c)
-        acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vf[c]),
-                                                         __builtin_bit_cast(bf16x8, pf), acc[c], 0, 0, 0);
     }
-  };
-  // Whole rounds, every store and load unconditional: a pair past the last
-  // is skipped by every wave's causal bound, and its stand-in data (the last
-  // pair again, values at positions >= T zeroed) is never read.  Without
-  // conditional paths the wait for a ring slot covers that slot's load only.
-  const int nrounds = (npairs + PF - 1) / PF;
-  for (int p0 = 0; p0 < nrounds * PF; p0 += PF) {
+    float mt = sc[0];
 #pragma unroll
-    for (int u = 0; u < PF; ++u) {
-      const int p = p0 + u;
-      pair_step(p, u & 1);
-      lstore((u + 1) & 1, stg[(u + 1) % PF], p + 1);  // loaded PF - 1 pairs ago
-      stg[u] = gload(min(p + PF, npairs - 1));
+    for (int i = 1; i < 8; ++i) mt = fmaxf(mt, sc[i]);
+    // scores in base 2: s * scale (scale > 0, so the maximum commutes)
+    const float m_new = fmaxf(m_run, rows4_max(mt) * scale);
+    // a query row with no key yet keeps m = -inf: use 0 as the base
+    const float m_use = m_new == -INFINITY ? 0.f : m_new;
+    float pr[8];
+    float ps = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      pr[i] = __builtin_amdgcn_exp2f(fmaf(sc[i], scale, -m_use));
+      ps += pr[i];
+    }
+    if (__any(m_new > m_run)) {
+      const float corr = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
+      l_run *= corr;
+#pragma unroll
+      for (int c = 0; c < 8; ++c) acc[c] = acc[c] * corr;
+    }
+    l_run += ps;
+    m_run = m_new;
+    const u32x4 pf = u32x4{pack2(pr[0], pr[1]), pack2(pr[2], pr[3]), pack2(pr[4], pr[5]), pack2(pr[6], pr[7])};
+    // the last pair of the prompt: value slots at positions >= T (stale
+    // cache slots, a missing second page) are zeroed, since 0 * NaN is NaN
+    if ((pg0 + 2) * 16 > T) {
+#pragma unroll
+      for (int c = 0; c < 8; ++c) vf[c] = mask8(vf[c], kp0, T);
+    }
+#pragma unroll
+    for (int c = 0; c < 8; ++c)
+      acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vf[c]),
+                                                       __builtin_bit_cast(bf16x8, pf), acc[c], 0, 0, 0);
+  };
+  // Both pairs' scores first: the first pair's softmax (VALU) then runs
+  // while the second pair's score MFMAs are in flight, and its value MFMAs
+  // while the second pair's softmax runs.
+  auto stage = [&](int st, const uint16_t *kb, const uint16_t *vb) __attribute__((always_inline)) {
+    static_assert(SP == 2, "two pairs per stage");
+    floatx4 a0, a1, b0, b1;
+    const bool act_a = pair_scores(st * SP, kb, a0, a1);
+    const bool act_b = pair_scores(st * SP + 1, kb + PB, b0, b1);
+    if (act_a) pair_finish(st * SP, vb, a0, a1);
+    if (act_b) pair_finish(st * SP + 1, vb + PB, b0, b1);
+  };
+
+  // Stage st: this wave's loads of stage st are waited for at the barrier
+  // (then the stage is in LDS and every wave has finished stage st - 1),
+  // stage st + 1 is loaded into the set stage st - 1 used, stage st is
+  // multiplied.  The loop runs in pairs of stages so each set is known at
+  // compile time; a stage past the last is loaded but never read.
+  const int nstages = (npairs + SP - 1) / SP;
+#pragma unroll
+  for (int j = 0; j < SP; ++j) dma(j, kl0 + j * PB, vl0 + j * PB);
+  for (int st = 0; st < nstages; st += 2) {
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < SP; ++j) dma((st + 1) * SP + j, kl1 + j * PB, vl1 + j * PB);
+    __builtin_amdgcn_sched_barrier(0);
+    stage(st, kl0, vl0);
+    if (st + 1 < nstages) {  // uniform
       __syncthreads();
+#pragma unroll
+      for (int j = 0; j < SP; ++j) dma((st + 2) * SP + j, kl0 + j * PB, vl0 + j * PB);
+      __builtin_amdgcn_sched_barrier(0);
+      stage(st + 1, kl1, vl1);
     }
   }
+  __syncthreads();  // no load into LDS outlives the workgroup
   l_run += __shfl_xor(l_run, 16, 64);
   l_run += __shfl_xor(l_run, 32, 64);
   if (qpos < T) {
