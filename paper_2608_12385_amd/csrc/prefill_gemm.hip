@@ -232,9 +232,21 @@ static bool tile_args_ok(const TileGemm &g, bool glu) {
 hipError_t launch_gemm_tile(const TileGemm &g, bool glu, hipStream_t st) {
   if (!tile_args_ok(g, glu)) return hipErrorInvalidValue;
   const int mt = (g.M + kTM - 1) / kTM;
+  // One workgroup per compute unit (128 KB of LDS): the wider tile (twice the
+  // multiplies per loaded byte) unless its tile count leaves more of the
+  // last round of workgroups idle than the narrower one's.
+  static int cus = 0;  // compute units of the current device (one device type per process)
+  if (!cus) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus <= 0)
+      cus = 256;
+  }
+  auto fill = [&](long long tiles) { return (double)tiles / (double)(((tiles + cus - 1) / cus) * cus); };
+  const long long t256 = (long long)(g.N / 256) * mt, t128 = (long long)((g.N + 127) / 128) * mt;
   if (glu) {
     hipLaunchKernelGGL((k_gemm_tile<256, true>), dim3((g.N + 127) / 128, mt), dim3(512), 0, st, g);
-  } else if (g.N % 256 == 0 && (long long)(g.N / 256) * mt >= 512) {
+  } else if (g.N % 256 == 0 && fill(t256) >= fill(t128)) {
     hipLaunchKernelGGL((k_gemm_tile<256, false>), dim3(g.N / 256, mt), dim3(512), 0, st, g);
   } else {
     hipLaunchKernelGGL((k_gemm_tile<128, false>), dim3((g.N + 127) / 128, mt), dim3(512), 0, st, g);
