@@ -488,21 +488,19 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
   // prompt, the weight-streaming kernel otherwise.
   auto project = [&](const WSegs &segs, int N, int K, const char *X, int ldx, int rows_M, float *Y, int ldy,
                      long long y_stride, const GemmConfig &g) -> hipError_t {
-    if (c.prefill && gemm_tile_ok(N, K, rows_M, cf.dtype)) {
-      TileGemm tg{};
-      for (int i = 0; i < 3; ++i) {
-        tg.w[i] = (const uint16_t *)segs.w[i];
-        tg.rows[i] = segs.rows[i];
-      }
-      tg.N = N;
-      tg.K = K;
-      tg.X = (const uint16_t *)X;
-      tg.ldx = ldx;
-      tg.M = rows_M;
-      tg.Y = Y;
-      tg.ldy = ldy;
-      return launch_gemm_tile(tg, false, st);
+    TileGemm tg{};
+    for (int i = 0; i < 3; ++i) {
+      tg.w[i] = (const uint16_t *)segs.w[i];
+      tg.rows[i] = segs.rows[i];
     }
+    tg.N = N;
+    tg.K = K;
+    tg.X = (const uint16_t *)X;
+    tg.ldx = ldx;
+    tg.M = rows_M;
+    tg.Y = Y;
+    tg.ldy = ldy;
+    if (c.prefill && cf.dtype == DBT_BF16 && gemm_tile_args_ok(tg, false)) return launch_gemm_tile(tg, false, st);
     return launch_gemm(segs, N, K, cf.dtype, X, ldx, rows_M, Y, ldy, y_stride, g, st);
   };
   const GemmConfig g_qkv = cfg(L.g_qkv), g_o = cfg(L.g_o), g_gu = cfg(L.g_gu), g_d = cfg(L.g_d);
@@ -536,7 +534,32 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
     nq = L.nqkv;
   }
   long long stride = (long long)c.rows_layout * nq;
-  {
+  // A whole prompt: the tiled projection applies the rotary embedding and
+  // writes Q and the cache itself (no fp32 Q/K/V slab, no finish kernel).
+  TileGemm tq{};
+  if (c.prefill && amode == MODE_PRIMARY && cf.dtype == DBT_BF16) {
+    for (int i = 0; i < 3; ++i) {
+      tq.w[i] = (const uint16_t *)qkv.w[i];
+      tq.rows[i] = qkv.rows[i];
+    }
+    tq.N = nq;
+    tq.K = d;
+    tq.X = (const uint16_t *)(Xn + (size_t)axrow0 * d * es);
+    tq.ldx = d;
+    tq.M = aM;
+    tq.rope = m->at<float2>(L.rope);
+    tq.Qout = Q;
+    tq.kv = kvl;
+    tq.seq = c.seq;
+    tq.ret = c.retain && !cm ? ret_q : nullptr;
+    tq.ret_src = c.ret_src;
+    tq.ret_dst = c.ret_dst;
+  }
+  const bool qkv_fused = tq.rope && gemm_tile_args_ok(tq, false);
+  if (qkv_fused) {
+    Timed tm(m, DBT_STAGE_QKV, st);
+    HIPCHK(launch_gemm_tile(tq, false, st));
+  } else {
     Timed tm(m, DBT_STAGE_QKV, st);
     HIPCHK(project(qkv, nq, d, Xn + (size_t)axrow0 * d * es, d, aM, P + (size_t)axrow0 * nq, nq, stride, g_qkv));
   }
@@ -559,7 +582,7 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
   qf.ret = Retain{c.retain && !cm ? ret_q : nullptr, c.ret_src, c.ret_dst};
   qf.kv = kvl;
   qf.dtype = cf.dtype;
-  HIPCHK(launch_qkv_finish(qf, st));
+  if (!qkv_fused) HIPCHK(launch_qkv_finish(qf, st));
 
   // 2. attention over the primary cache
   if (c.prefill) {
@@ -607,8 +630,8 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
   // 4. gate/up + SwiGLU + b coupling (fused into the projection's epilogue
   // when the tiles fill the chip)
   const Retain ret_h_keep{c.retain ? ret_h : nullptr, c.ret_src, c.ret_dst};
-  if (c.prefill && c.mode == MODE_PRIMARY && c.rows.np == 1 && gemm_tile_ok(f, d, M, cf.dtype)) {
-    TileGemm tg{};
+  TileGemm tg{};
+  if (c.prefill && c.mode == MODE_PRIMARY && c.rows.np == 1 && cf.dtype == DBT_BF16) {
     tg.w[0] = (const uint16_t *)W.w_gate;
     tg.w[1] = (const uint16_t *)W.w_up;
     tg.rows[0] = tg.rows[1] = f;
@@ -622,6 +645,8 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
     tg.ret = ret_h_keep.ptr;
     tg.ret_src = ret_h_keep.src_row;
     tg.ret_dst = ret_h_keep.dst_row;
+  }
+  if (tg.w[0] && gemm_tile_args_ok(tg, true)) {
     Timed tm(m, DBT_STAGE_GATEUP, st);
     HIPCHK(launch_gemm_tile(tg, true, st));
   } else if (gemm_glu_ok(f, M, c.rows.np, cf.dtype)) {

@@ -82,6 +82,11 @@ int gemm_tile_rows(const GemmConfig &g);  // weight rows (output columns) per wo
 // GLU: w[0] = gate, w[1] = up (N = f rows each); writes H (bf16, [M][ldh]) =
 // silu(X Wg^T) * (X Wu^T), and row ret_src of H in fp32 to ret + ret_dst*N
 // when ret is not NULL (ret_src < 0: every row m to ret + m*N).
+// QKV (rope != NULL; bf16 cache, d_h 128, rows = positions of sequence seq,
+// w = W_Q, W_K, W_V): the rotary embedding on Q and K, Q (fp32, [M][rows[0]])
+// to Qout and its row ret_src to ret + ret_dst*rows[0] (when ret is not
+// NULL; ret_src < 0: every row m to ret + m*rows[0]), K and V into the cache
+// slots of their positions; no Y.
 struct TileGemm {
   const uint16_t *w[3];
   int rows[3];
@@ -94,8 +99,16 @@ struct TileGemm {
   int ldh;
   float *ret;
   int ret_src, ret_dst;
+  const float2 *rope;  // [max_pos][64] (cos, sin)
+  float *Qout;
+  KVRef kv;
+  int seq;
 };
 bool gemm_tile_ok(int N, int K, int M, int dtype);
+// Everything launch_gemm_tile requires of g (the shape test above, segment
+// sizes multiples of 8 summing to N, row strides multiples of 8, element
+// offsets within 32 bits); callers fall back to launch_gemm otherwise.
+bool gemm_tile_args_ok(const TileGemm &g, bool glu);
 hipError_t launch_gemm_tile(const TileGemm &g, bool glu, hipStream_t st);
 
 // ---- row-wise and elementwise stages ----

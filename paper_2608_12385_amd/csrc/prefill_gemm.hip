@@ -18,11 +18,16 @@
 // rate, where the unswizzled rows take 4x and c ^ ((r & 7) ^ ((r >> 3) & 1))
 // 2x as long per read.
 //
-// GLU: the gate/up projection of the SwiGLU MLP (Eq. (13), primary rows):
-// a tile holds BN/2 gate and the same BN/2 up rows, laid out so each lane
-// holds gate and up values of the same (row, column), and the epilogue writes
-// H = silu(gate) * up in bf16 (and keeps one row in fp32 when asked) instead
-// of the fp32 gate/up outputs.
+// Epilogues (EPI): plain fp32 output; GLU, the gate/up projection of the
+// SwiGLU MLP (Eq. (13), primary rows): a tile holds BN/2 gate and the same
+// BN/2 up rows, laid out so each lane holds gate and up values of the same
+// (row, column), and the epilogue writes H = silu(gate) * up in bf16 (and
+// keeps one row in fp32 when asked) instead of the fp32 gate/up outputs;
+// QKV, the stacked Q/K/V projection of a prompt (Eq. (8), rows = positions):
+// a 128-column tile is one head, laid out so each lane holds dimensions i
+// and i + 64 of it (the rotary pair), and the epilogue applies the rotary
+// embedding to Q and K, writes Q in fp32 (and the kept row) and K and V in
+// the model dtype into the cache pages, instead of the fp32 Q/K/V outputs.
 #include "common.h"
 #include "kernels.h"
 
@@ -36,8 +41,12 @@ __device__ __forceinline__ int swz(int row, int c) { return (c ^ (row & 7)) * 8;
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-template <int BN, bool GLU>
+enum { EPI_PLAIN = 0, EPI_GLU = 1, EPI_QKV = 2 };
+
+template <int BN, int EPI>
 __global__ __launch_bounds__(512) void k_gemm_tile(TileGemm g) {
+  constexpr bool GLU = EPI == EPI_GLU, QKV = EPI == EPI_QKV;
+  static_assert(!QKV || BN == 128, "one head of 128 dimensions per tile");
   constexpr int NA = BN / 32;      // 16-column tiles per wave
   constexpr int WP = BN / 64;      // W row groups (8 rows) loaded per wave per step
   __shared__ __attribute__((aligned(16))) uint16_t xs0[kTM * kTK], xs1[kTM * kTK];
@@ -108,9 +117,10 @@ __global__ __launch_bounds__(512) void k_gemm_tile(TileGemm g) {
       __builtin_amdgcn_global_load_lds((const void *)(wb[i] + (wo[i] + k0)),
                                        (lds_void *)(ws + (8 * (WP * wave_u + i)) * kTK), 16, 0, 0);
   };
-  // W tile row of the wave's column tile a
+  // W tile row of the wave's column tile a (GLU, QKV: tiles a and a + NA/2
+  // are the same columns of the tile's two halves)
   auto wrow = [&](int a) {
-    if (GLU) return a < NA / 2 ? (BN / 4) * wn + 16 * a : BN / 2 + (BN / 4) * wn + 16 * (a - NA / 2);
+    if (GLU || QKV) return a < NA / 2 ? (BN / 4) * wn + 16 * a : BN / 2 + (BN / 4) * wn + 16 * (a - NA / 2);
     return (BN / 2) * wn + 16 * a;
   };
 
@@ -188,7 +198,54 @@ __global__ __launch_bounds__(512) void k_gemm_tile(TileGemm g) {
   for (int b = 0; b < 4; ++b) {
     const int m = m0 + 64 * wm + 16 * b + r;
     if (m >= g.M) continue;
-    if (GLU) {
+    if (QKV) {
+      // tile n0 is Q head n0/128, then K heads, then V heads
+      const int dq = g.rows[0], dkv = g.rows[1];
+      const int pos = m;
+      const size_t page = (size_t)g.kv.page_table[(size_t)g.seq * g.kv.mpps + pos / 16];
+      const int slot = pos % 16;
+#pragma unroll
+      for (int a = 0; a < NA / 2; ++a) {
+        const int d0 = (BN / 4) * wn + 16 * a + 4 * gq;  // dimensions d0 .. d0+3 and d0+64 .. d0+67
+        float x0[4], x1[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          x0[i] = acc[a][b][i];
+          x1[i] = acc[a + NA / 2][b][i];
+        }
+        if (n0 < dq + dkv) {  // uniform over the workgroup: rotary embedding on Q and K
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float2 y = rope_pair(x0[i], x1[i], g.rope[(size_t)pos * 64 + d0 + i]);
+            x0[i] = y.x;
+            x1[i] = y.y;
+          }
+        }
+        if (n0 < dq) {
+          const int c0 = n0 + d0;
+          *(float4 *)(g.Qout + (size_t)m * dq + c0) = float4{x0[0], x0[1], x0[2], x0[3]};
+          *(float4 *)(g.Qout + (size_t)m * dq + c0 + 64) = float4{x1[0], x1[1], x1[2], x1[3]};
+          if (g.ret && (g.ret_src < 0 || m == g.ret_src)) {
+            float *kept = g.ret + (size_t)(g.ret_src < 0 ? m : g.ret_dst) * dq + c0;
+            *(float4 *)kept = float4{x0[0], x0[1], x0[2], x0[3]};
+            *(float4 *)(kept + 64) = float4{x1[0], x1[1], x1[2], x1[3]};
+          }
+        } else if (n0 < dq + dkv) {
+          const int hd = (n0 - dq) / 128;
+          uint16_t *kp = (uint16_t *)g.kv.k + ((page * g.kv.n_kv + hd) * 16 + slot) * 128;
+          *(u32x2 *)(kp + d0) = u32x2{pack2(x0[0], x0[1]), pack2(x0[2], x0[3])};
+          *(u32x2 *)(kp + d0 + 64) = u32x2{pack2(x1[0], x1[1]), pack2(x1[2], x1[3])};
+        } else {
+          const int hd = (n0 - dq - dkv) / 128;
+          uint16_t *vp = (uint16_t *)g.kv.v + (page * g.kv.n_kv + hd) * 128 * 16 + slot;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            vp[(d0 + i) * 16] = f2bf(x0[i]);
+            vp[(d0 + 64 + i) * 16] = f2bf(x1[i]);
+          }
+        }
+      }
+    } else if (GLU) {
       const bool keep = g.ret && (g.ret_src < 0 || m == g.ret_src);
       const int kept_row = g.ret_src < 0 ? m : g.ret_dst;
 #pragma unroll
@@ -222,15 +279,19 @@ bool gemm_tile_ok(int N, int K, int M, int dtype) {
   return dtype == 1 && M >= kTM && K % kTK == 0 && N % 16 == 0;
 }
 
-static bool tile_args_ok(const TileGemm &g, bool glu) {
+bool gemm_tile_args_ok(const TileGemm &g, bool glu) {
   if (!gemm_tile_ok(g.N, g.K, g.M, 1) || g.ldx % 8 != 0) return false;
   if (!glu && (g.rows[0] % 8 != 0 || g.rows[1] % 8 != 0 || g.rows[0] + g.rows[1] + g.rows[2] != g.N)) return false;
+  // the QKV epilogue: heads of 128 dimensions, Q then K then V (as many V as K heads)
+  if (g.rope && (g.kv.d_h != 128 || g.rows[0] % 128 != 0 || g.rows[1] != g.kv.n_kv * 128 || g.rows[2] != g.rows[1] ||
+                 !g.Qout || !g.kv.k || !g.kv.v || !g.kv.page_table))
+    return false;
   // 32-bit element offsets
   return (long long)g.M * g.ldx < (1LL << 32) && (long long)g.N * g.K < (1LL << 32);
 }
 
 hipError_t launch_gemm_tile(const TileGemm &g, bool glu, hipStream_t st) {
-  if (!tile_args_ok(g, glu)) return hipErrorInvalidValue;
+  if (!gemm_tile_args_ok(g, glu)) return hipErrorInvalidValue;
   const int mt = (g.M + kTM - 1) / kTM;
   // One workgroup per compute unit (128 KB of LDS): the wider tile (twice the
   // multiplies per loaded byte) unless its tile count leaves more of the
@@ -245,11 +306,13 @@ hipError_t launch_gemm_tile(const TileGemm &g, bool glu, hipStream_t st) {
   auto fill = [&](long long tiles) { return (double)tiles / (double)(((tiles + cus - 1) / cus) * cus); };
   const long long t256 = (long long)(g.N / 256) * mt, t128 = (long long)((g.N + 127) / 128) * mt;
   if (glu) {
-    hipLaunchKernelGGL((k_gemm_tile<256, true>), dim3((g.N + 127) / 128, mt), dim3(512), 0, st, g);
+    hipLaunchKernelGGL((k_gemm_tile<256, EPI_GLU>), dim3((g.N + 127) / 128, mt), dim3(512), 0, st, g);
+  } else if (g.rope) {
+    hipLaunchKernelGGL((k_gemm_tile<128, EPI_QKV>), dim3(g.N / 128, mt), dim3(512), 0, st, g);
   } else if (g.N % 256 == 0 && fill(t256) >= fill(t128)) {
-    hipLaunchKernelGGL((k_gemm_tile<256, false>), dim3(g.N / 256, mt), dim3(512), 0, st, g);
+    hipLaunchKernelGGL((k_gemm_tile<256, EPI_PLAIN>), dim3(g.N / 256, mt), dim3(512), 0, st, g);
   } else {
-    hipLaunchKernelGGL((k_gemm_tile<128, false>), dim3((g.N + 127) / 128, mt), dim3(512), 0, st, g);
+    hipLaunchKernelGGL((k_gemm_tile<128, EPI_PLAIN>), dim3((g.N + 127) / 128, mt), dim3(512), 0, st, g);
   }
   return hipGetLastError();
 }
