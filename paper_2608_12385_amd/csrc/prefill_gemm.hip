@@ -255,8 +255,11 @@ __global__ __launch_bounds__(512) void k_gemm_tile(TileGemm g) {
         float h[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
+          // silu with the hardware exponential and reciprocal (v_exp_f32,
+          // v_rcp_f32: about 1 ulp each, far below the bf16 rounding of H);
+          // the IEEE-exact forms cost ~20 instructions per value
           const float gt = acc[a][b][i], up = acc[a + NA / 2][b][i];
-          h[i] = gt / (1.0f + expf(-gt)) * up;
+          h[i] = gt * __builtin_amdgcn_rcpf(1.0f + __expf(-gt)) * up;
         }
         *(u32x2 *)(g.H + (size_t)m * g.ldh + j) =
             u32x2{(uint32_t)f2bf(h[0]) | ((uint32_t)f2bf(h[1]) << 16), (uint32_t)f2bf(h[2]) | ((uint32_t)f2bf(h[3]) << 16)};
