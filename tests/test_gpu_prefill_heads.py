@@ -1,0 +1,48 @@
+"""GPU parity of the prefill path (Sec. 4.4: the primary path over the
+prompt writes the cache) for every query-group size its attention kernels
+tell apart.  G = n_q / n_kv = 1, 2 and 8 run the LDS-shared kernel with 16/G
+query blocks per workgroup (G = 4 is covered by test_gpu_parity.py); G = 3,
+which does not divide 16, runs the per-position-block fallback.  Prompts of
+256 or more positions also run the tiled projections (gate/up with the
+SwiGLU epilogue, QKV with the rotary embedding and cache writes in its
+epilogue); shorter ones the weight-streaming projections.  Every cache byte
+is poisoned with 0xFF (bf16 NaN) first, so slots past each prompt hold NaN.
+
+Bars as elsewhere: bf16 2e-2 max relative error per row for both paths'
+logits at the boundary and after one continuation step, alpha within the
+same bar, greedy tokens equal except at certified near-ties.
+"""
+import pytest
+
+import synth
+from oracle import Oracle
+from tests.gpu_util import check_readout, make_session
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+BF16_TOL = 2e-2
+
+
+@pytest.mark.parametrize("n_q,n_kv", [(2, 2), (4, 2), (8, 1), (6, 2)])
+def test_prefill_query_group_sizes(n_q, n_kv):
+    shape = synth.ModelShape(n_layers=1, d_model=256, n_q_heads=n_q, n_kv_heads=n_kv, head_dim=128, d_ff=512,
+                             vocab=512, dtype="bf16", has_embeddings=True, std=0.05, coupling_std=0.5)
+    W = synth.make_weights(shape, seed=1)
+    # 300 and 529 end inside a page pair (the last pair's value mask), 529
+    # one position into its last page; 45 and 17 stay below the tiled
+    # projections' 256 rows
+    lens = [300, 45, 529, 17]
+    prompts = [synth.make_tokens(1, 60 + i, (L,), shape.vocab) for i, L in enumerate(lens)]
+    orc = Oracle(shape, W.values)
+    obs = orc.prefill(prompts, run_boundary=True)
+    sess = make_session(shape, W, max_batch=len(lens), max_pos=540, max_prompt=529)
+    sess.k_pages.fill_(0xFF)
+    sess.v_pages.fill_(0xFF)
+    tag = f"G={n_q // n_kv}"
+    t = sess.prefill(prompts, run_boundary=True)
+    check_readout(t, obs, BF16_TOL, f"boundary {tag}")
+    toks = [o["next"] for o in obs]
+    outs = orc.decode_step(tokens=toks)
+    t = sess.decode(tokens=toks)
+    check_readout(t, outs, BF16_TOL, f"step {tag}")
