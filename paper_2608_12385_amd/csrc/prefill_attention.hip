@@ -143,6 +143,8 @@ __global__ __launch_bounds__(1024) void k_attn_prefill_bf16(const float *Q, int 
 
 // Longest prompt (in 16-position pages) of the LDS-shared prefill kernel.
 constexpr int kPrefillMaxPages = 1024;
+// Growth of a row's score maximum (base 2) that moves its softmax base.
+constexpr float kLazyMargin = 8.f;
 
 // Causal attention over the prompt of one sequence on MFMA, K/V shared
 // through LDS (bf16 cache, d_h = 128, G = n_q/n_kv dividing 16).  A
@@ -300,7 +302,16 @@ __global__ __launch_bounds__(1024) void k_attn_prefill_wide(const float *Q, int 
 #pragma unroll
     for (int i = 1; i < 8; ++i) mt = fmaxf(mt, sc[i]);
     // scores in base 2: s * scale (scale > 0, so the maximum commutes)
-    const float m_new = fmaxf(m_run, rows4_max(mt) * scale);
+    // Lazy rescaling: a row's base m moves only when the pair's maximum
+    // exceeds it by more than kLazyMargin (base 2), so every score seen so
+    // far stays <= m + kLazyMargin, the exponentials stay <= 2^kLazyMargin
+    // and the accumulators are rescaled a few times per row instead of
+    // whenever the maximum grows; output = acc / l with the same base, exact
+    // up to rounding.  A row with no key yet keeps m = -inf (any finite
+    // maximum then moves it).
+    const float mt_s = rows4_max(mt) * scale;
+    const bool grow = mt_s > m_run + kLazyMargin;
+    const float m_new = grow ? mt_s : m_run;
     // a query row with no key yet keeps m = -inf: use 0 as the base
     const float m_use = m_new == -INFINITY ? 0.f : m_new;
     float pr[8];
@@ -310,8 +321,8 @@ __global__ __launch_bounds__(1024) void k_attn_prefill_wide(const float *Q, int 
       pr[i] = __builtin_amdgcn_exp2f(fmaf(sc[i], scale, -m_use));
       ps += pr[i];
     }
-    if (__any(m_new > m_run)) {
-      const float corr = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
+    if (__any(grow)) {
+      const float corr = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);  // 1 where m stayed
       l_run *= corr;
 #pragma unroll
       for (int c = 0; c < 8; ++c) acc[c] = acc[c] * corr;
