@@ -245,7 +245,12 @@ __global__ __launch_bounds__(1024) void k_attn_prefill_wide(const float *Q, int 
       __builtin_amdgcn_global_load_lds((const void *)(vbase + blk + loff), (lds_void *)(vb + ldst), 16, 0, 0);
   };
 
-  float m_run = -INFINITY, l_run = 0.f;
+  float m_run = -INFINITY;
+  // the softmax denominator of each query row: one more value MFMA with V = 1
+  // sums the same bf16 probabilities that weight the values (every row of the
+  // result holds the sum of its column's query)
+  floatx4 acc_l = floatx4{0.f, 0.f, 0.f, 0.f};
+  const u32x4 ones = u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u};
   floatx4 acc[8];
 #pragma unroll
   for (int c = 0; c < 8; ++c) acc[c] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -315,21 +320,18 @@ __global__ __launch_bounds__(1024) void k_attn_prefill_wide(const float *Q, int 
     // a query row with no key yet keeps m = -inf: use 0 as the base
     const float m_use = m_new == -INFINITY ? 0.f : m_new;
     float pr[8];
-    float ps = 0.f;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      pr[i] = __builtin_amdgcn_exp2f(fmaf(sc[i], scale, -m_use));
-      ps += pr[i];
-    }
+    for (int i = 0; i < 8; ++i) pr[i] = __builtin_amdgcn_exp2f(fmaf(sc[i], scale, -m_use));
     if (__any(grow)) {
       const float corr = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);  // 1 where m stayed
-      l_run *= corr;
+      acc_l = acc_l * corr;
 #pragma unroll
       for (int c = 0; c < 8; ++c) acc[c] = acc[c] * corr;
     }
-    l_run += ps;
     m_run = m_new;
     const u32x4 pf = u32x4{pack2(pr[0], pr[1]), pack2(pr[2], pr[3]), pack2(pr[4], pr[5]), pack2(pr[6], pr[7])};
+    acc_l = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ones), __builtin_bit_cast(bf16x8, pf),
+                                                    acc_l, 0, 0, 0);
     // the last pair of the prompt: value slots at positions >= T (stale
     // cache slots, a missing second page) are zeroed, since 0 * NaN is NaN
     if ((pg0 + 2) * 16 > T) {
@@ -376,8 +378,7 @@ __global__ __launch_bounds__(1024) void k_attn_prefill_wide(const float *Q, int 
     }
   }
   __syncthreads();  // no load into LDS outlives the workgroup
-  l_run += __shfl_xor(l_run, 16, 64);
-  l_run += __shfl_xor(l_run, 32, 64);
+  const float l_run = acc_l[0];
   if (qpos < T) {
     const float inv = 1.f / l_run;
     uint16_t *o = O + (size_t)qpos * ldo + head * DH;
