@@ -26,6 +26,9 @@ namespace dbt {
 
 namespace {
 
+// Growth of a row's score maximum (base 2) that moves its softmax base.
+constexpr float kLazyMargin = 8.f;
+
 // Split s of a sequence of npages pages: pages [*pb, *pe); false when the
 // sequence has fewer splits.
 __device__ __forceinline__ bool split_range(int npages, int target, int s, int *pb, int *pe) {
@@ -144,20 +147,25 @@ __global__ __launch_bounds__(NW * 64) void k_attn_decode_bf16(AttnArgs a) {
     float mt = sc[0];
 #pragma unroll
     for (int i = 1; i < 8; ++i) mt = fmaxf(mt, sc[i]);
-    mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
-    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-    const float m_new = fmaxf(m_run, mt);
+    mt = rows4_max(mt);
+    // Lazy rescaling: a row's base m moves only when the pair's maximum
+    // exceeds it by more than kLazyMargin (base 2), so the exponentials stay
+    // <= 2^kLazyMargin and the running sums are rescaled a few times per row
+    // (every pair a wave takes holds a valid position, so m is finite after
+    // its first pair; the wave merge below works for any common base).
+    const bool grow = mt > m_run + kLazyMargin;
+    const float m_new = grow ? mt : m_run;
     float p[8];
     float ps = 0.f;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      p[i] = exp2f(sc[i] - m_new);
+      p[i] = __builtin_amdgcn_exp2f(sc[i] - m_new);
       ps += p[i];
     }
-    // rescale the running sums only when some row's max grew (wave-uniform
-    // test; a factor of exactly 1 otherwise)
-    if (__any(m_new > m_run)) {
-      const float corr = exp2f(m_run - m_new);
+    // rescale the running sums only when some row's base moved (wave-uniform
+    // test; a factor of exactly 1 for the other rows)
+    if (__any(grow)) {
+      const float corr = __builtin_amdgcn_exp2f(m_run - m_new);
       l_run *= corr;
 #pragma unroll
       for (int c = 0; c < 8; ++c) acc[c] = acc[c] * corr;
