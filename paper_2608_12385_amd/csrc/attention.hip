@@ -79,18 +79,26 @@ __global__ __launch_bounds__(NW * 64) void k_attn_decode_bf16(AttnArgs a) {
   };
 
   // Query operand: lane (query r, group gq) holds Q[r][s*32 + gq*8 .. +8].
+  // Rows past the group's queries read row 0 and are zeroed: all eight
+  // loads are issued at once (a load guarded per element compiles to a
+  // branch and a full wait each, 32 round trips before the first page).
   u32x4 qf[4];
   {
     const bool valid = r < nrows;
     const int path = a.rows.p0 + (valid ? r / G : 0);
     const int head = g * G + (valid ? r % G : 0);
     const float *qp = a.Q + (size_t)(path * a.rows.Bp + b) * dq + head * DH + gq * 8;
+    float4 x[8];
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-      float x[8];
+      x[2 * s] = *(const float4 *)(qp + s * 32);
+      x[2 * s + 1] = *(const float4 *)(qp + s * 32 + 4);
+    }
+    const float z = valid ? 1.f : 0.f;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) x[e] = valid ? qp[s * 32 + e] : 0.f;
-      qf[s] = u32x4{pack2(x[0], x[1]), pack2(x[2], x[3]), pack2(x[4], x[5]), pack2(x[6], x[7])};
+    for (int s = 0; s < 4; ++s) {
+      const float4 u = x[2 * s] * z, w = x[2 * s + 1] * z;
+      qf[s] = u32x4{pack2(u.x, u.y), pack2(u.z, u.w), pack2(w.x, w.y), pack2(w.z, w.w)};
     }
   }
 

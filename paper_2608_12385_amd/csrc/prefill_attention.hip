@@ -35,15 +35,20 @@ __global__ __launch_bounds__(1024) void k_attn_prefill_bf16(const float *Q, int 
 
   u32x4 qf[4];
   {
+    // row 0 stands in for positions past the prompt: the loads are
+    // unconditional (all in flight at once), then zeroed
     const bool valid = qpos < T;
     const float *qp = Q + (size_t)(valid ? qpos : 0) * ldq + head * DH + gq * 8;
+    float x[4][8];
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      float x[8];
+    for (int s = 0; s < 4; ++s)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) x[e] = valid ? qp[s * 32 + e] : 0.f;
-      qf[s] = u32x4{pack2(x[0], x[1]), pack2(x[2], x[3]), pack2(x[4], x[5]), pack2(x[6], x[7])};
-    }
+      for (int e = 0; e < 8; ++e) x[s][e] = qp[s * 32 + e];
+    const float z = valid ? 1.f : 0.f;
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+      qf[s] = u32x4{pack2(x[s][0] * z, x[s][1] * z), pack2(x[s][2] * z, x[s][3] * z), pack2(x[s][4] * z, x[s][5] * z),
+                    pack2(x[s][6] * z, x[s][7] * z)};
   }
   const uint16_t *kbase = (const uint16_t *)kv.k;
   const uint16_t *vbase = (const uint16_t *)kv.v;
