@@ -116,16 +116,17 @@ __global__ __launch_bounds__(NW * 64) void k_attn_decode_bf16(AttnArgs a) {
   const int kpage = r >> 3, kpos = 8 * ((r >> 2) & 1) + (r & 3);
   const int vpage = gq >> 1, vpos = 8 * (gq & 1);
   const int npairs = (pe - pb + 1) >> 1;
-  for (int q = wave; q < npairs; q += NW) {
-    const int pg0 = pb + 2 * q;                 // first page of the pair
-    const int last = pe - pb - 1;               // a missing second page re-reads the first (masked)
+  const int last = pe - pb - 1;  // a missing second page re-reads the first (masked)
+  // K/V of pair q into registers (q past the last pair re-reads the last one:
+  // loads stay unconditional, so each wait covers its own pair only)
+  auto load_pair = [&](int q, u32x4 (&ka)[4], u32x4 (&kb)[4], u32x4 (&vf)[8]) __attribute__((always_inline)) {
+    q = min(q, npairs - 1);
     const int phys0 = page_id(2 * q);
     const int phys1 = page_id(min(2 * q + 1, last));
     const int kphys = kpage ? phys1 : phys0;
     const int vphys = vpage ? phys1 : phys0;
     const uint16_t *kp = kbase + ((size_t)kphys * n_kv + g) * 16 * DH + kpos * DH + gq * 8;
     const uint16_t *vp = vbase + ((size_t)vphys * n_kv + g) * DH * 16 + r * 16 + vpos;
-    u32x4 ka[4], kb[4], vf[8];
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
       ka[s] = *(const u32x4 *)(kp + s * 32);
@@ -133,7 +134,9 @@ __global__ __launch_bounds__(NW * 64) void k_attn_decode_bf16(AttnArgs a) {
     }
 #pragma unroll
     for (int c = 0; c < 8; ++c) vf[c] = *(const u32x4 *)(vp + c * 16 * 16);
-
+  };
+  auto pair = [&](int q, const u32x4 (&ka)[4], const u32x4 (&kb)[4], u32x4 (&vf)[8]) __attribute__((always_inline)) {
+    const int pg0 = pb + 2 * q;  // first page of the pair
     floatx4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
@@ -190,6 +193,19 @@ __global__ __launch_bounds__(NW * 64) void k_attn_decode_bf16(AttnArgs a) {
     for (int c = 0; c < 8; ++c)
       acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vf[c]),
                                                        __builtin_bit_cast(bf16x8, pf), acc[c], 0, 0, 0);
+  };
+  // Two register sets: the pair after next loads while this one is multiplied.
+  u32x4 kaA[4], kbA[4], vfA[8], kaB[4], kbB[4], vfB[8];
+  if (wave < npairs) load_pair(wave, kaA, kbA, vfA);
+  // (the scheduling barriers keep each prefetch in front of the multiplies
+  // of the pair already in registers)
+  for (int q = wave; q < npairs; q += 2 * NW) {
+    load_pair(q + NW, kaB, kbB, vfB);
+    __builtin_amdgcn_sched_barrier(0);
+    pair(q, kaA, kbA, vfA);
+    load_pair(q + 2 * NW, kaA, kbA, vfA);
+    __builtin_amdgcn_sched_barrier(0);
+    if (q + NW < npairs) pair(q + NW, kaB, kbB, vfB);  // uniform over the wave
   }
   l_run += __shfl_xor(l_run, 16, 64);
   l_run += __shfl_xor(l_run, 32, 64);
