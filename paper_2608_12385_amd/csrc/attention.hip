@@ -332,10 +332,14 @@ __global__ void k_attn_combine(AttnArgs a, T *O, int ldo) {
   if (e >= nrows * Q4) return;
   const int qr = e / Q4, d4 = e % Q4;
   const size_t base = ((size_t)b * n_kv + g) * a.max_splits;
+  // (unrolled: the loads of eight splits are in flight together; a rolled
+  // loop waits for each split's load before the next)
   float mx = -INFINITY;
+#pragma unroll 8
   for (int s = 0; s < nsplit; ++s) mx = fmaxf(mx, a.ostat[((base + s) * 16 + qr) * 2]);
   float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
   float l = 0.f;
+#pragma unroll 8
   for (int s = 0; s < nsplit; ++s) {
     const size_t ix = (base + s) * 16 + qr;
     const float f = exp2f(a.ostat[ix * 2] - mx);

@@ -173,7 +173,8 @@ __device__ __forceinline__ int moe_entry(const MoeDispatch &a, int q, int &row, 
 // Expert-grouped order as a stable counting sort of the assignments
 // (path, b, slot) by expert, for up to 64 chunks of 64 entries (one
 // workgroup).  A lane's rank among equal experts of its chunk comes from a
-// shuffle loop; per-chunk counts are prefix-summed per expert in chunk order.
+// loop over the wave's lanes (v_readlane broadcasts); per-chunk counts are
+// prefix-summed per expert in chunk order.
 __global__ __launch_bounds__(256) void k_moe_dispatch(MoeDispatch a) {
   constexpr int MAXC = 64;
   __shared__ int ccnt[MAXC][257];
@@ -188,7 +189,7 @@ __global__ __launch_bounds__(256) void k_moe_dispatch(MoeDispatch a) {
     const int e = moe_entry(a, c * 64 + lane, row, j);
     int before = 0, total = 0;
     for (int o = 0; o < 64; ++o) {
-      const int v = __shfl(e, o, 64);
+      const int v = __builtin_amdgcn_readlane(e, o);  // uniform source lane: no LDS round trip
       if (v == e) {
         ++total;
         if (o < lane) ++before;
@@ -224,7 +225,7 @@ __global__ __launch_bounds__(256) void k_moe_dispatch(MoeDispatch a) {
     const int e = moe_entry(a, c * 64 + lane, row, j);
     int before = 0;
     for (int o = 0; o < 64; ++o) {
-      const int v = __shfl(e, o, 64);
+      const int v = __builtin_amdgcn_readlane(e, o);
       if (v == e && o < lane) ++before;
     }
     if (e >= 0) {
@@ -414,17 +415,35 @@ __global__ void k_moe_combine(MoeCombine a) {
     const int k = p == 0 ? a.k1 : a.k2;
     const int r = p == 0 ? r1 : r2;
     if ((p == 0 && prim) || (p == 1 && br)) {
-      int ord[8];
-      for (int j = 0; j < k; ++j) ord[j] = j;
-      for (int j = 1; j < k; ++j)
-        for (int q = j; q > 0 && a.idx[(size_t)r * 8 + ord[q]] < a.idx[(size_t)r * 8 + ord[q - 1]]; --q) {
-          const int tmp = ord[q];
-          ord[q] = ord[q - 1];
-          ord[q - 1] = tmp;
-        }
-      for (int j = 0; j < k; ++j) {
-        sl[p][j] = a.aslot[(size_t)r * 8 + ord[j]];
-        sw[p][j] = a.wts[(size_t)r * 8 + ord[j]];
+      // all eight slots of the row loaded at once (the arrays hold 8 per row),
+      // then an odd-even transposition sort in registers; slots >= k sort last
+      int id[8], sj[8];
+      float wj[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int v = a.idx[(size_t)r * 8 + j];
+        id[j] = j < k ? v : 0x7fffffff;
+        sj[j] = a.aslot[(size_t)r * 8 + j];
+        wj[j] = a.wts[(size_t)r * 8 + j];
+      }
+#pragma unroll
+      for (int round = 0; round < 8; ++round)
+#pragma unroll
+        for (int j = round & 1; j + 1 < 8; j += 2)
+          if (id[j + 1] < id[j]) {
+            const int ti = id[j], ts = sj[j];
+            const float tw = wj[j];
+            id[j] = id[j + 1];
+            sj[j] = sj[j + 1];
+            wj[j] = wj[j + 1];
+            id[j + 1] = ti;
+            sj[j + 1] = ts;
+            wj[j + 1] = tw;
+          }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        sl[p][j] = j < k ? sj[j] : sj[0];  // padding: a valid row with weight 0
+        sw[p][j] = j < k ? wj[j] : 0.f;
       }
     }
   }
@@ -433,9 +452,12 @@ __global__ void k_moe_combine(MoeCombine a) {
   float4 *s2 = (float4 *)(a.S + (size_t)r2 * d);
   const bool keep = a.ret.ptr && (a.ret.src_row < 0 || a.ret.src_row == b);
   float4 *kept = keep ? (float4 *)(a.ret.ptr + (size_t)(a.ret.src_row < 0 ? b : a.ret.dst_row) * d) : nullptr;
-  auto experts = [&](int p, int k, int i) {  // routed experts, ascending id
+  // routed experts, ascending id; all eight slots (weight 0 past k: adding
+  // zeros leaves the sum unchanged) so the loads are in flight together
+  auto experts = [&](int p, int k, int i) {
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int j = 0; j < k; ++j) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
       const float4 y = ((const float4 *)(a.Yexp + (size_t)sl[p][j] * d))[i];
       const float w = sw[p][j];
       acc.x += w * y.x;
@@ -447,6 +469,7 @@ __global__ void k_moe_combine(MoeCombine a) {
   };
   auto shared = [&](int row, int i) {  // shared-expert slabs in split order
     float4 sh = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 4
     for (int q = 0; q < a.S_sh; ++q) {
       const float4 v = ((const float4 *)(a.part + q * a.stride + (size_t)row * d))[i];
       sh.x += v.x;
