@@ -46,3 +46,23 @@ def test_prefill_query_group_sizes(n_q, n_kv):
     outs = orc.decode_step(tokens=toks)
     t = sess.decode(tokens=toks)
     check_readout(t, outs, BF16_TOL, f"step {tag}")
+
+
+def test_prefill_tile_threshold_prompts():
+    """Prompts of 255, 256 and 257 positions: below, at and one past the
+    256-row threshold of the tiled projections (the last also one row into a
+    second row tile), against the oracle at the boundary and one step."""
+    shape = synth.ModelShape(n_layers=2, d_model=256, n_q_heads=8, n_kv_heads=2, head_dim=128, d_ff=512,
+                             vocab=512, dtype="bf16", has_embeddings=True, std=0.05, coupling_std=0.5)
+    W = synth.make_weights(shape, seed=2)
+    lens = [255, 256, 257]
+    prompts = [synth.make_tokens(1, 80 + i, (L,), shape.vocab) for i, L in enumerate(lens)]
+    orc = Oracle(shape, W.values)
+    obs = orc.prefill(prompts, run_boundary=True)
+    sess = make_session(shape, W, max_batch=len(lens), max_pos=270, max_prompt=257)
+    t = sess.prefill(prompts, run_boundary=True)
+    check_readout(t, obs, BF16_TOL, "boundary 255/256/257")
+    toks = [o["next"] for o in obs]
+    outs = orc.decode_step(tokens=toks)
+    t = sess.decode(tokens=toks)
+    check_readout(t, outs, BF16_TOL, "step 255/256/257")
