@@ -355,7 +355,8 @@ def main():
     ap.add_argument("--grouped-only", action="store_true",
                     help="time only the grouped step (counter runs: every dispatch after the calibration "
                          "copies belongs to a grouped step)")
-    ap.add_argument("--only", metavar="WORKLOAD", choices=("layer8b_bf16", "longctx_bf16", "moe_bf16", "full24_bf16"),
+    ap.add_argument("--only", metavar="WORKLOAD", choices=("layer8b_bf16", "longctx_bf16", "moe_bf16", "full24_bf16",
+                                                         "tp8shard_bf16"),
                     help="time only this other workload (one JSON line of its fields)")
     ap.add_argument("--top-k2", type=int, default=4, help="branch fan-out of --only moe_bf16")
     ap.add_argument("--full24-steps", type=int, default=0,

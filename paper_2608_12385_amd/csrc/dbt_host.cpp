@@ -45,8 +45,12 @@ constexpr int kPage = 16;
 // Decode attention reads a sequence of P pages in ceil(P / target) equal
 // splits; 86 pages (1376 positions) keeps the splits long enough to amortise a
 // workgroup's start, and e.g. 4097 positions (257 pages) in three equal splits.
+// A model with few (sequence, KV head) pairs (max_batch x n_kv below 256)
+// takes shorter splits, down to 16 pages, so that its longest caches fill
+// about 512 workgroups.  The target is fixed when the model is created, so a
+// row's result depends only on its own query and cache.
 // The fp32 kernel holds a split's scores in LDS (at most 64 pages).
-constexpr int kSplitTargetBf16 = 86, kSplitTargetF32 = 64;
+constexpr int kSplitTargetBf16 = 86, kSplitMinBf16 = 16, kSplitTargetF32 = 64;
 constexpr int kMixChunk = 4096;
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -58,7 +62,7 @@ int n_branches(const dbt_config &c) { return c.n_branches > 1 ? c.n_branches : 1
 struct Layout {
   int Bp_max = 0, R_max = 0, rows_max = 0, max_in = 0, nqkv = 0, f = 0;
   GemmConfig g_qkv{1, 1, 1}, g_o{1, 1, 1}, g_gu{1, 1, 1}, g_d{1, 1, 1}, g_lm{1, 1, 1};
-  int max_splits = 0, nch = 0, nstat = 0;
+  int split_target = 0, max_splits = 0, nch = 0, nstat = 0;
   bool moe = false;
   int fe = 0, fs = 0, amax = 0;
   GemmConfig g_sgu{1, 1, 1}, g_sd{1, 1, 1};
@@ -137,8 +141,14 @@ Layout make_layout(const dbt_config *c) {
     L.g_sd = gemm_config(d, L.fs, c->dtype, d, L.R_max);
   }
   const int maxpages = (c->max_pos + kPage - 1) / kPage;
-  const int split_target = c->dtype == DBT_BF16 ? kSplitTargetBf16 : kSplitTargetF32;
-  L.max_splits = (maxpages + split_target - 1) / split_target;
+  if (c->dtype == DBT_BF16) {
+    const int pairs = c->max_batch * c->n_kv_heads;
+    const int want = pairs >= 256 ? 1 : (512 + pairs - 1) / pairs;  // splits per pair
+    L.split_target = std::clamp((maxpages + want - 1) / want, kSplitMinBf16, kSplitTargetBf16);
+  } else {
+    L.split_target = kSplitTargetF32;
+  }
+  L.max_splits = (maxpages + L.split_target - 1) / L.split_target;
   L.nch = c->vocab > 0 ? (c->vocab + kMixChunk - 1) / kMixChunk : 0;
   size_t part = std::max({(size_t)L.g_qkv.S * L.R_max * L.nqkv, (size_t)L.g_o.S * L.R_max * d,
                           (size_t)L.g_gu.S * L.R_max * 2 * L.f, (size_t)L.g_d.S * L.R_max * d});
@@ -594,7 +604,7 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
     aa.pos_arr = m->at<int>(L.pos);
     aa.rows = arows;
     aa.n_q = cf.n_q_heads;
-    aa.pages_per_split = cf.dtype == DBT_BF16 ? kSplitTargetBf16 : kSplitTargetF32;
+    aa.pages_per_split = L.split_target;
     aa.max_splits = L.max_splits;
     aa.opart = m->at<float>(L.apart);
     aa.ostat = m->at<float>(L.astat);

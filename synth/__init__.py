@@ -108,7 +108,8 @@ class ModelShape:
         return self.n_experts > 0
 
 
-# The five workloads: shapes and run recipes (one GPU each).
+# The five workloads and one tensor-parallel shard: shapes and run recipes
+# (one GPU each).
 WORKLOADS = {
     "tiny_f32": dict(
         shape=ModelShape(n_layers=2, d_model=256, n_q_heads=4, n_kv_heads=4, head_dim=64,
@@ -128,6 +129,14 @@ WORKLOADS = {
                          n_experts=64, d_ff_expert=1408, n_shared_experts=1, d_ff_shared=1408,
                          top_k1=2, top_k2=4),
         batch=64, cache_len=8192, steps=1),
+    # one GPU's share of the 8B-shape layer under eight-way tensor parallelism
+    # (one KV-head group: 4 query heads and 1 KV head, d_ff / 8, the vocabulary
+    # split eight ways and rounded up to a multiple of 64); run as one GPU's
+    # step, without the exchanges between the shards
+    "tp8shard_bf16": dict(
+        shape=ModelShape(n_layers=1, d_model=4096, n_q_heads=4, n_kv_heads=1, head_dim=128,
+                         d_ff=1792, vocab=16064, dtype="bf16", has_embeddings=False),
+        batch=32, cache_len=4096, steps=1),
     "full24_bf16": dict(
         shape=ModelShape(n_layers=24, d_model=2048, n_q_heads=16, n_kv_heads=4, head_dim=128,
                          d_ff=5632, vocab=32000, dtype="bf16", has_embeddings=True),

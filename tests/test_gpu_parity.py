@@ -134,10 +134,12 @@ def _layer_case(lengths, steps=2, vocab=512, seed_h=2, poison=0):
     return shape, W, orc, sess
 
 
-# The cache is read in splits of 1024 positions: lengths at and around split
-# boundaries, a last split of one page, and (second set) page bytes poisoned
-# with 0xFF (bf16 0xFFFF, a NaN) so slots past each sequence's end hold NaN:
-# they must be masked, not multiplied by a zero probability.
+# Lengths at and around page and power-of-two boundaries, caches of one
+# position and of one position into a new page, caches read in several
+# splits (with few sequences the splits are 16 pages long, so 1041 and 2063
+# positions end inside a split), and (last two sets) page bytes poisoned with
+# 0xFF (bf16 0xFFFF, a NaN) so slots past each sequence's end hold NaN: they
+# must be masked, not multiplied by a zero probability.
 @pytest.mark.parametrize("lengths,poison", [([1, 15, 16, 17, 600], 0), ([511, 512, 513], 0),
                                             ([1023, 1024, 1025, 2063], 0xFF), ([3, 1041, 17], 0xFF)])
 def test_layer_bf16_ragged_cache(lengths, poison):
