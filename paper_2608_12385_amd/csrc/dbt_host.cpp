@@ -1001,9 +1001,9 @@ dbt_status dbt_decode_step(dbt_model *m, dbt_kv *kv, const dbt_step_in *in, int3
   hipStream_t st = (hipStream_t)stream;
   const dbt_config &cf = m->cfg;
   const int B = in->batch, Bp = round16(B);
+  if ((s = ensure_device(m, st))) return s;  // before any state changes
   m->bnd_kv = nullptr;
   std::vector<int> pos = begin_step(kv, B);
-  if ((s = ensure_device(m, st))) return s;
   StepBegin sb;
   if ((s = flush(kv, pos.data(), B, st, &sb))) return s;
   const bool on = branch_on != 0;
@@ -1040,9 +1040,9 @@ dbt_status dbt_decode_step_ungrouped(dbt_model *m, dbt_kv *kv, const dbt_step_in
   hipStream_t st = (hipStream_t)stream;
   const dbt_config &cf = m->cfg;
   const int B = in->batch, Bp = round16(B);
+  if ((s = ensure_device(m, st))) return s;  // before any state changes
   m->bnd_kv = nullptr;
   std::vector<int> pos = begin_step(kv, B);
-  if ((s = ensure_device(m, st))) return s;
   StepBegin sb;
   if ((s = flush(kv, pos.data(), B, st, &sb))) return s;
   // pass 1: every primary layer, keeping Q1, H1, M1
@@ -1090,6 +1090,7 @@ dbt_status dbt_prefill(dbt_model *m, dbt_kv *kv, const int32_t *tokens, const in
   }
   if (need > (int)kv->free_pages.size()) return fail(DBT_ERR_NO_PAGES, "need %d free pages, have %zu", need, kv->free_pages.size());
   hipStream_t st = (hipStream_t)stream;
+  if ((s = ensure_device(m, st))) return s;  // before any state changes
   for (int b = 0; b < batch; ++b) {  // pages for every sequence first, in batch order
     const int np = (h_prompt_lens[b] + kPage - 1) / kPage;
     for (int i = 0; i < np; ++i) {
@@ -1099,7 +1100,6 @@ dbt_status dbt_prefill(dbt_model *m, dbt_kv *kv, const int32_t *tokens, const in
     }
     kv->len[b] = h_prompt_lens[b];
   }
-  if ((s = ensure_device(m, st))) return s;
   if ((s = flush(kv, nullptr, 0, st))) return s;
   const Layout &L = m->L;
   const int d = cf.d_model;

@@ -158,3 +158,52 @@ def test_boundary_without_prefill_is_state_error():
     finally:
         B.dbt_kv_destroy(kv)
         B.dbt_destroy(m)
+
+
+def test_degenerate_calls_rejected_without_state_change():
+    """Empty batches and prompts, a batch above max_batch, a prompt above
+    max_prompt, a step past max_pos, a non-empty sequence given to prefill and
+    an exhausted page pool are rejected with their documented status before
+    any device work, and leave every length and page table as it was."""
+    cfg = _cfg(max_pos=64)
+    w, _keep = _fake_weights(cfg)
+    m = B.dbt_create(cfg, w, FAKE)
+    kv = B.dbt_kv_create(m, FAKE, FAKE, 9, FAKE, 16)   # 9 pages of 16 positions
+    try:
+        B.dbt_kv_reserve(kv, 0, 64)     # at max_pos: 4 pages
+        B.dbt_kv_reserve(kv, 1, 32)     # 2 pages, a step needs a new page
+        B.dbt_kv_reserve(kv, 2, 48)     # 3 pages: the pool is empty
+        state = lambda: [(B.dbt_kv_length(kv, b), B.dbt_kv_pages(kv, b)) for b in range(4)]
+        before = state()
+        out = B.dbt_step_out()
+
+        def status(fn, *a):
+            with pytest.raises(B.DbtError) as e:
+                fn(*a)
+            assert state() == before, fn.__name__
+            return e.value.status
+
+        for batch in (0, -1, 5):
+            sin = B.dbt_step_in(tokens=FAKE, batch=batch)
+            assert status(B.dbt_decode_step, m, kv, sin, 1, out, 0) == 1
+            assert status(B.dbt_decode_step_ungrouped, m, kv, sin, out, 0) == 1
+        assert status(B.dbt_prefill, m, kv, FAKE, [], 0, 1, out, 0) == 1
+        # sequence 0 is at max_pos: no room for another position
+        assert status(B.dbt_decode_step, m, kv, B.dbt_step_in(tokens=FAKE, batch=1), 1, out, 0) == 2
+        # prompts: empty, longer than max_prompt, into a non-empty sequence
+        B.dbt_kv_truncate(kv, 0, 0)
+        before = state()
+        assert status(B.dbt_prefill, m, kv, FAKE, [0], 1, 1, out, 0) == 2
+        assert status(B.dbt_prefill, m, kv, FAKE, [cfg.max_prompt + 1], 1, 1, out, 0) == 2
+        assert status(B.dbt_prefill, m, kv, FAKE, [5, 5], 2, 1, out, 0) == 4
+        # the truncation freed four pages; two more taken leave two free,
+        # while sequences at 16, 32, 48 and 16 positions need four
+        B.dbt_kv_reserve(kv, 3, 16)
+        B.dbt_kv_reserve(kv, 0, 16)
+        before = state()
+        sin = B.dbt_step_in(tokens=FAKE, batch=4)
+        assert status(B.dbt_decode_step, m, kv, sin, 1, out, 0) == 3
+        assert status(B.dbt_decode_step_ungrouped, m, kv, sin, out, 0) == 3
+    finally:
+        B.dbt_kv_destroy(kv)
+        B.dbt_destroy(m)
