@@ -9,7 +9,7 @@ import pytest
 
 import synth
 from oracle import Oracle
-from tests.gpu_util import fill_cache, make_session, row_err
+from tests.gpu_util import check_readout, fill_cache, make_session, row_err
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -215,4 +215,35 @@ def _full_size(k2, compute_matched):
     for key in ("route_w1", "route_w2"):
         wts = _np(t[key])[0]
         np.testing.assert_allclose(wts.sum(axis=1), 1.0, rtol=1e-5)
+    sess.close()
+
+
+@pytest.mark.parametrize("compute_matched", [False, True])
+def test_moe_prefill_boundary_and_steps(compute_matched):
+    """Prompts through a two-layer MoE model with token embeddings: the
+    prefill routes every prompt position on the primary path (Sec. 4.4,
+    step 1; the 600-position prompt has 4800 assignments per layer, more
+    than the chunked dispatch sorts, so its layers take the scanning
+    dispatch), the boundary routes the branch once (step 2), then two
+    grouped steps.  Cache pages are poisoned with NaN first."""
+    shape = _moe_shape(n_layers=2, has_embeddings=True, top_k2=3, compute_matched=compute_matched)
+    W = synth.make_weights(shape, seed=0)
+    if compute_matched:
+        W = _gated(W, shape)
+    lens = [37, 300, 1, 600]
+    prompts = [synth.make_tokens(1, 70 + i, (L,), shape.vocab) for i, L in enumerate(lens)]
+    orc = Oracle(shape, W.values)
+    obs = orc.prefill(prompts, run_boundary=True)
+    sess = make_session(shape, W, max_batch=len(lens), max_pos=610, max_prompt=600)
+    sess.k_pages.fill_(0xFF)
+    sess.v_pages.fill_(0xFF)
+    tag = f"moe prefill cm={compute_matched}"
+    t = sess.prefill(prompts, run_boundary=True)
+    check_readout(t, obs, BF16_TOL, tag + " boundary")
+    toks = [o["next"] for o in obs]
+    for step in range(2):
+        outs = orc.decode_step(tokens=toks)
+        t = sess.decode(tokens=toks)
+        _check_outputs(t, outs, shape, f"{tag} step {step}")
+        toks = [o["next"] for o in outs]
     sess.close()
