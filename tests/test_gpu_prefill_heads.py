@@ -66,3 +66,26 @@ def test_prefill_tile_threshold_prompts():
     outs = orc.decode_step(tokens=toks)
     t = sess.decode(tokens=toks)
     check_readout(t, outs, BF16_TOL, "step 255/256/257")
+
+
+@pytest.mark.slow
+def test_prefill_at_the_shared_kernel_page_limit():
+    """A prompt of 16384 positions (1024 pages: the most the LDS-shared
+    kernel stages) and one of 16385 (the per-position-block kernel), one
+    query head per KV head, against the oracle at the boundary and one step."""
+    shape = synth.ModelShape(n_layers=1, d_model=256, n_q_heads=1, n_kv_heads=1, head_dim=128, d_ff=512,
+                             vocab=512, dtype="bf16", has_embeddings=True, std=0.05, coupling_std=0.5)
+    W = synth.make_weights(shape, seed=3)
+    lens = [16384, 16385]
+    prompts = [synth.make_tokens(1, 90 + i, (L,), shape.vocab) for i, L in enumerate(lens)]
+    orc = Oracle(shape, W.values)
+    obs = orc.prefill(prompts, run_boundary=True)
+    sess = make_session(shape, W, max_batch=2, max_pos=16400, max_prompt=16385)
+    sess.k_pages.fill_(0xFF)
+    sess.v_pages.fill_(0xFF)
+    t = sess.prefill(prompts, run_boundary=True)
+    check_readout(t, obs, BF16_TOL, "boundary 16384/16385")
+    toks = [o["next"] for o in obs]
+    outs = orc.decode_step(tokens=toks)
+    t = sess.decode(tokens=toks)
+    check_readout(t, outs, BF16_TOL, "step 16384/16385")
