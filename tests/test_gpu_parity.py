@@ -154,6 +154,28 @@ def test_layer_bf16_ragged_cache(lengths, poison):
         assert row_err(_np(t["h2_out"]), np.stack([o["h2"] for o in outs])).max() <= BF16_TOL
 
 
+def test_partial_batches_of_a_larger_session():
+    """A session sized for 20 sequences steps its first 5, then all 20, then
+    the first 17 (one row past a 16-row activation tile): the call's batch
+    sets the stacked rows and the launch grids; lengths, page tables and the
+    cache of the sequences a step leaves out stay as they were."""
+    lengths = [1 + 37 * i for i in range(20)]
+    shape, W, orc, sess = _layer_case(lengths, steps=3)
+    for step, B in enumerate((5, 20, 17)):
+        h = synth.make_hidden(shape, B, step=step, seed=2)
+        outs = orc.decode_step(h1=h[0], h2=h[1])
+        t = sess.decode(h1=h[0], h2=h[1])
+        _check_readout(t, outs, BF16_TOL, f"step {step} batch {B}")
+        assert row_err(_np(t["h1_out"]), np.stack([o["h1"] for o in outs])).max() <= BF16_TOL
+        assert row_err(_np(t["h2_out"]), np.stack([o["h2"] for o in outs])).max() <= BF16_TOL
+    from paper_2608_12385_amd import binding
+    for b in range(20):
+        steps_taken = (b < 5) + 1 + (b < 17)
+        assert binding.dbt_kv_length(sess.kv, b) == lengths[b] + steps_taken
+        assert sess_pages(sess, b) == orc.alloc.table[b]
+    sess.close()
+
+
 def test_primary_bitwise_branch_on_off_and_grouped_equals_ungrouped():
     lengths = [3, 40, 530, 16]
     B = len(lengths)
