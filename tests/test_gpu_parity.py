@@ -176,6 +176,35 @@ def test_partial_batches_of_a_larger_session():
     sess.close()
 
 
+def test_step_to_max_pos_then_rejected():
+    """Caches one position short of max_pos (the last page of each table
+    and of the pool about to be taken, or its last slot): the step that fills
+    them matches the oracle; the next is rejected before any work and leaves
+    lengths, page tables and the cache as they were."""
+    lengths = [47, 32, 46]   # max_pos 48: tables of 3 pages
+    shape = _small_bf16(n_layers=1, vocab=512, has_embeddings=False, coupling_std=0.5)
+    W = synth.make_weights(shape, seed=0)
+    orc = Oracle(shape, W.values)
+    sess = make_session(shape, W, max_batch=3, max_pos=48, num_pages=9)
+    fill_cache(sess, orc, shape, lengths)
+    h = synth.make_hidden(shape, 3, step=0, seed=2)
+    outs = orc.decode_step(h1=h[0], h2=h[1])
+    t = sess.decode(h1=h[0], h2=h[1])
+    _check_readout(t, outs, BF16_TOL, "step to max_pos")
+    assert row_err(_np(t["h1_out"]), np.stack([o["h1"] for o in outs])).max() <= BF16_TOL
+    from paper_2608_12385_amd import binding
+    before = [(binding.dbt_kv_length(sess.kv, b), sess_pages(sess, b)) for b in range(3)]
+    assert [n for n, _ in before] == [48, 33, 47]
+    k0, v0 = _np(sess.k_pages).copy(), _np(sess.v_pages).copy()
+    with pytest.raises(binding.DbtError) as e:
+        sess.decode(h1=h[0], h2=h[1])
+    assert e.value.status == 2
+    assert [(binding.dbt_kv_length(sess.kv, b), sess_pages(sess, b)) for b in range(3)] == before
+    np.testing.assert_array_equal(_np(sess.k_pages), k0)
+    np.testing.assert_array_equal(_np(sess.v_pages), v0)
+    sess.close()
+
+
 def test_primary_bitwise_branch_on_off_and_grouped_equals_ungrouped():
     lengths = [3, 40, 530, 16]
     B = len(lengths)
