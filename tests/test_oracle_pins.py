@@ -596,3 +596,94 @@ def test_more_branches_leave_the_primary_and_cache_untouched():
                 for u, v in zip(a, b):
                     np.testing.assert_array_equal(u, v)
 
+
+
+# ----------------------------------------------------------------------------
+# Pins of the routed combine, the MoE coupling and the branch embeddings
+# ----------------------------------------------------------------------------
+
+def _basis_experts(d, gains, ups):
+    """E experts of width 1 whose output is a multiple of a basis vector:
+    Expert_e(U) = silu(g_e . U) (u_e . U) e_e for U = ones(d), with
+    g_e . U = gains[e] and u_e . U = ups[e] (first coordinate carries them)."""
+    E = len(gains)
+    Xg = np.zeros((E, 1, d), np.float32)
+    Xu = np.zeros((E, 1, d), np.float32)
+    Xd = np.zeros((E, d, 1), np.float32)
+    for e in range(E):
+        Xg[e, 0, 0] = gains[e]
+        Xu[e, 0, 1] = ups[e]
+        Xd[e, e, 0] = 1.0
+    return Xg, Xu, Xd
+
+
+def test_routed_combine_pairs_each_weight_with_its_expert():
+    """Sec. 3.2, Eq. (6): the routed output is sum_{e in I} w_e Expert_e(U).
+    Three width-1 experts write multiples of distinct basis vectors, so each
+    coordinate of the combine shows which weight went with which expert.
+    The selection is passed in router order (logit descending), not sorted
+    by expert id, with distinct weights."""
+    shape = tiny_moe_shape(n_experts=3, d_ff_expert=1, top_k1=2, top_k2=2, n_shared_experts=0,
+                           d_ff_shared=0)
+    P = dict(params(shape))
+    gains, ups = [1.0, 2.0, 0.5], [3.0, -1.5, 4.0]
+    P["L0.X_gate"], P["L0.X_up"], P["L0.X_down"] = _basis_experts(shape.d_model, gains, ups)
+    orc = Oracle(shape, P)
+    U = np.ones(shape.d_model)
+    s = [scipy.special.expit(g) * g * u for g, u in zip(gains, ups)]   # silu(g) * u
+    for idx, wts in (([2, 0], [0.7, 0.3]), ([1, 2], [0.125, 0.875]), ([0, 1], [0.6, 0.4])):
+        out = orc._experts(0, U, np.array(idx), np.array(wts))
+        want = np.zeros(shape.d_model)
+        for e, w in zip(idx, wts):
+            want[e] = w * s[e]
+        np.testing.assert_allclose(out, want, rtol=1e-14, atol=1e-15)
+
+
+def test_moe_coupling_closed_form_on_shared_expert():
+    """Reading R10 of the MoE coupling.  With router replay, the same residual
+    input on both paths and a = 0, the branch sees the primary's state up to
+    the MLP and routes to the same experts with the same weights, so R2 = R1
+    and, with b = beta on the shared-expert intermediate and c = gamma on the
+    MoE output, M2 = R1 + (1 + beta) G1 + gamma M1 (Eqs. (13)-(16) with the
+    shared expert in place of the dense MLP)."""
+    beta, gamma = 0.625, -0.25
+    shape = tiny_moe_shape(replay=True, top_k1=2, top_k2=2)
+    P = dict(params(shape))
+    P["L0.a"] = np.zeros_like(P["L0.a"])
+    P["L0.b"] = np.full_like(P["L0.b"], beta)
+    P["L0.c"] = np.full_like(P["L0.c"], gamma)
+    h = synth.make_hidden(shape, 3)
+    orc = Oracle(shape, P)
+    _fill(orc, shape, 3, 10)
+    for b, o in enumerate(orc.decode_step(h1=h[0], h2=h[0])):
+        rec = o["layers"][0]
+        G1, M1 = rec["G1"], rec["M1"]
+        R1 = M1 - G1
+        assert np.max(np.abs(G1)) > 1e-2 and np.max(np.abs(R1)) > 1e-2
+        Sb = h[0, b].astype(np.float64) + rec["A1"]
+        np.testing.assert_allclose(o["h1"], Sb + M1, rtol=1e-13, atol=1e-14)
+        np.testing.assert_allclose(o["h2"], Sb + R1 + (1 + beta) * G1 + gamma * M1, rtol=1e-12, atol=1e-13)
+
+
+@pytest.mark.parametrize("n_branches", [1, 2])
+def test_branch_embeddings_are_the_branch_tables(n_branches):
+    """Sec. 4, Eq. (7) (and App. C.1 for more branches): path j starts from
+    RMSNorm of its own table's row.  With W_O = W_down = 0 and a = b = c = 0
+    every layer passes the residual through unchanged, so after the step the
+    primary holds RMSNorm(E1[x]) and branch j RMSNorm(E_{j+1}[x]); the tables
+    differ, so reading the wrong one shows."""
+    shape = tiny_shape(n_layers=2, n_branches=n_branches)
+    P = dict(params(shape))
+    for l in range(shape.n_layers):
+        for nm in ("W_O", "W_down", "a", "b", "c"):
+            P[f"L{l}.{nm}"] = np.zeros_like(P[f"L{l}.{nm}"])
+    orc = Oracle(shape, P)
+    g = np.asarray(P["g_emb"], np.float64)
+    for tok in (3, 17, 40):
+        o = orc.decode_step(tokens=[tok])[0]
+        tabs = [P[f"E{j + 1}"][tok].astype(np.float64) for j in range(n_branches + 1)]
+        assert min(np.max(np.abs(tabs[0] - t)) for t in tabs[1:]) > 1e-2
+        np.testing.assert_allclose(o["h1"], rmsnorm(tabs[0], g, shape.rms_eps), rtol=1e-13)
+        states = o["hb"] if n_branches > 1 else [o["h2"]]
+        for j, st in enumerate(states):
+            np.testing.assert_allclose(st, rmsnorm(tabs[j + 1], g, shape.rms_eps), rtol=1e-13)
