@@ -140,8 +140,13 @@ typedef struct {
   int32_t batch;
 } dbt_step_in;
 
-/* Outputs of a step; any pointer may be NULL.  Routing arrays are
- * [n_layers][batch][top_k] in the order selected (logit descending). */
+/* Outputs of a step; any pointer may be NULL.  Routing arrays (MoE layers,
+ * continuation steps) are [n_layers][batch][top_k] in the order selected
+ * (logit descending): the selected experts I_i and their renormalised
+ * weights (Sec. 3.2, Eqs. (5)-(6); Eq. (19) with replay).  route_logits1/2
+ * are the float32 router logits r_i = U_i W_r^T the selection was made from,
+ * [n_layers][batch][n_experts] (Sec. 3.2, Eq. (5)), so a caller can check
+ * the selection against its own top-k of the same values. */
 typedef struct {
   float *logits1;           /* [batch][vocab] */
   float *logits2;           /* [n_branches][batch][vocab] */
@@ -151,6 +156,7 @@ typedef struct {
   float *h2_out;            /* [n_branches][batch][d] final branch residual states */
   int32_t *route_idx1, *route_idx2;
   float *route_w1, *route_w2;
+  float *route_logits1, *route_logits2;
 } dbt_step_out;
 
 /* ---- host-only calls (no GPU needed) ---------------------------------- */
@@ -232,7 +238,11 @@ dbt_status dbt_decode_step(dbt_model *m, dbt_kv *kv, const dbt_step_in *in, int3
 
 /* The same step computed in two passes: every primary layer first (keeping
  * Q1, H1, M1 per layer), then every branch layer, so weights and cache pages
- * are read twice.  Results are bit-identical to dbt_decode_step(branch_on=1). */
+ * are read twice.  This is the unshared execution against which Sec. 4.4
+ * ("Decode") and Sec. 4.5 (Eq. (20): decode traffic is weights plus KV
+ * state, read once by the grouped step) measure grouping; it computes the
+ * same definition.  Results are bit-identical to
+ * dbt_decode_step(branch_on=1). */
 dbt_status dbt_decode_step_ungrouped(dbt_model *m, dbt_kv *kv, const dbt_step_in *in,
                                      dbt_step_out *out, dbt_stream stream);
 

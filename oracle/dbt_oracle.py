@@ -485,7 +485,11 @@ class Oracle:
         Z1 = self.logits(np.stack([o["h1"] for o in outs]))
         have2 = [o for o in outs if o["h2"] is not None]
         Z2 = self.logits(np.stack([o["h2"] for o in have2])) if have2 else None
-        j = 0
+        # further branches (App. C.1): branch j of every row in one product
+        many = [o for o in have2 if "hb" in o]
+        Zb = [self.logits(np.stack([o["hb"][j] for o in many]))
+              for j in range(1, len(many[0]["hb"]))] if many else []
+        j = jm = 0
         for i, o in enumerate(outs):
             z1 = Z1[i]
             z2 = None
@@ -494,7 +498,8 @@ class Oracle:
                 z2 = Z2[j]
                 j += 1
                 if "hb" in o:   # more branches: q is the mean branch softmax (App. C.1)
-                    zb = [z2] + [self.logits(h) for h in o["hb"][1:]]
+                    zb = [z2] + [Z[jm] for Z in Zb]
+                    jm += 1
                     o["zb"] = zb
             alpha, m, nxt = mixture_readout(z1, z2, branch_on=z2 is not None, z_branches=zb)
             o.update(z1=z1, z2=z2, alpha=alpha, m=m, next=nxt)

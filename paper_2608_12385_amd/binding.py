@@ -54,7 +54,8 @@ class dbt_step_in(ctypes.Structure):
 
 class dbt_step_out(ctypes.Structure):
     _fields_ = [(n, P) for n in ("logits1", "logits2", "alpha", "next_token", "h1_out", "h2_out",
-                                 "route_idx1", "route_idx2", "route_w1", "route_w2")]
+                                 "route_idx1", "route_idx2", "route_w1", "route_w2",
+                                 "route_logits1", "route_logits2")]
 
 
 _lib = None
@@ -326,6 +327,8 @@ class Session:
             t["route_w1"] = torch.empty(L, batch, s.top_k1, dtype=torch.float32, device=self.device)
             t["route_idx2"] = torch.empty(L, batch, k2, dtype=torch.int32, device=self.device)
             t["route_w2"] = torch.empty(L, batch, k2, dtype=torch.float32, device=self.device)
+            t["route_logits1"] = torch.empty(L, batch, s.n_experts, dtype=torch.float32, device=self.device)
+            t["route_logits2"] = torch.empty(L, batch, s.n_experts, dtype=torch.float32, device=self.device)
         out = dbt_step_out(**{k: v.data_ptr() for k, v in t.items()})
         return out, t
 

@@ -64,6 +64,10 @@ struct Layout {
   GemmConfig g_qkv{1, 1, 1}, g_o{1, 1, 1}, g_gu{1, 1, 1}, g_d{1, 1, 1}, g_lm{1, 1, 1};
   int split_target = 0, max_splits = 0, nch = 0, nstat = 0;
   bool moe = false;
+  // Decode gate/up on the fused SwiGLU kernel: fixed per model (from the
+  // largest stacked call), so every call of a step sums each output element
+  // in the same order whatever paths it carries.
+  bool glu = false;
   int fe = 0, fs = 0, amax = 0;
   GemmConfig g_sgu{1, 1, 1}, g_sd{1, 1, 1};
   size_t moe_idx = 0, moe_logits = 0, moe_w = 0, moe_aslot = 0, moe_counts = 0, moe_offsets = 0, moe_arow = 0, moe_h = 0,
@@ -136,6 +140,7 @@ Layout make_layout(const dbt_config *c) {
   L.g_d = gemm_config(d, L.f, c->dtype, d, L.R_max);
   L.g_lm = gemm_config(std::max(c->vocab, 1), d, c->dtype, std::max(c->vocab, 1), L.R_max);
   L.g_lm.S = 1;  // the logits are written in place (one slab)
+  L.glu = !L.moe && gemm_glu_ok(L.f, L.R_max, 1 + n_branches(*c), c->dtype);
   if (L.moe && L.fs > 0) {
     L.g_sgu = gemm_config(2 * L.fs, d, c->dtype, L.fs, L.R_max);
     L.g_sd = gemm_config(d, L.fs, c->dtype, d, L.R_max);
@@ -380,6 +385,9 @@ dbt_status run_moe_mlp(dbt_model *m, int l, const LayerCall &c, hipStream_t st) 
     ro.out_w1 = c.out->route_w1 ? c.out->route_w1 + (size_t)l * B * cf.top_k1 : nullptr;
     ro.out_idx2 = c.out->route_idx2 ? c.out->route_idx2 + (size_t)l * B * k2 : nullptr;
     ro.out_w2 = c.out->route_w2 ? c.out->route_w2 + (size_t)l * B * k2 : nullptr;
+    const size_t E = cf.n_experts;
+    ro.out_lg1 = c.out->route_logits1 ? c.out->route_logits1 + (size_t)l * B * E : nullptr;
+    ro.out_lg2 = c.out->route_logits2 ? c.out->route_logits2 + (size_t)l * B * E : nullptr;
   }
   ro.ret_idx = c.retain ? ret_idx : nullptr;
   ro.ret_src = c.ret_src;
@@ -659,7 +667,7 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
   if (tg.w[0] && gemm_tile_args_ok(tg, true)) {
     Timed tm(m, DBT_STAGE_GATEUP, st);
     HIPCHK(launch_gemm_tile(tg, true, st));
-  } else if (gemm_glu_ok(f, M, c.rows.np, cf.dtype)) {
+  } else if (c.prefill ? gemm_glu_ok(f, M, c.rows.np, cf.dtype) : L.glu) {
     const GluEpi ep{c.rows, c.mode, f, W.b, ret_h, ret_h_keep, (uint16_t *)Xh, f};
     Timed tm(m, DBT_STAGE_GATEUP, st);
     HIPCHK(launch_gemm_glu((const uint16_t *)W.w_gate, (const uint16_t *)W.w_up, f, d, Xn + (size_t)xrow0 * d * es,

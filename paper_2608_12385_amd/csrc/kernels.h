@@ -235,6 +235,7 @@ struct MoeRoute {
   const int *idx1_in; // branch mode + replay: retained primary selections [*, 8]
   int *out_idx1, *out_idx2;
   float *out_w1, *out_w2;  // caller outputs [B][k] of this layer (may be NULL)
+  float *out_lg1, *out_lg2;  // caller router logits [B][E] of this layer (may be NULL)
   int *ret_idx;       // retained primary selections (may be NULL)
   int ret_src, ret_dst;
 };

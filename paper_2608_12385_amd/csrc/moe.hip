@@ -86,6 +86,8 @@ __global__ __launch_bounds__(256) void k_moe_logits(MoeRoute a) {
     if (lane == 0) {
       if (prim) a.logits[(size_t)prow(a.rows, 0, b) * 256 + e] = s0;
       if (br) a.logits[(size_t)prow(a.rows, 1, b) * 256 + e] = s1;
+      if (prim && a.out_lg1) a.out_lg1[(size_t)b * E + e] = s0;
+      if (br && a.out_lg2) a.out_lg2[(size_t)b * E + e] = s1;
     }
   }
 }

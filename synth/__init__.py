@@ -43,8 +43,11 @@ def bf16_bits(x: np.ndarray) -> np.ndarray:
 
     Finite inputs only (generated data is finite)."""
     u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
-    lsb = (u >> np.uint32(16)) & np.uint32(1)
-    r = (u + np.uint32(0x7FFF) + lsb) >> np.uint32(16)
+    r = u >> np.uint32(16)          # in place from here: (u + 0x7FFF + lsb) >> 16
+    r &= np.uint32(1)
+    r += np.uint32(0x7FFF)
+    r += u
+    r >>= np.uint32(16)
     return r.astype(np.uint16)
 
 

@@ -25,15 +25,10 @@ F32_TOL = 1e-5
 BF16_TOL = 2e-2
 
 
-def _check(t, outs, tol, tag, nb):
-    """Primary logits, alpha and tokens, then every branch's logits."""
-    check_readout(t, outs, tol, tag, branch=False)
-    l2 = to_np(t["logits2"])
-    assert l2.shape[0] == nb, (tag, l2.shape)
-    for j in range(nb):
-        zj = np.stack([o["zb"][j] for o in outs])
-        err = row_err(l2[j], zj)
-        assert err.max() <= tol, (tag, j, err)
+def _check(t, outs, tol, tag, nb, alpha_own_tol=None):
+    """Primary and every branch's logits, alpha and tokens."""
+    assert to_np(t["logits2"]).shape[0] == nb, (tag, to_np(t["logits2"]).shape)
+    check_readout(t, outs, tol, tag, alpha_own_tol=alpha_own_tol)
 
 
 def _check_states(t, outs, tol, tag, nb):
@@ -153,7 +148,7 @@ def test_equal_tables_give_identical_branches():
 # ----------------------------------------------------------------------------
 
 @pytest.mark.slow
-def test_layer8b_three_branches_full_size_sampled():
+def test_layer8b_three_branches_full_size_all_rows():
     w = synth.workload("layer8b_bf16")
     shape = dataclasses.replace(w["shape"], n_branches=3)
     B, L = w["batch"], w["cache_len"]
@@ -164,17 +159,51 @@ def test_layer8b_three_branches_full_size_sampled():
     t = sess.decode(h1=h[0], h2=h[1:])
     t = {k: to_np(v).copy() for k, v in t.items()}
     sess.close()
-    sample = [0, 21, 31]
     orc = Oracle(shape, W.values)
-    for b in sample:
+    for b in range(B):
         (kv_, _), (vv_, _) = synth.make_kv(shape, 0, b, L, seed=3)
         orc.kv_fill(b, L, [kv_], [vv_])
-    outs = [orc.step_one(b, h1=h[0, b], h2=[h[1 + j, b] for j in range(3)], readout=False) for b in sample]
+    outs = [orc.step_one(b, h1=h[0, b], h2=[h[1 + j, b] for j in range(3)], readout=False) for b in range(B)]
     orc._readout(outs)
-    sub = {k: (v[:, sample] if k in ("logits2", "h2_out") else v[sample]) for k, v in t.items()}
-    _check(sub, outs, BF16_TOL, "layer8b three branches", 3)
-    _check_states(sub, outs, BF16_TOL, "layer8b three branches", 3)
-    a = t["alpha"]
-    assert np.all((a >= 0.5) & (a <= 1.0))
-    nt = t["next_token"]
-    assert np.all((nt >= 0) & (nt < shape.vocab))
+    _check(t, outs, BF16_TOL, "layer8b three branches", 3, alpha_own_tol=1e-5)
+    _check_states(t, outs, BF16_TOL, "layer8b three branches", 3)
+
+
+@pytest.mark.slow
+@pytest.mark.timeout(900)
+def test_full_vocab_three_branches_alpha_inside_its_clip():
+    """The benchmark layer's shape with token embeddings, three decode
+    branches and the full 128256-entry vocabulary, final-norm gain 12 so that
+    sum p^2 leaves its clip: prompts through dbt_prefill with the boundary,
+    then two grouped steps.  Alpha takes values inside (0.55, 0.95), at 0.5
+    and near 1; it equals sum p^2 of the GPU's own logits to float32
+    accuracy and the oracle's within the logit-error bound; every branch's
+    logits and state within the bf16 bar; tokens the oracle's or certified
+    near-ties."""
+    w = synth.workload("layer8b_bf16")
+    shape = dataclasses.replace(w["shape"], has_embeddings=True, n_branches=3)
+    W = synth.make_weights(shape, seed=0)
+    print("weights generated", flush=True)
+    W.values["g_final"] = np.full(shape.d_model, 12.0, np.float32)
+    lens = [5, 37, 100, 64]
+    prompts = [synth.make_tokens(1, 80 + i, (L,), shape.vocab) for i, L in enumerate(lens)]
+    orc = Oracle(shape, W.values)
+    obs = orc.prefill(prompts, run_boundary=True)
+    print("oracle prefill done", flush=True)
+    sess = make_session(shape, W, max_batch=len(lens), max_pos=110, max_prompt=100)
+    sess.k_pages.fill_(0xFF)
+    sess.v_pages.fill_(0xFF)
+    t = sess.prefill(prompts, run_boundary=True)
+    _check(t, obs, BF16_TOL, "boundary", 3, alpha_own_tol=1e-5)
+    seen = [o["alpha"] for o in obs]
+    toks = [o["next"] for o in obs]
+    for step in range(2):
+        outs = orc.decode_step(tokens=toks)
+        t = sess.decode(tokens=toks)
+        _check(t, outs, BF16_TOL, f"step {step}", 3, alpha_own_tol=1e-5)
+        _check_states(t, outs, BF16_TOL, f"step {step}", 3)
+        seen += [o["alpha"] for o in outs]
+        toks = [o["next"] for o in outs]
+    seen = np.array(seen)
+    assert np.sum((seen > 0.55) & (seen < 0.95)) >= 4 and np.any(seen == 0.5) and np.any(seen > 0.99), seen
+    sess.close()

@@ -1,14 +1,16 @@
 """GPU parity of the MoE decode layer (Sec. 3.2, Sec. 4.3 router replay,
 Sec. 5 independent fan-outs k1/k2) against the CPU oracle.
 
-Routing indices must match the oracle exactly, except where the oracle's
-own k-th and (k+1)-th router logits are closer than the stated margin
-(then either choice is correct and the rest is checked for validity)."""
+Routing is checked bit-exactly at stage level: the oracle's top-k of the
+GPU's own float32 router logits equals the GPU's selection for every row and
+layer.  Against the oracle run from scratch, selections must match except
+where the oracle's own logits are closer than twice the measured router-logit
+error (a certified near-tie; the rest is then checked for validity)."""
 import numpy as np
 import pytest
 
 import synth
-from oracle import Oracle
+from oracle import Oracle, route
 from tests.gpu_util import check_readout, fill_cache, make_session, row_err
 
 torch = pytest.importorskip("torch")
@@ -29,35 +31,63 @@ def _moe_shape(**kw):
     return synth.ModelShape(**base)
 
 
-def _check_routing(t, outs, shape, tag):
-    """Indices equal the oracle's, or differ only where the oracle's router
-    logits are within the margin that the bf16-level error of the router
-    input allows (then the GPU choice is a valid top-k under that margin).
-    Returns, per path, the rows whose indices equal the oracle's."""
+def _check_stage_routing(t, shape, tag, layers=None):
+    """Stage-level routing (Sec. 3.2, Eqs. (5)-(6); Eq. (19) with replay):
+    the oracle's top-k and renormalised weights applied to the GPU's own
+    float32 router logits give exactly the GPU's selected experts, for every
+    row and layer, and the same weights to float32 accuracy."""
     k2 = shape.top_k1 if shape.replay else shape.top_k2
+    lg1, lg2 = _np(t["route_logits1"]), _np(t["route_logits2"])
+    gi1, gw1 = _np(t["route_idx1"]), _np(t["route_w1"])
+    gi2, gw2 = _np(t["route_idx2"]), _np(t["route_w2"])
+    for l in (range(lg1.shape[0]) if layers is None else layers):
+        for b in range(lg1.shape[1]):
+            oi1, ow1 = route(lg1[l, b].astype(np.float64), shape.top_k1)
+            np.testing.assert_array_equal(gi1[l, b], oi1, err_msg=f"{tag} layer {l} row {b} primary")
+            np.testing.assert_allclose(gw1[l, b], ow1, rtol=1e-5, atol=1e-7, err_msg=tag)
+            rep = gi1[l, b] if shape.replay else None
+            oi2, ow2 = route(lg2[l, b].astype(np.float64), k2, replay_idx=rep)
+            np.testing.assert_array_equal(gi2[l, b], oi2, err_msg=f"{tag} layer {l} row {b} branch")
+            np.testing.assert_allclose(gw2[l, b], ow2, rtol=1e-5, atol=1e-7, err_msg=tag)
+
+
+def _check_routing(t, outs, shape, tag):
+    """End to end against the oracle run from scratch.
+
+    The GPU's router logits lie within the bf16 bar of the oracle's; the
+    selection is checked bit-exactly on the GPU's own logits
+    (_check_stage_routing).  Where the oracle's selection differs, the
+    difference must be certified by the measured logit error e =
+    max |r_gpu - r_oracle| of that row: each of the GPU's experts then sits
+    within 2e of the oracle's logit of the same rank (a smaller gap cannot
+    be resolved at that error).  Returns, per path, the rows whose selection
+    equals the oracle's, and the number of certified near-ties."""
+    k2 = shape.top_k1 if shape.replay else shape.top_k2
+    _check_stage_routing(t, shape, tag)
+    lg1, lg2 = _np(t["route_logits1"])[0], _np(t["route_logits2"])[0]
     gi1, gw1 = _np(t["route_idx1"])[0], _np(t["route_w1"])[0]
     gi2, gw2 = _np(t["route_idx2"])[0], _np(t["route_w2"])[0]
     same = ([], [])
+    ties = 0
     for b, o in enumerate(outs):
         rec = o["layers"][0]
-        for path, (gi, gw, oi, ow, r, k) in enumerate(
-                ((gi1[b], gw1[b], rec["idx1"], rec["w1"], rec["r1"], shape.top_k1),
-                 (gi2[b], gw2[b], rec["idx2"], rec["w2"], rec.get("r2"), k2))):
-            assert len(set(gi.tolist())) == k
+        for path, (gl, gi, gw, oi, ow, r, k) in enumerate(
+                ((lg1[b], gi1[b], gw1[b], rec["idx1"], rec["w1"], rec["r1"], shape.top_k1),
+                 (lg2[b], gi2[b], gw2[b], rec["idx2"], rec["w2"], rec.get("r2"), k2))):
+            r = np.asarray(r, np.float64)
+            assert row_err(gl[None], r[None]).max() <= BF16_TOL, (tag, b, path)
             if np.array_equal(gi, oi):
                 np.testing.assert_allclose(gw, ow, rtol=BF16_TOL, atol=1e-4, err_msg=tag)
                 same[path].append(b)
                 continue
-            r = np.asarray(r)
+            if path == 1 and shape.replay:
+                continue        # follows the primary's selection (checked above)
+            e = float(np.max(np.abs(gl.astype(np.float64) - r)))
             rs = np.sort(r)[::-1]
-            margin = BF16_TOL * np.max(np.abs(r))
             for j in range(k):
-                assert abs(r[gi[j]] - rs[j]) <= margin, (tag, b, j, gi, oi, r[gi[j]], rs[j])
-            if set(gi.tolist()) == set(oi.tolist()):
-                og = dict(zip(oi.tolist(), ow.tolist()))
-                np.testing.assert_allclose(gw, [og[e] for e in gi.tolist()], rtol=BF16_TOL, atol=1e-4)
-                same[path].append(b)
-    return same
+                assert abs(r[gi[j]] - rs[j]) <= 2 * e, (tag, b, j, gi, oi, r[gi[j]], rs[j], e)
+            ties += 1
+    return same, ties
 
 
 def _check_outputs(t, outs, shape, tag, logits=True):
@@ -65,9 +95,9 @@ def _check_outputs(t, outs, shape, tag, logits=True):
     compared on the rows whose expert choice matches the oracle's.  A row
     the GPU routed differently at a certified near-tie takes other experts,
     so its outputs differ legitimately; such rows must stay rare."""
-    same1, same2 = _check_routing(t, outs, shape, tag)
+    (same1, same2), ties = _check_routing(t, outs, shape, tag)
     both = sorted(set(same1) & set(same2))
-    assert len(same1) >= len(outs) - 1 and len(both) >= len(outs) - 1, (tag, same1, same2)
+    assert len(both) >= len(outs) - max(1, len(outs) // 16), (tag, same1, same2, ties)
     h1 = np.stack([o["h1"] for o in outs])
     h2 = np.stack([o["h2"] for o in outs])
     assert row_err(_np(t["h1_out"])[same1], h1[same1]).max() <= BF16_TOL, tag
@@ -77,6 +107,7 @@ def _check_outputs(t, outs, shape, tag, logits=True):
         z2 = np.stack([o["z2"] for o in outs])
         assert row_err(_np(t["logits1"])[same1], z1[same1]).max() <= BF16_TOL, tag
         assert row_err(_np(t["logits2"])[both], z2[both]).max() <= BF16_TOL, tag
+    return ties
 
 
 def _gated(W, shape):
@@ -135,10 +166,10 @@ def test_moe_primary_bitwise_on_off_and_grouped_equals_ungrouped():
         got[mode]["k"] = _np(sess.k_pages).copy()
         sess.close()
     on, off, ug = got["on"], got["off"], got["ungrouped"]
-    for k in ("h1_out", "logits1", "route_idx1", "route_w1", "k"):
+    for k in ("h1_out", "logits1", "route_idx1", "route_w1", "route_logits1", "k"):
         np.testing.assert_array_equal(on[k], off[k], err_msg=k)
     for k in ("h1_out", "h2_out", "logits1", "logits2", "alpha", "next_token", "route_idx1", "route_idx2",
-              "route_w1", "route_w2", "k"):
+              "route_w1", "route_w2", "route_logits1", "route_logits2", "k"):
         np.testing.assert_array_equal(on[k], ug[k], err_msg=k)
 
 
@@ -167,27 +198,39 @@ def test_moe_compute_matched_bitwise_modes():
         got[mode]["k"] = _np(sess.k_pages).copy()
         sess.close()
     on, off, ug = got["on"], got["off"], got["ungrouped"]
-    for k in ("h1_out", "logits1", "route_idx1", "route_w1", "k"):
+    for k in ("h1_out", "logits1", "route_idx1", "route_w1", "route_logits1", "k"):
         np.testing.assert_array_equal(on[k], off[k], err_msg=k)
     for k in ("h1_out", "h2_out", "logits1", "logits2", "alpha", "next_token", "route_idx1", "route_idx2",
-              "route_w1", "route_w2", "k"):
+              "route_w1", "route_w2", "route_logits1", "route_logits2", "k"):
         np.testing.assert_array_equal(on[k], ug[k], err_msg=k)
 
 
+@pytest.fixture(scope="module")
+def moe_kv():
+    """The MoE workload's cache contents (64 sequences x 8192 positions),
+    generated once: (values, bf16 bits) of K and V per sequence."""
+    w = synth.workload("moe_bf16")
+    shape, B, L = w["shape"], w["batch"], w["cache_len"]
+    return [(synth.make_kv(shape, 0, b, L, seed=3)) for b in range(B)]
+
+
 @pytest.mark.slow
+@pytest.mark.timeout(600)
 @pytest.mark.parametrize("k2", [2, 4, 8])
-def test_moe_full_size_sampled(k2):
-    """64 experts x 1408 + shared 1408, d 2048, batch 64, cache 8192."""
-    _full_size(k2, compute_matched=False)
+def test_moe_full_size_all_rows(moe_kv, k2):
+    """64 experts x 1408 + shared 1408, d 2048, batch 64, cache 8192: every
+    sequence against the oracle, routing bit-exact at stage level."""
+    _full_size(moe_kv, k2, compute_matched=False)
 
 
 @pytest.mark.slow
-def test_moe_compute_matched_full_size_sampled():
+@pytest.mark.timeout(600)
+def test_moe_compute_matched_full_size_all_rows(moe_kv):
     """The compute-matched variant at the MoE workload's full size, k1 = k2 = 2."""
-    _full_size(2, compute_matched=True)
+    _full_size(moe_kv, 2, compute_matched=True)
 
 
-def _full_size(k2, compute_matched):
+def _full_size(moe_kv, k2, compute_matched):
     w = synth.workload("moe_bf16")
     shape = synth.ModelShape(**{**w["shape"].__dict__, "top_k2": k2, "compute_matched": compute_matched})
     B, L = w["batch"], w["cache_len"]
@@ -195,23 +238,16 @@ def _full_size(k2, compute_matched):
     if compute_matched:
         W = _gated(W, shape)
     sess = make_session(shape, W, max_batch=B, max_pos=L + 16)
-    fill_cache(sess, None, shape, [L] * B)
+    orc = Oracle(shape, W.values)
+    for b, ((kv_, kb), (vv_, vb)) in enumerate(moe_kv):
+        sess.reserve_fill(b, [kb], [vb])
+        orc.kv_fill(b, L, [kv_], [vv_])
     h = synth.make_hidden(shape, B, step=0, seed=2)
     t = sess.decode(h1=h[0], h2=h[1])
-    sample = [0, 33, 63]
-    orc = Oracle(shape, W.values)
-    for b in sample:
-        (kv_, _), (vv_, _) = synth.make_kv(shape, 0, b, L, seed=3)
-        orc.kv_fill(b, L, [kv_], [vv_])
-    outs = [orc.step_one(b, h1=h[0, b], h2=h[1, b], readout=False) for b in sample]
-    sub = {k: (v[:, sample] if k.startswith("route") else v[sample]) for k, v in t.items()}
-    _check_outputs(sub, outs, shape, f"full k2={k2} compute_matched={compute_matched}", logits=False)
-    # every row: k distinct valid experts, weights positive summing to one
-    for key, k in (("route_idx1", shape.top_k1), ("route_idx2", k2)):
-        idx = _np(t[key])[0]
-        assert idx.shape == (B, k)
-        assert all(len(set(r.tolist())) == k for r in idx)
-        assert np.all((idx >= 0) & (idx < shape.n_experts))
+    print("GPU step done", flush=True)
+    outs = [orc.step_one(b, h1=h[0, b], h2=h[1, b], readout=False) for b in range(B)]
+    ties = _check_outputs(t, outs, shape, f"full k2={k2} compute_matched={compute_matched}", logits=False)
+    print(f"full-size MoE k2={k2} compute_matched={compute_matched}: {ties} certified routing near-ties")
     for key in ("route_w1", "route_w2"):
         wts = _np(t[key])[0]
         np.testing.assert_allclose(wts.sum(axis=1), 1.0, rtol=1e-5)
