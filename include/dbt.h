@@ -246,6 +246,23 @@ dbt_status dbt_decode_step(dbt_model *m, dbt_kv *kv, const dbt_step_in *in, int3
 dbt_status dbt_decode_step_ungrouped(dbt_model *m, dbt_kv *kv, const dbt_step_in *in,
                                      dbt_step_out *out, dbt_stream stream);
 
+/* For callers that cannot allocate device memory while they step (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * dbt_decode_step with the step's buffers (activations, split partials,
+ * logits and their statistics, MoE lists) in a static device array of the
+ * library instead of the model workspace's step region.  It allocates
+ * nothing and calls no allocating routine; results equal
+ * dbt_decode_step's bit for bit.  The array holds DBT_STATIC_SCRATCH_BYTES
+ * on every GPU the library runs on, from load until the process ends; a
+ * model whose step buffers need more (large vocabularies with many
+ * sequences, or models sized for long prompts) gets DBT_ERR_UNSUPPORTED
+ * before anything changes.  Every call on one GPU shares that GPU's array:
+ * calls that overlap on one GPU (other streams, threads or models) race.
+ * The model still needs its workspace for the state kept between calls. */
+#define DBT_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+dbt_status dbt_decode_step_noalloc(dbt_model *m, dbt_kv *kv, const dbt_step_in *in, int32_t branch_on,
+                                   dbt_step_out *out, dbt_stream stream);
+
 /* ---- stage timing -------------------------------------------------------
  * While enabled for a stage, every later device call records a HIP event pair
  * on its stream around the kernel(s) of that stage, once per launch.

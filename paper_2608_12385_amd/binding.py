@@ -77,6 +77,7 @@ _SIGS = {
     "dbt_boundary": (I32, [P, P, I32, ctypes.POINTER(dbt_step_out), P]),
     "dbt_decode_step": (I32, [P, P, ctypes.POINTER(dbt_step_in), I32, ctypes.POINTER(dbt_step_out), P]),
     "dbt_decode_step_ungrouped": (I32, [P, P, ctypes.POINTER(dbt_step_in), ctypes.POINTER(dbt_step_out), P]),
+    "dbt_decode_step_noalloc": (I32, [P, P, ctypes.POINTER(dbt_step_in), I32, ctypes.POINTER(dbt_step_out), P]),
     "dbt_stage_timing": (I32, [P, I32, I32]),
     "dbt_stage_time": (ctypes.c_double, [P, I32, ctypes.POINTER(I32)]),
 }
@@ -185,6 +186,10 @@ def dbt_decode_step(m, kv, step_in, branch_on, out, stream):
 
 def dbt_decode_step_ungrouped(m, kv, step_in, out, stream):
     _check(lib().dbt_decode_step_ungrouped(m, kv, ctypes.byref(step_in), ctypes.byref(out), P(stream)))
+
+
+def dbt_decode_step_noalloc(m, kv, step_in, branch_on, out, stream):
+    _check(lib().dbt_decode_step_noalloc(m, kv, ctypes.byref(step_in), branch_on, ctypes.byref(out), P(stream)))
 
 
 def dbt_stage_timing(m, stage, enable):

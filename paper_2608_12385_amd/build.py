@@ -14,7 +14,8 @@ BUILD = os.path.join(HERE, "_build")
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["dbt_host.cpp", "gemm.hip", "prefill_gemm.hip", "attention.hip", "prefill_attention.hip", "decode_ops.hip", "moe.hip"]
+SOURCES = ["dbt_host.cpp", "gemm.hip", "prefill_gemm.hip", "attention.hip", "prefill_attention.hip", "decode_ops.hip", "moe.hip",
+           "static_scratch.hip"]
 # Packed fp32 vector instructions are disabled for device code.
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall", "-Wno-unused-function",

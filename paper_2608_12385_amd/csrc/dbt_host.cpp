@@ -17,6 +17,7 @@
 #include <vector>
 
 #include "../../include/dbt.h"
+#include "host_internal.h"
 #include "kernels.h"
 
 using namespace dbt;
@@ -74,7 +75,7 @@ struct Layout {
          moe_y = 0, ret_idx = 0;
   size_t rope = 0, pos = 0, S = 0, Xn = 0, Xh = 0, Q = 0, O = 0, P = 0, apart = 0, astat = 0,
          logits = 0, mstats = 0, ret_q = 0, ret_h = 0, ret_m = 0, ret_a = 0, btok = 0, slast = 0,
-         total = 0;
+         state_total = 0, total = 0;  // [0, state_total): state; [state_total, total): step buffers
 };
 
 dbt_status check_config(const dbt_config *c) {
@@ -161,8 +162,23 @@ Layout make_layout(const dbt_config *c) {
   part = std::max(part, (size_t)c->max_prompt * std::max({L.nqkv, d, 2 * L.f}));
   size_t o = 0;
   auto take = [&](size_t bytes) { size_t at = o; o += align256(bytes); return at; };
+  // State kept between calls: the RoPE table, positions, the primary
+  // intermediates retained for a later branch evaluation, the boundary's
+  // token and residual.
   L.rope = take((size_t)c->max_pos * (c->head_dim / 2) * 2 * sizeof(float));
   L.pos = take((size_t)c->max_batch * sizeof(int));
+  L.ret_q = take((size_t)c->n_layers * L.Bp_max * dq * 4);
+  L.ret_h = take((size_t)c->n_layers * L.Bp_max * L.f * 4);
+  L.ret_m = take((size_t)c->n_layers * L.Bp_max * d * 4);
+  L.ret_a = take(c->compute_matched ? (size_t)c->n_layers * L.Bp_max * d * 4 : 0);
+  if (L.moe) L.ret_idx = take((size_t)c->n_layers * L.Bp_max * 8 * 4);
+  L.btok = take((size_t)c->max_batch * 4);
+  L.slast = take((size_t)L.Bp_max * d * 4);
+  // Step buffers: written and read within one call (every element a call
+  // reads is written earlier in the same call, apart from padding rows whose
+  // results are never used), so any memory of this size can hold them.
+  o = align256(o);
+  L.state_total = o;
   L.S = take((size_t)L.rows_max * d * 4);
   L.Xn = take((size_t)L.rows_max * L.max_in * 4);
   L.Xh = take((size_t)L.rows_max * L.f * 4);
@@ -175,10 +191,6 @@ Layout make_layout(const dbt_config *c) {
   L.nstat = gemm_stats_tiles(std::max(c->vocab, 1), L.g_lm, c->dtype);
   if (L.nstat == 0) L.nstat = std::max(L.nch, 1);
   L.mstats = take((size_t)L.R_max * L.nstat * 3 * 4);
-  L.ret_q = take((size_t)c->n_layers * L.Bp_max * dq * 4);
-  L.ret_h = take((size_t)c->n_layers * L.Bp_max * L.f * 4);
-  L.ret_m = take((size_t)c->n_layers * L.Bp_max * d * 4);
-  L.ret_a = take(c->compute_matched ? (size_t)c->n_layers * L.Bp_max * d * 4 : 0);
   if (L.moe) {
     L.amax = L.rows_max * 8;
     L.moe_idx = take((size_t)L.rows_max * 8 * 4);
@@ -190,10 +202,7 @@ Layout make_layout(const dbt_config *c) {
     L.moe_arow = take((size_t)L.amax * 4);
     L.moe_h = take((size_t)L.amax * L.fe * 2);
     L.moe_y = take((size_t)L.amax * d * 4);
-    L.ret_idx = take((size_t)c->n_layers * L.Bp_max * 8 * 4);
   }
-  L.btok = take((size_t)c->max_batch * 4);
-  L.slast = take((size_t)L.Bp_max * d * 4);
   L.total = o;
   return L;
 }
@@ -225,7 +234,11 @@ struct dbt_model {
   // boundary state: set by dbt_prefill(run_boundary = 0)
   const dbt_kv *bnd_kv = nullptr;
   int bnd_batch = 0;
-  template <typename T> T *at(size_t off) const { return (T *)(ws + off); }
+  // Step buffers of the current call: the workspace's own step region, or
+  // memory a call supplies for them (see decode_step_in).
+  char *step = nullptr;
+  char *p(size_t off) const { return off >= L.state_total ? step + (off - L.state_total) : ws + off; }
+  template <typename T> T *at(size_t off) const { return (T *)p(off); }
 };
 
 struct dbt_kv {
@@ -293,7 +306,7 @@ KVRef kv_layer(const dbt_kv *kv, int l) {
 dbt_status ensure_device(dbt_model *m, hipStream_t st) {
   if (m->dev_ready) return DBT_OK;
   HIPCHK(hipMemsetAsync(m->ws, 0, m->L.total, st));
-  HIPCHK(hipMemcpyAsync(m->ws + m->L.rope, m->rope_host.data(), m->rope_host.size() * sizeof(float),
+  HIPCHK(hipMemcpyAsync(m->p(m->L.rope), m->rope_host.data(), m->rope_host.size() * sizeof(float),
                         hipMemcpyHostToDevice, st));
   m->dev_ready = true;
   return DBT_OK;
@@ -408,7 +421,7 @@ dbt_status run_moe_mlp(dbt_model *m, int l, const LayerCall &c, hipStream_t st) 
   {
     Timed tm(m, DBT_STAGE_GATEUP, st);
     MoeGemm g{};
-    g.X = m->ws + L.Xn;
+    g.X = m->p(L.Xn);
     g.ldx = d;
     g.W0 = W.x_gate;
     g.W1 = W.x_up;
@@ -418,14 +431,14 @@ dbt_status run_moe_mlp(dbt_model *m, int l, const LayerCall &c, hipStream_t st) 
     g.counts = di.counts;
     g.offsets = di.offsets;
     g.arow = di.arow;
-    g.Y = m->ws + L.moe_h;
+    g.Y = m->p(L.moe_h);
     g.ldy = L.fe;
     HIPCHK(launch_moe_gemm(g, true, max_rows, st));
   }
   {
     Timed tm(m, DBT_STAGE_DOWN, st);
     MoeGemm g{};
-    g.X = m->ws + L.moe_h;
+    g.X = m->p(L.moe_h);
     g.ldx = L.fe;
     g.W0 = W.x_down;
     g.E = cf.n_experts;
@@ -434,7 +447,7 @@ dbt_status run_moe_mlp(dbt_model *m, int l, const LayerCall &c, hipStream_t st) 
     g.counts = di.counts;
     g.offsets = di.offsets;
     g.arow = di.arow;
-    g.Y = m->ws + L.moe_y;
+    g.Y = m->p(L.moe_y);
     g.ldy = d;
     HIPCHK(launch_moe_gemm(g, false, max_rows, st));
   }
@@ -451,13 +464,13 @@ dbt_status run_moe_mlp(dbt_model *m, int l, const LayerCall &c, hipStream_t st) 
     if (c.prefill) g_sgu.S = g_sd.S = 1;
     WSegs gu{{W.s_gate, W.s_up, nullptr}, {fs, fs, 0}};
     long long st_gu = (long long)c.rows_layout * 2 * fs;
-    HIPCHK(launch_gemm(gu, 2 * fs, d, cf.dtype, m->ws + L.Xn + (size_t)sxrow0 * d * es, d, sM,
+    HIPCHK(launch_gemm(gu, 2 * fs, d, cf.dtype, m->p(L.Xn) + (size_t)sxrow0 * d * es, d, sM,
                        P + (size_t)sxrow0 * 2 * fs, 2 * fs, st_gu, g_sgu, st));
     HIPCHK(launch_swiglu_finish(P, st_gu, g_sgu.S, 2 * fs, fs, smode, srows, W.b, ret_h,
                                 Retain{c.retain && !cm ? ret_h : nullptr, c.ret_src, c.ret_dst}, cf.dtype,
-                                m->ws + L.Xh, fs, st));
+                                m->p(L.Xh), fs, st));
     WSegs sd{{W.s_down, nullptr, nullptr}, {d, 0, 0}};
-    HIPCHK(launch_gemm(sd, d, fs, cf.dtype, m->ws + L.Xh + (size_t)sxrow0 * fs * es, fs, sM, P + (size_t)sxrow0 * d,
+    HIPCHK(launch_gemm(sd, d, fs, cf.dtype, m->p(L.Xh) + (size_t)sxrow0 * fs * es, fs, sM, P + (size_t)sxrow0 * d,
                        d, stride, g_sd, st));
     S_sh = g_sd.S;
   }
@@ -484,7 +497,7 @@ dbt_status run_moe_mlp(dbt_model *m, int l, const LayerCall &c, hipStream_t st) 
   cb.S = S;
   cb.g_next = g_next;
   cb.eps = cf.rms_eps;
-  cb.Xn = m->ws + L.Xn;
+  cb.Xn = m->p(L.Xn);
   cb.ldx = d;
   HIPCHK(launch_moe_combine(cb, cf.dtype, st));
   return DBT_OK;
@@ -498,7 +511,7 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
   const size_t es = esize(cf);
   const int xrow0 = c.rows.p0 * c.rows.Bp;
   const int M = c.rows.np * c.rows.Bp;
-  char *Xn = m->ws + L.Xn, *Xh = m->ws + L.Xh, *O = m->ws + L.O;
+  char *Xn = m->p(L.Xn), *Xh = m->p(L.Xh), *O = m->p(L.O);
   float *P = m->at<float>(L.P), *S = m->at<float>(L.S), *Q = m->at<float>(L.Q);
   // prompt-wide rows: no reduction split (plenty of row tiles)
   auto cfg = [&](GemmConfig g) { if (c.prefill) g.S = 1; return g; };
@@ -709,11 +722,11 @@ dbt_status load_inputs(dbt_model *m, dbt_kv *kv, const dbt_step_in *in, const in
   const float *g0 = m->layers[0].attn_norm;
   if (cf.has_embeddings) {
     HIPCHK(launch_embed(tokens, cf.vocab, m->w.emb1, m->w.emb2, m->w.emb_norm, g0, cf.rms_eps, cf.d_model, cf.dtype, rows,
-                        m->at<float>(L.S), m->ws + L.Xn, cf.d_model, st, sb, m->at<int>(L.pos), kv->page_table,
+                        m->at<float>(L.S), m->p(L.Xn), cf.d_model, st, sb, m->at<int>(L.pos), kv->page_table,
                         kv->mpps));
   } else {
     HIPCHK(launch_load_hidden(in->h1_in, in->h2_in, g0, cf.rms_eps, cf.d_model, cf.dtype, rows, m->at<float>(L.S),
-                              m->ws + L.Xn, cf.d_model, st, sb, m->at<int>(L.pos), kv->page_table, kv->mpps));
+                              m->p(L.Xn), cf.d_model, st, sb, m->at<int>(L.pos), kv->page_table, kv->mpps));
   }
   return DBT_OK;
 }
@@ -726,7 +739,7 @@ dbt_status lm_head(dbt_model *m, Rows rows, hipStream_t st) {
   WSegs lm{{m->w.lm_head, nullptr, nullptr}, {cf.vocab, 0, 0}};
   Timed tm(m, DBT_STAGE_LMHEAD, st);
   const bool fused = gemm_stats_tiles(cf.vocab, L.g_lm, cf.dtype) > 0;
-  HIPCHK(launch_gemm(lm, cf.vocab, cf.d_model, cf.dtype, m->ws + L.Xn + (size_t)xrow0 * cf.d_model * esize(cf),
+  HIPCHK(launch_gemm(lm, cf.vocab, cf.d_model, cf.dtype, m->p(L.Xn) + (size_t)xrow0 * cf.d_model * esize(cf),
                      cf.d_model, rows.np * rows.Bp, m->at<float>(L.logits) + (size_t)xrow0 * cf.vocab, cf.vocab,
                      0, L.g_lm, st, fused ? m->at<float>(L.mstats) + (size_t)xrow0 * L.nstat * 3 : nullptr));
   return DBT_OK;
@@ -840,6 +853,45 @@ dbt_status branch_pass(dbt_model *m, dbt_kv *kv, int B, int Bp, hipStream_t st, 
   return DBT_OK;
 }
 
+dbt_status decode_step_impl(dbt_model *m, dbt_kv *kv, const dbt_step_in *in, int32_t branch_on, dbt_step_out *out,
+                            dbt_stream stream) {
+  dbt_status s = check_model_kv(m, kv);
+  if (s) return s;
+  s = check_step_in(m, kv, in, branch_on);
+  if (s) return s;
+  hipStream_t st = (hipStream_t)stream;
+  const dbt_config &cf = m->cfg;
+  const int B = in->batch, Bp = round16(B);
+  if ((s = ensure_device(m, st))) return s;  // before any state changes
+  m->bnd_kv = nullptr;
+  std::vector<int> pos = begin_step(kv, B);
+  StepBegin sb;
+  if ((s = flush(kv, pos.data(), B, st, &sb))) return s;
+  const bool on = branch_on != 0;
+  const int nb = n_branches(cf);
+  const Rows rows{B, Bp, 0, on ? 1 + nb : 1};
+  if ((s = load_inputs(m, kv, in, in->tokens, rows, st, &sb))) return s;
+  LayerCall lc{};
+  lc.rows = rows;
+  lc.mode = on ? MODE_GROUPED : MODE_PRIMARY;
+  lc.retain = false;
+  lc.ret_src = -1;
+  lc.prefill = false;
+  lc.rows_layout = (1 + nb) * Bp;
+  lc.last_norm = true;
+  lc.out = out;
+  for (int l = 0; l < cf.n_layers; ++l)
+    if ((s = run_layer(m, kv, l, lc, st))) return s;
+  if (cf.vocab > 0 && (s = lm_head(m, rows, st))) return s;
+  for (int b = 0; b < B; ++b) kv->len[b] += 1;
+  if (out) {
+    if ((s = readout(m, B, Bp, on, out, st))) return s;
+    if ((s = copy_rows(out->h1_out, m->at<float>(m->L.S), B, cf.d_model, st))) return s;
+    if (on && (s = copy_branch_rows(m, out->h2_out, B, Bp, st))) return s;
+  }
+  return DBT_OK;
+}
+
 }  // namespace
 
 // ===========================================================================
@@ -887,6 +939,7 @@ dbt_status dbt_create(const dbt_config *cfg, const dbt_weights *w, void *workspa
   m->w.h_layers = nullptr;
   m->ws = (char *)workspace;
   m->L = make_layout(cfg);
+  m->step = m->ws + m->L.state_total;
   // RoPE table (Eq. (8)): angle pos * theta^(-2i/d_h), evaluated in double.
   const int half = cfg->head_dim / 2;
   m->rope_host.resize((size_t)cfg->max_pos * half * 2);
@@ -1002,41 +1055,7 @@ dbt_status dbt_kv_fill(dbt_kv *kv, int32_t layer, int32_t b, int32_t start, int3
 
 dbt_status dbt_decode_step(dbt_model *m, dbt_kv *kv, const dbt_step_in *in, int32_t branch_on, dbt_step_out *out,
                            dbt_stream stream) {
-  dbt_status s = check_model_kv(m, kv);
-  if (s) return s;
-  s = check_step_in(m, kv, in, branch_on);
-  if (s) return s;
-  hipStream_t st = (hipStream_t)stream;
-  const dbt_config &cf = m->cfg;
-  const int B = in->batch, Bp = round16(B);
-  if ((s = ensure_device(m, st))) return s;  // before any state changes
-  m->bnd_kv = nullptr;
-  std::vector<int> pos = begin_step(kv, B);
-  StepBegin sb;
-  if ((s = flush(kv, pos.data(), B, st, &sb))) return s;
-  const bool on = branch_on != 0;
-  const int nb = n_branches(cf);
-  const Rows rows{B, Bp, 0, on ? 1 + nb : 1};
-  if ((s = load_inputs(m, kv, in, in->tokens, rows, st, &sb))) return s;
-  LayerCall lc{};
-  lc.rows = rows;
-  lc.mode = on ? MODE_GROUPED : MODE_PRIMARY;
-  lc.retain = false;
-  lc.ret_src = -1;
-  lc.prefill = false;
-  lc.rows_layout = (1 + nb) * Bp;
-  lc.last_norm = true;
-  lc.out = out;
-  for (int l = 0; l < cf.n_layers; ++l)
-    if ((s = run_layer(m, kv, l, lc, st))) return s;
-  if (cf.vocab > 0 && (s = lm_head(m, rows, st))) return s;
-  for (int b = 0; b < B; ++b) kv->len[b] += 1;
-  if (out) {
-    if ((s = readout(m, B, Bp, on, out, st))) return s;
-    if ((s = copy_rows(out->h1_out, m->at<float>(m->L.S), B, cf.d_model, st))) return s;
-    if (on && (s = copy_branch_rows(m, out->h2_out, B, Bp, st))) return s;
-  }
-  return DBT_OK;
+  return decode_step_impl(m, kv, in, branch_on, out, stream);
 }
 
 dbt_status dbt_decode_step_ungrouped(dbt_model *m, dbt_kv *kv, const dbt_step_in *in, dbt_step_out *out,
@@ -1117,7 +1136,7 @@ dbt_status dbt_prefill(dbt_model *m, dbt_kv *kv, const int32_t *tokens, const in
     const int T = h_prompt_lens[b];
     const Rows rows{T, T, 0, 1};
     HIPCHK(launch_embed(tokens + off, cf.vocab, m->w.emb1, m->w.emb2, m->w.emb_norm, m->layers[0].attn_norm, cf.rms_eps, d,
-                        cf.dtype, rows, m->at<float>(L.S), m->ws + L.Xn, d, st));
+                        cf.dtype, rows, m->at<float>(L.S), m->p(L.Xn), d, st));
     LayerCall lc{};
     lc.rows = rows;
     lc.mode = MODE_PRIMARY;
@@ -1138,7 +1157,7 @@ dbt_status dbt_prefill(dbt_model *m, dbt_kv *kv, const int32_t *tokens, const in
   // primary logits at each prompt's final position
   if (cf.vocab > 0) {
     HIPCHK(launch_rmsnorm_rows(m->at<float>(L.slast), m->w.final_norm, cf.rms_eps, d, cf.dtype, Rows{batch, 0, 0, 1},
-                               m->ws + L.Xn, d, st));
+                               m->p(L.Xn), d, st));
     if ((s = lm_head(m, Rows{batch, Bp, 0, 1}, st))) return s;
   }
   if (out) {
@@ -1166,7 +1185,7 @@ dbt_status dbt_boundary(dbt_model *m, dbt_kv *kv, int32_t batch, dbt_step_out *o
   if ((s = flush(kv, pos.data(), B, st))) return s;
   const Rows br{B, Bp, 1, n_branches(cf)};
   HIPCHK(launch_embed(m->at<int>(L.btok), cf.vocab, m->w.emb1, m->w.emb2, m->w.emb_norm, m->layers[0].attn_norm, cf.rms_eps,
-                      cf.d_model, cf.dtype, br, m->at<float>(L.S), m->ws + L.Xn, cf.d_model, st));
+                      cf.d_model, cf.dtype, br, m->at<float>(L.S), m->p(L.Xn), cf.d_model, st));
   if ((s = branch_pass(m, kv, B, Bp, st))) return s;
   m->bnd_kv = nullptr;
   if (out) {
@@ -1200,3 +1219,25 @@ double dbt_stage_time(dbt_model *m, int32_t stage, int32_t *h_launches) {
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Hooks for the allocation-free step (static_scratch.hip)
+// ---------------------------------------------------------------------------
+namespace dbt {
+
+dbt_status set_error(dbt_status s, const char *msg) { return fail(s, "%s", msg); }
+
+size_t step_bytes(const dbt_model *m) { return m->L.total - m->L.state_total; }
+
+dbt_status decode_step_in(dbt_model *m, dbt_kv *kv, const dbt_step_in *in, int32_t branch_on, dbt_step_out *out,
+                          dbt_stream stream, char *step_mem) {
+  // the model's own step region again when the call returns, whatever it returns
+  struct Restore {
+    dbt_model *m;
+    ~Restore() { m->step = m->ws + m->L.state_total; }
+  } restore{m};
+  m->step = step_mem;
+  return decode_step_impl(m, kv, in, branch_on, out, stream);
+}
+
+}  // namespace dbt

@@ -207,3 +207,24 @@ def test_degenerate_calls_rejected_without_state_change():
     finally:
         B.dbt_kv_destroy(kv)
         B.dbt_destroy(m)
+
+
+def test_noalloc_step_rejects_models_whose_step_buffers_exceed_the_static_scratch():
+    """The allocation-free step refuses, before touching the GPU or any
+    state, a model whose step buffers exceed the library's static array:
+    64 sequences of a 128256-entry vocabulary need 128 rows of logits
+    alone (62.6 MiB)."""
+    big = _cfg(dtype=B.DBT_BF16, n_layers=1, d_model=4096, n_q_heads=32, n_kv_heads=8, head_dim=128,
+               d_ff=14336, vocab=128256, has_embeddings=0, max_batch=64, max_pos=4112, max_prompt=0)
+    assert B.dbt_workspace_bytes(big) > 0
+    w, _keep = _fake_weights(big)
+    m = B.dbt_create(big, w, FAKE)
+    kv = B.dbt_kv_create(m, FAKE, FAKE, 64 * 257, FAKE, 257)
+    sin = B.dbt_step_in(tokens=0, h1_in=FAKE, h2_in=FAKE, batch=4)
+    out = B.dbt_step_out()
+    with pytest.raises(B.DbtError) as e:
+        B.dbt_decode_step_noalloc(m, kv, sin, 1, out, 0)
+    assert e.value.status == 5 and "static scratch" in str(e.value), e.value
+    assert B.dbt_kv_length(kv, 0) == 0
+    B.dbt_kv_destroy(kv)
+    B.dbt_destroy(m)
