@@ -11,10 +11,15 @@ sequences are truncated back to 4096 positions so every step sees the same
 cache length.
 
 Prints one JSON line.  value = tokens/s of the grouped step (32 continuation
-tokens per step).  Also reported: the primary-only and ungrouped step times,
-the branch overhead, the step's algorithmic HBM bytes and the roofline of the
-dominant kernel (the output-matrix projection), timed with HIP events on the
-stream it runs on, plus the CPU oracle timed on a bounded sample.
+tokens per step) over the contract's block of exactly K steps after W
+warm-ups.  Then the measurement protocol: grouped, primary-only and
+ungrouped steps interleaved for 100 iterations after 10 warm-ups, each step
+timed by HIP events on its stream, reported as median, p10 and p90 per mode
+(step_us, primary_only_us, ungrouped_us and the branch overhead are the
+medians).  Also reported: the step's algorithmic HBM bytes, every stage
+kernel's launch time and fraction of the HBM peak, the roofline of the
+dominant kernel (the output-matrix projection: its weight bytes over its
+event-timed launch), and the CPU oracle timed per mode on a bounded sample.
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--no-cpu-baseline]
 """
@@ -160,8 +165,10 @@ def algorithmic_bytes(shape, B, L):
     return layer, head, kv
 
 
-def time_mode(sess, B, L, h1d, h2d, mode, steps, warmup):
-    import torch
+def step_fn(sess, B, L, h1d, h2d, mode):
+    """A callable that enqueues one step of `mode` (grouped, primary or
+    ungrouped) and truncates every sequence back to L cached positions (host
+    bookkeeping only), so that every step sees the same cache."""
     from paper_2608_12385_amd import binding
     sin = sess.step_in(B, None, h1d, h2d)
     out, _t = sess.outputs(B, logits=False, hidden=False)
@@ -174,7 +181,14 @@ def time_mode(sess, B, L, h1d, h2d, mode, steps, warmup):
             binding.dbt_decode_step(sess.model, sess.kv, sin, 1 if mode == "grouped" else 0, out, st)
         for b in range(B):
             binding.dbt_kv_truncate(sess.kv, b, L)
+    one.keep = (sin, out, _t)
+    return one
 
+
+def time_block(one, steps, warmup):
+    """W untimed steps, then exactly K steps bracketed by device
+    synchronisation on both sides: seconds per step."""
+    import torch
     for _ in range(warmup):
         one()
     torch.cuda.synchronize()
@@ -182,28 +196,75 @@ def time_mode(sess, B, L, h1d, h2d, mode, steps, warmup):
     for _ in range(steps):
         one()
     torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    if mode != "grouped":
-        return (t1 - t0) / steps, 0.0, 0
-    # Second timed region for the roofline: the same steps with the library's
-    # HIP events around the LM-head launch, on the stream it is launched on
-    # (the event pair adds a few microseconds to each step, so the step time
-    # above is taken without it).
-    binding.dbt_stage_timing(sess.model, binding.STAGES["lmhead"], 1)
+    return (time.perf_counter() - t0) / steps
+
+
+def time_interleaved(fns, iters, warmup):
+    """The modes interleaved step by step (so drift in clocks or memory state
+    hits every mode alike), each step bracketed by HIP events recorded on the
+    stream the library launches on: per mode the list of step times (us)."""
+    import torch
+    names = list(fns)
+    for _ in range(warmup):
+        for n in names:
+            fns[n]()
+    torch.cuda.synchronize()
+    ev = {n: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(iters)]
+          for n in names}
+    for i in range(iters):
+        for n in names:
+            a, b = ev[n][i]
+            a.record()
+            fns[n]()
+            b.record()
+    torch.cuda.synchronize()
+    return {n: [a.elapsed_time(b) * 1e3 for a, b in ev[n]] for n in names}
+
+
+def dist(us):
+    """median, p10 and p90 of a list of step times."""
+    x = np.asarray(us, np.float64)
+    return {"median": float(np.median(x)), "p10": float(np.percentile(x, 10)), "p90": float(np.percentile(x, 90)),
+            "n": int(x.size)}
+
+
+STAGE_NAMES = ("qkv", "attn", "wo", "gateup", "down", "lmhead", "mix")
+
+
+def time_stages(sess, one, steps):
+    """Average launch time (us) of every stage kernel over `steps` grouped
+    steps, from HIP events the library records around each launch on its
+    stream (a separate pass: the event pairs add a few us per step)."""
+    import torch
+    from paper_2608_12385_amd import binding
+    for n in STAGE_NAMES:
+        binding.dbt_stage_timing(sess.model, binding.STAGES[n], 1)
     torch.cuda.synchronize()
     for _ in range(steps):
         one()
     torch.cuda.synchronize()
-    lm_ms, lm_n = binding.dbt_stage_time(sess.model, binding.STAGES["lmhead"])
-    binding.dbt_stage_timing(sess.model, binding.STAGES["lmhead"], 0)
-    return (t1 - t0) / steps, lm_ms, lm_n
+    res = {}
+    for n in STAGE_NAMES:
+        ms, cnt = binding.dbt_stage_time(sess.model, binding.STAGES[n])
+        binding.dbt_stage_timing(sess.model, binding.STAGES[n], 0)
+        res[n] = ms * 1e3 / max(cnt, 1)
+    return res
 
 
-def cpu_baseline(shape, W, h, L, B, min_seconds):
-    """The oracle as it stands on the same workload: all B sequences, one
-    grouped step after another (each sequence truncated back to L cached
-    positions, as in the timed GPU steps) until min_seconds have passed; the
-    first step includes the oracle's one-time parameter widening."""
+def stage_bytes(shape, B, L):
+    """Algorithmic bytes per launch of each stage kernel at batch B, cache L:
+    the weights the kernel reads once (the attention: the live cache)."""
+    d, dq, dkv, f, V = shape.d_model, shape.d_q, shape.d_kv, shape.d_ff, shape.vocab
+    return {"qkv": (dq + 2 * dkv) * d * 2, "attn": B * (L + 1) * 2 * dkv * 2, "wo": d * dq * 2,
+            "gateup": 2 * f * d * 2, "down": d * f * 2, "lmhead": V * d * 2}
+
+
+def cpu_baseline(shape, W, h, L, B, seconds_per_mode):
+    """The oracle as it stands on the same workload, per mode: whole steps of
+    all B sequences (each truncated back to L cached positions, as in the
+    timed GPU steps) until seconds_per_mode have passed, for the grouped
+    step, the primary-only step and the two-pass step.  The oracle's one-time
+    parameter widening is done before the clocks start."""
     import synth
     from oracle import Oracle
     try:
@@ -211,24 +272,32 @@ def cpu_baseline(shape, W, h, L, B, min_seconds):
         threads = max([i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()] or [1])
     except Exception:  # pragma: no cover
         threads = os.cpu_count()
-    kvs = [synth.make_kv(shape, 0, b, L, seed=3) for b in range(B)]
-    t0 = time.perf_counter()
     orc = Oracle(shape, W.values)
     for b in range(B):
-        (k, _), (v, _) = kvs[b]
+        (k, _), (v, _) = synth.make_kv(shape, 0, b, L, seed=3)
         orc.kv_fill(b, L, [k], [v])
-    steps = 0
-    while True:
-        orc.decode_step(h1=h[0], h2=h[1])
-        for b in range(B):
-            orc.truncate(b, L)
-        steps += 1
-        dt = time.perf_counter() - t0
-        if dt >= min_seconds or steps >= 64:
-            break
-    return dict(value=steps * B / dt, unit="tokens/s", cores=int(threads), kind="oracle",
-                sample=f"{steps} grouped steps of all {B} sequences (float64 NumPy oracle, parameter widening "
-                       f"included), {dt:.1f} s")
+    for name in list(W.values):
+        orc.w(name)                      # widen the parameters once
+    modes = {"grouped": dict(branch_on=True, grouped=True), "primary_only": dict(branch_on=False),
+             "ungrouped": dict(branch_on=True, grouped=False)}
+    per = {}
+    for mode, kw in modes.items():
+        steps = 0
+        t0 = time.perf_counter()
+        while True:
+            orc.decode_step(h1=h[0], h2=h[1], **kw)
+            for b in range(B):
+                orc.truncate(b, L)
+            steps += 1
+            dt = time.perf_counter() - t0
+            if dt >= seconds_per_mode or steps >= 64:
+                break
+        per[mode] = {"tokens_per_s": steps * B / dt, "step_s": dt / steps, "steps": steps}
+    return dict(value=per["grouped"]["tokens_per_s"], unit="tokens/s", cores=int(threads), kind="oracle",
+                sample=f"whole steps of all {B} sequences per mode (float64 NumPy oracle): "
+                       + ", ".join(f"{m} {v['steps']} steps in {v['step_s'] * v['steps']:.1f} s"
+                                   for m, v in per.items()),
+                per_mode={m: v["tokens_per_s"] for m, v in per.items()})
 
 
 def time_workload(name, steps, warmup, **shape_kw):
@@ -346,8 +415,12 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0,
-                    help="minimum CPU time of the oracle baseline (whole grouped steps)")
+    ap.add_argument("--cpu-seconds", type=float, default=8.0,
+                    help="minimum CPU time of the oracle baseline per mode (whole steps)")
+    ap.add_argument("--protocol-iters", type=int, default=100,
+                    help="timed iterations of the interleaved three-mode measurement")
+    ap.add_argument("--protocol-warmup", type=int, default=10,
+                    help="untimed iterations before the interleaved measurement")
     ap.add_argument("--all", action="store_true",
                     help="also time the long-context and MoE workloads (extra fields)")
     ap.add_argument("--calib-copy", action="store_true",
@@ -413,21 +486,28 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    t_grp, lm_ms, lm_n = time_mode(sess, B, L, h1d, h2d, "grouped", args.steps, args.warmup)
-    if args.grouped_only:
-        t_pri = t_ung = float("nan")
-    else:
-        t_pri, _, _ = time_mode(sess, B, L, h1d, h2d, "primary", args.steps, args.warmup)
-        t_ung, _, _ = time_mode(sess, B, L, h1d, h2d, "ungrouped", args.steps, args.warmup)
+    fns = {m: step_fn(sess, B, L, h1d, h2d, m) for m in ("grouped", "primary", "ungrouped")}
+    # the contract's timed block: exactly K grouped steps after W warm-ups
+    t_grp = time_block(fns["grouped"], args.steps, args.warmup)
+    proto = stages = None
+    if not args.grouped_only:
+        # the measurement protocol: the three modes interleaved, each step
+        # timed by HIP events; median, p10 and p90 per mode
+        us = time_interleaved(fns, args.protocol_iters, args.protocol_warmup)
+        proto = {m: dist(v) for m, v in us.items()}
+        paired = [100.0 * (g - p) / p for g, p in zip(us["grouped"], us["primary"])]
+        proto["overhead_pct_paired"] = dist(paired)
+    stages = time_stages(sess, fns["grouped"], max(args.steps, 20))
 
     traffic_lm, traffic_step = recorded_traffic()
     layer_b, head_b, kv_b = algorithmic_bytes(shape, B, L)
     step_bytes = layer_b + head_b + kv_b
-    x_bytes = 2 * B * shape.d_model * 2
     logit_bytes = 2 * B * shape.vocab * 4
-    lm_alg = head_b + x_bytes + logit_bytes
-    lm_s = (lm_ms / max(lm_n, 1)) / 1e3
-    lm_gbps = lm_alg / lm_s / 1e9
+    sb = stage_bytes(shape, B, L)
+    lm_s = stages["lmhead"] / 1e6
+    lm_gbps = sb["lmhead"] / lm_s / 1e9
+    med = (lambda m: proto[m]["median"]) if proto else (lambda m: float("nan"))
+    t_med = med("grouped") if proto else t_grp * 1e6
     line = {
         "metric": METRIC,
         "value": B / t_grp,
@@ -447,15 +527,28 @@ def main():
                         "batch 32, KV cache 4096/sequence in 16-token pages",
             "batch": B, "cache_len": L, "page": 16,
         },
-        "step_us": t_grp * 1e6,
-        "primary_only_us": t_pri * 1e6,
-        "ungrouped_us": t_ung * 1e6,
-        "branch_overhead_pct": 100.0 * (t_grp - t_pri) / t_pri,
+        "step_us": t_med,
+        "step_us_block_mean": t_grp * 1e6,
+        "primary_only_us": med("primary"),
+        "ungrouped_us": med("ungrouped"),
+        "branch_overhead_pct": 100.0 * (med("grouped") - med("primary")) / med("primary"),
+        "protocol": None if proto is None else {
+            "iterations": args.protocol_iters, "warmup": args.protocol_warmup,
+            "order": "grouped, primary-only, ungrouped interleaved per iteration; HIP events per step",
+            "grouped_us": proto["grouped"], "primary_only_us": proto["primary"],
+            "ungrouped_us": proto["ungrouped"], "branch_overhead_pct_paired": proto["overhead_pct_paired"]},
         "algorithmic_MB_per_step": step_bytes / 1e6,
-        "step_GBps": step_bytes / t_grp / 1e9,
-        "step_frac_of_peak": step_bytes / t_grp / 1e9 / HBM_PEAK_GBPS,
+        "step_GBps": step_bytes / t_med * 1e6 / 1e9,
+        "step_frac_of_peak": step_bytes / t_med * 1e6 / 1e9 / HBM_PEAK_GBPS,
         "step_traffic_MB": None if traffic_step is None else traffic_step / 1e6,
         "step_traffic_vs_algorithmic": None if traffic_step is None else traffic_step / step_bytes,
+        "stages": {n: {"launch_us": stages[n],
+                       **({"algorithmic_MB": sb[n] / 1e6, "GBps": sb[n] / stages[n] / 1e3,
+                           "frac": sb[n] / stages[n] / 1e3 / HBM_PEAK_GBPS} if n in sb else {})}
+                   for n in STAGE_NAMES},
+        "stages_note": "grouped step; launch times from library HIP events on the step's stream (separate pass); "
+                       "the remainder of the step is the row kernels (norms, rotary/append, split sums, "
+                       "coupling) and launch gaps",
         "roofline": {
             "kernel": "LM-head projection (k_gemm_bf16, 64 stacked rows)",
             "bound": "hbm",
@@ -464,8 +557,11 @@ def main():
             "unit": "GB/s",
             "frac": lm_gbps / HBM_PEAK_GBPS,
             "traffic": traffic_lm,
-            "launch_us": lm_s * 1e6,
-            "algorithmic_MB_per_launch": lm_alg / 1e6,
+            "launch_us": stages["lmhead"],
+            "algorithmic_MB_per_launch": sb["lmhead"] / 1e6,
+            "algorithmic_note": "the output matrix read once (vocab x d_model bf16); the fp32 logits it also "
+                                "writes are counted in traffic, not here",
+            "logits_written_MB_per_launch": logit_bytes / 1e6,
         },
     }
     if not args.no_cpu_baseline:
