@@ -87,6 +87,7 @@ dbt_status check_config(const dbt_config *c) {
   if (c->n_q_heads % c->n_kv_heads) return fail(DBT_ERR_SHAPE, "n_q_heads %% n_kv_heads != 0");
   if (c->head_dim % 4) return fail(DBT_ERR_SHAPE, "head_dim must be a multiple of 4");
   if (c->d_model % 4) return fail(DBT_ERR_SHAPE, "d_model must be a multiple of 4");
+  if (c->d_model > 32768) return fail(DBT_ERR_UNSUPPORTED, "d_model above 32768");
   if (c->max_prompt > c->max_pos) return fail(DBT_ERR_SHAPE, "max_prompt > max_pos");
   if (c->n_experts > 0) {
     if (c->dtype != DBT_BF16) return fail(DBT_ERR_UNSUPPORTED, "MoE layers run in bf16 only");

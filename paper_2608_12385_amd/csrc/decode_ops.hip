@@ -77,8 +77,27 @@ __device__ void norm_row(const float *x, const float *g, float eps, int d, T *ou
     st4<T>(out, i, mul4(((const float4 *)x)[i], inv, ((const float4 *)g)[i]));
 }
 
+// The same norm on a row a thread holds in registers: v[k] is element
+// (float4) i = threadIdx.x + k * blockDim.x of the row, valid while i < d/4.
+// The row is not read back from memory.
+template <typename T, int R>
+__device__ __forceinline__ void norm_regs(const float4 (&v)[R], const float *g, float eps, int d, T *out,
+                                          float *red) {
+  float ss = 0.f;
+#pragma unroll
+  for (int k = 0; k < R; ++k)
+    if (threadIdx.x + k * blockDim.x < d / 4) ss += dot4(v[k]);
+  ss = block_sum(ss, red);
+  const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+#pragma unroll
+  for (int k = 0; k < R; ++k) {
+    const int i = threadIdx.x + k * blockDim.x;
+    if (i < d / 4) st4<T>(out, i, mul4(v[k], inv, ((const float4 *)g)[i]));
+  }
+}
+
 // Tokens outside [0, vocab) read as a zero embedding row (no out-of-bounds read).
-template <typename T>
+template <typename T, int R>
 __global__ void k_embed(const int *tokens, int vocab, const T *e1, const T *e2, const float *g_emb,
                         const float *g_next, float eps, int d, Rows rows, float *S, T *Xn, int ldx, StepBegin sb,
                         int *pos_arr, int *page_table, int mpps) {
@@ -90,21 +109,29 @@ __global__ void k_embed(const int *tokens, int vocab, const T *e1, const T *e2, 
   const bool valid = tok >= 0 && tok < vocab;
   // decode branch j >= 1 reads table j of the branch tables (App. C.1 for j >= 2)
   const T *e = (path == 0 ? e1 : e2 + (size_t)(path - 1) * vocab * d) + (size_t)(valid ? tok : 0) * d;
-  float *s = S + (size_t)row * d;
+  float4 v[R];
   float ss = 0.f;
-  for (int i = threadIdx.x; i < d / 4; i += blockDim.x) {
-    const float4 v = valid ? ld4<T>(e, i) : make_float4(0.f, 0.f, 0.f, 0.f);
-    ((float4 *)s)[i] = v;
-    ss += dot4(v);
+#pragma unroll
+  for (int k = 0; k < R; ++k) {
+    const int i = threadIdx.x + k * blockDim.x;
+    v[k] = valid && i < d / 4 ? ld4<T>(e, i) : make_float4(0.f, 0.f, 0.f, 0.f);
+    ss += dot4(v[k]);
   }
   ss = block_sum(ss, red);
   const float inv = 1.0f / sqrtf(ss / (float)d + eps);
-  for (int i = threadIdx.x; i < d / 4; i += blockDim.x) ((float4 *)s)[i] = mul4(((float4 *)s)[i], inv, ((const float4 *)g_emb)[i]);
-  __syncthreads();
-  norm_row<T>(s, g_next, eps, d, Xn + (size_t)row * ldx, red);
+  float4 *s = (float4 *)(S + (size_t)row * d);
+#pragma unroll
+  for (int k = 0; k < R; ++k) {
+    const int i = threadIdx.x + k * blockDim.x;
+    if (i < d / 4) {
+      v[k] = mul4(v[k], inv, ((const float4 *)g_emb)[i]);
+      s[i] = v[k];
+    }
+  }
+  norm_regs<T, R>(v, g_next, eps, d, Xn + (size_t)row * ldx, red);
 }
 
-template <typename T>
+template <typename T, int R>
 __global__ void k_load_hidden(const float *h1, const float *h2, const float *g_next, float eps, int d,
                               Rows rows, float *S, T *Xn, int ldx, StepBegin sb, int *pos_arr, int *page_table,
                               int mpps) {
@@ -112,11 +139,16 @@ __global__ void k_load_hidden(const float *h1, const float *h2, const float *g_n
   apply_step_begin(sb, pos_arr, page_table, mpps);
   const int b = blockIdx.x, path = rows.p0 + blockIdx.y;
   const int row = phys_row(rows, path, b);
-  const float *h = (path == 0 ? h1 : h2 + (size_t)(path - 1) * rows.B * d) + (size_t)b * d;
-  float *s = S + (size_t)row * d;
-  for (int i = threadIdx.x; i < d / 4; i += blockDim.x) ((float4 *)s)[i] = ((const float4 *)h)[i];
-  __syncthreads();
-  norm_row<T>(s, g_next, eps, d, Xn + (size_t)row * ldx, red);
+  const float4 *h = (const float4 *)((path == 0 ? h1 : h2 + (size_t)(path - 1) * rows.B * d) + (size_t)b * d);
+  float4 *s = (float4 *)(S + (size_t)row * d);
+  float4 v[R];
+#pragma unroll
+  for (int k = 0; k < R; ++k) {
+    const int i = threadIdx.x + k * blockDim.x;
+    v[k] = i < d / 4 ? h[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+    if (i < d / 4) s[i] = v[k];
+  }
+  norm_regs<T, R>(v, g_next, eps, d, Xn + (size_t)row * ldx, red);
 }
 
 template <typename T>
@@ -205,36 +237,37 @@ __global__ void k_qkv_finish(QKVFinish f) {
 // MLP input RMSNorm.  Compute-matched variant (App. B.3): a branch row adds
 // g_A * A1, A1 being the primary row's projection output (both paths in the
 // call) or the kept A1 (branch-only call); primary rows can keep A1.
-template <typename T>
+template <typename T, int R>
 __global__ void k_resid_norm(const float *part, long long stride, int S, int ldp, float *Sres,
                              const float *g, float eps, int d, Rows rows, T *Xn, int ldx, GatedCopy gc) {
   __shared__ float red[16];
   const int b = blockIdx.x, path = rows.p0 + blockIdx.y;
   const int row = phys_row(rows, path, b);
-  float *s = Sres + (size_t)row * d;
-  if (!gc.g) {
-    for (int i = threadIdx.x; i < d / 4; i += blockDim.x)
-      ((float4 *)s)[i] = add4(((float4 *)s)[i], psum4(part, stride, S, ((size_t)row * ldp) / 4 + i));
-  } else if (path == 0) {
-    const bool keep = gc.ret.ptr && (gc.ret.src_row < 0 || gc.ret.src_row == b);
-    float4 *kept = keep ? (float4 *)(gc.ret.ptr + (size_t)(gc.ret.src_row < 0 ? b : gc.ret.dst_row) * d) : nullptr;
-    for (int i = threadIdx.x; i < d / 4; i += blockDim.x) {
+  float4 *s = (float4 *)(Sres + (size_t)row * d);
+  const bool keep = gc.g && path == 0 && gc.ret.ptr && (gc.ret.src_row < 0 || gc.ret.src_row == b);
+  float4 *kept = keep ? (float4 *)(gc.ret.ptr + (size_t)(gc.ret.src_row < 0 ? b : gc.ret.dst_row) * d) : nullptr;
+  const int r1 = phys_row(rows, 0, b);
+  float4 v[R];
+#pragma unroll
+  for (int k = 0; k < R; ++k) {
+    const int i = threadIdx.x + k * blockDim.x;
+    v[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (i >= d / 4) continue;
+    if (!gc.g || path == 0) {
       const float4 a1 = psum4(part, stride, S, ((size_t)row * ldp) / 4 + i);
-      ((float4 *)s)[i] = add4(((float4 *)s)[i], a1);
+      v[k] = add4(s[i], a1);
       if (keep) kept[i] = a1;
-    }
-  } else {
-    const int r1 = phys_row(rows, 0, b);
-    for (int i = threadIdx.x; i < d / 4; i += blockDim.x) {
+    } else {
+      // compute-matched branch row: S_bar2 = S2 + g_A * A1
       const float4 a1 = rows.p0 == 0 ? psum4(part, stride, S, ((size_t)r1 * ldp) / 4 + i)
                                      : ((const float4 *)(gc.in + (size_t)b * d))[i];
       const float4 ga = ((const float4 *)gc.g)[i];
-      const float4 v = ((float4 *)s)[i];
-      ((float4 *)s)[i] = make_float4(v.x + ga.x * a1.x, v.y + ga.y * a1.y, v.z + ga.z * a1.z, v.w + ga.w * a1.w);
+      const float4 x = s[i];
+      v[k] = make_float4(x.x + ga.x * a1.x, x.y + ga.y * a1.y, x.z + ga.z * a1.z, x.w + ga.w * a1.w);
     }
+    s[i] = v[k];
   }
-  __syncthreads();
-  norm_row<T>(s, g, eps, d, Xn + (size_t)row * ldx, red);
+  norm_regs<T, R>(v, g, eps, d, Xn + (size_t)row * ldx, red);
 }
 
 // SwiGLU and the MLP-intermediate coupling H2~ = H2 + b * H1 (Eq. (14)).
@@ -273,7 +306,7 @@ __global__ void k_swiglu_finish(const float *part, long long stride, int S, int 
 // After the MLP down projection: M1, M2 = M2' + c * M1 (Eq. (15)),
 // S <- S_bar + M (Eq. (16)), then the next RMSNorm (next layer's attention
 // norm, or the final norm before the output matrix).
-template <typename T>
+template <typename T, int R>
 __global__ void k_down_finish(const float *part, long long stride, int S, int ldp, int d, int mode,
                               Rows rows, const float *cvec, const float *M1_in, Retain ret,
                               float *Sres, const float *g_next, float eps, T *Xn, int ldx) {
@@ -285,33 +318,43 @@ __global__ void k_down_finish(const float *part, long long stride, int S, int ld
   float4 *s1 = (float4 *)(Sres + (size_t)r1 * d);
   const bool keep = ret.ptr && (ret.src_row < 0 || ret.src_row == b);
   float4 *kept = keep ? (float4 *)(ret.ptr + (size_t)(ret.src_row < 0 ? b : ret.dst_row) * d) : nullptr;
-  for (int i = threadIdx.x; i < d / 4; i += blockDim.x) {
+  constexpr int MP = 4;  // paths of one sequence: the primary and up to three branches
+  float4 v[MP][R];
+#pragma unroll
+  for (int k = 0; k < R; ++k) {
+    const int i = threadIdx.x + k * blockDim.x;
+#pragma unroll
+    for (int p = 0; p < MP; ++p) v[p][k] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (i >= d / 4) continue;
     float4 m1;
     if (prim) {
       m1 = psum4(part, stride, S, ((size_t)r1 * ldp) / 4 + i);
-      s1[i] = add4(s1[i], m1);
+      v[0][k] = add4(s1[i], m1);
+      s1[i] = v[0][k];
       if (keep) kept[i] = m1;
     } else {
       m1 = ((const float4 *)(M1_in + (size_t)b * d))[i];
     }
     if (br)
-      for (int p = pb0; p < pb1; ++p) {
+#pragma unroll
+      for (int p = 1; p < MP; ++p) {
+        if (p < pb0 || p >= pb1) continue;
         const int r2 = phys_row(rows, p, b);
         float4 *s2 = (float4 *)(Sres + (size_t)r2 * d);
         const float4 m2 = psum4(part, stride, S, ((size_t)r2 * ldp) / 4 + i);
         const float4 c = ((const float4 *)cvec)[i];
         const float4 t = make_float4(m2.x + c.x * m1.x, m2.y + c.y * m1.y, m2.z + c.z * m1.z, m2.w + c.w * m1.w);
-        s2[i] = add4(s2[i], t);
+        v[p][k] = add4(s2[i], t);
+        s2[i] = v[p][k];
       }
   }
   if (!g_next) return;
-  __syncthreads();
-  if (prim) norm_row<T>((const float *)s1, g_next, eps, d, Xn + (size_t)r1 * ldx, red);
+  if (prim) norm_regs<T, R>(v[0], g_next, eps, d, Xn + (size_t)r1 * ldx, red);
   if (br)
-    for (int p = pb0; p < pb1; ++p) {
-      const int r2 = phys_row(rows, p, b);
-      __syncthreads();
-      norm_row<T>(Sres + (size_t)r2 * d, g_next, eps, d, Xn + (size_t)r2 * ldx, red);
+#pragma unroll
+    for (int p = 1; p < MP; ++p) {
+      if (p < pb0 || p >= pb1) continue;
+      norm_regs<T, R>(v[p], g_next, eps, d, Xn + (size_t)phys_row(rows, p, b) * ldx, red);
     }
 }
 
@@ -586,6 +629,20 @@ static int row_threads(int d) {
   return t < 64 ? 64 : t > 1024 ? 1024 : t;
 }
 
+// float4 elements per thread of the register-resident row kernels (d up to
+// 32768, checked when the model is created).
+static int row_regs(int d) {
+  const int n = (d / 4 + row_threads(d) - 1) / row_threads(d);
+  return n <= 1 ? 1 : n <= 2 ? 2 : n <= 4 ? 4 : 8;
+}
+#define DBT_ROW_LAUNCH(KERNEL, T, d, ...)                                                            \
+  switch (row_regs(d)) {                                                                            \
+    case 1: hipLaunchKernelGGL((KERNEL<T, 1>), __VA_ARGS__); break;                                 \
+    case 2: hipLaunchKernelGGL((KERNEL<T, 2>), __VA_ARGS__); break;                                 \
+    case 4: hipLaunchKernelGGL((KERNEL<T, 4>), __VA_ARGS__); break;                                 \
+    default: hipLaunchKernelGGL((KERNEL<T, 8>), __VA_ARGS__); break;                                \
+  }
+
 hipError_t launch_embed(const int *tokens, int vocab, const void *e1, const void *e2, const float *g_emb,
                         const float *g_next, float eps, int d, int dtype, Rows rows, float *S,
                         void *Xn, int ldx, hipStream_t st, const StepBegin *sb, int *pos_arr, int *page_table,
@@ -596,14 +653,15 @@ hipError_t launch_embed(const int *tokens, int vocab, const void *e1, const void
   none.b0 = 0;
   const StepBegin &s = sb ? *sb : none;
   const int threads = std::max(row_threads(d), 64);
-  if (dtype == 1)
-    hipLaunchKernelGGL(k_embed<uint16_t>, grid, dim3(threads), 0, st, tokens, vocab, (const uint16_t *)e1,
-                       (const uint16_t *)e2, g_emb, g_next, eps, d, rows, S, (uint16_t *)Xn, ldx, s, pos_arr,
-                       page_table, mpps);
-  else
-    hipLaunchKernelGGL(k_embed<float>, grid, dim3(threads), 0, st, tokens, vocab, (const float *)e1,
-                       (const float *)e2, g_emb, g_next, eps, d, rows, S, (float *)Xn, ldx, s, pos_arr, page_table,
-                       mpps);
+  if (dtype == 1) {
+    DBT_ROW_LAUNCH(k_embed, uint16_t, d, grid, dim3(threads), 0, st, tokens, vocab, (const uint16_t *)e1,
+                   (const uint16_t *)e2, g_emb, g_next, eps, d, rows, S, (uint16_t *)Xn, ldx, s, pos_arr,
+                   page_table, mpps)
+  } else {
+    DBT_ROW_LAUNCH(k_embed, float, d, grid, dim3(threads), 0, st, tokens, vocab, (const float *)e1,
+                   (const float *)e2, g_emb, g_next, eps, d, rows, S, (float *)Xn, ldx, s, pos_arr, page_table,
+                   mpps)
+  }
   return hipGetLastError();
 }
 
@@ -616,12 +674,13 @@ hipError_t launch_load_hidden(const float *h1, const float *h2, const float *g_n
   none.b0 = 0;
   const StepBegin &s = sb ? *sb : none;
   const int threads = std::max(row_threads(d), 64);
-  if (dtype == 1)
-    hipLaunchKernelGGL(k_load_hidden<uint16_t>, grid, dim3(threads), 0, st, h1, h2, g_next, eps, d, rows, S,
-                       (uint16_t *)Xn, ldx, s, pos_arr, page_table, mpps);
-  else
-    hipLaunchKernelGGL(k_load_hidden<float>, grid, dim3(threads), 0, st, h1, h2, g_next, eps, d, rows, S,
-                       (float *)Xn, ldx, s, pos_arr, page_table, mpps);
+  if (dtype == 1) {
+    DBT_ROW_LAUNCH(k_load_hidden, uint16_t, d, grid, dim3(threads), 0, st, h1, h2, g_next, eps, d, rows, S,
+                   (uint16_t *)Xn, ldx, s, pos_arr, page_table, mpps)
+  } else {
+    DBT_ROW_LAUNCH(k_load_hidden, float, d, grid, dim3(threads), 0, st, h1, h2, g_next, eps, d, rows, S,
+                   (float *)Xn, ldx, s, pos_arr, page_table, mpps)
+  }
   return hipGetLastError();
 }
 
@@ -650,12 +709,13 @@ hipError_t launch_resid_norm(const float *part, long long stride, int S, int ldp
                              const float *g, float eps, int d, int dtype, Rows rows, void *Xn, int ldx,
                              hipStream_t st, const GatedCopy &gc) {
   dim3 grid(rows.B, rows.np);
-  if (dtype == 1)
-    hipLaunchKernelGGL(k_resid_norm<uint16_t>, grid, dim3(row_threads(d)), 0, st, part, stride, S, ldp, Sres, g, eps, d,
-                       rows, (uint16_t *)Xn, ldx, gc);
-  else
-    hipLaunchKernelGGL(k_resid_norm<float>, grid, dim3(row_threads(d)), 0, st, part, stride, S, ldp, Sres, g, eps, d,
-                       rows, (float *)Xn, ldx, gc);
+  if (dtype == 1) {
+    DBT_ROW_LAUNCH(k_resid_norm, uint16_t, d, grid, dim3(row_threads(d)), 0, st, part, stride, S, ldp, Sres, g, eps,
+                   d, rows, (uint16_t *)Xn, ldx, gc)
+  } else {
+    DBT_ROW_LAUNCH(k_resid_norm, float, d, grid, dim3(row_threads(d)), 0, st, part, stride, S, ldp, Sres, g, eps, d,
+                   rows, (float *)Xn, ldx, gc)
+  }
   return hipGetLastError();
 }
 
@@ -676,12 +736,13 @@ hipError_t launch_down_finish(const float *part, long long stride, int S, int ld
                               Rows rows, const float *cvec, const float *M1_in, Retain ret, float *Sres,
                               const float *g_next, float eps, int dtype, void *Xn, int ldx, hipStream_t st) {
   dim3 grid(rows.B);
-  if (dtype == 1)
-    hipLaunchKernelGGL(k_down_finish<uint16_t>, grid, dim3(row_threads(d)), 0, st, part, stride, S, ldp, d, mode, rows,
-                       cvec, M1_in, ret, Sres, g_next, eps, (uint16_t *)Xn, ldx);
-  else
-    hipLaunchKernelGGL(k_down_finish<float>, grid, dim3(row_threads(d)), 0, st, part, stride, S, ldp, d, mode, rows,
-                       cvec, M1_in, ret, Sres, g_next, eps, (float *)Xn, ldx);
+  if (dtype == 1) {
+    DBT_ROW_LAUNCH(k_down_finish, uint16_t, d, grid, dim3(row_threads(d)), 0, st, part, stride, S, ldp, d, mode, rows,
+                   cvec, M1_in, ret, Sres, g_next, eps, (uint16_t *)Xn, ldx)
+  } else {
+    DBT_ROW_LAUNCH(k_down_finish, float, d, grid, dim3(row_threads(d)), 0, st, part, stride, S, ldp, d, mode, rows,
+                   cvec, M1_in, ret, Sres, g_next, eps, (float *)Xn, ldx)
+  }
   return hipGetLastError();
 }
 

@@ -24,6 +24,12 @@ namespace {
 constexpr int kChunk = 128;  // reduction elements per pipeline stage
 constexpr int kLdsRow = kChunk + 8;  // padded LDS row of a staged activation chunk (elements)
 
+constexpr int gcd2(int a, int b) { return b == 0 ? a : gcd2(b, a % b); }
+constexpr int lcm3(int a, int b, int c) {
+  const int ab = a / gcd2(a, b) * b;
+  return ab / gcd2(ab, c) * c;
+}
+
 // A workgroup owns NW*16*RB consecutive weight rows of one segment (the last
 // tile of a segment may be partial: its rows past the end re-read the last
 // row and are not stored); wave w owns rows w*16*RB .. +16*RB and runs the
@@ -52,7 +58,7 @@ constexpr int kLdsRow = kChunk + 8;  // padded LDS row of a staged activation ch
 // half of the waves) and the same rows of segment 1 (up, the second half);
 // instead of storing Y it finishes the MLP intermediate in its epilogue (see
 // GluEpi).
-template <int MB, int RB, int PD, int NW, bool GLU = false>
+template <int MB, int RB, int PD, int NW, bool GLU = false, int XA = 2>
 __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const uint16_t *__restrict__ X, int ldx,
                                                        int M, float *__restrict__ Y, int ldy,
                                                        long long y_split_stride, float *__restrict__ row_stats,
@@ -115,7 +121,8 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
 #pragma unroll
     for (int cb = 0; cb < MB; ++cb) acc[rb][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  u32x4 a[PD][RB][4], stg[2][PPT];
+  static_assert(XA >= 2, "activation chunks are loaded at least two steps ahead");
+  u32x4 a[PD][RB][4], stg[XA][PPT];
   auto koff = [&](int c) {  // logical chunk c (clamped) of this workgroup's rotated order
     c = min(c, nch - 1) + crot;
     return (c >= nch ? c - nch : c) * kChunk;
@@ -137,10 +144,12 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
     for (int j = 0; j < PPT; ++j)
       if (PIECES % (NW * 64) == 0 || xdst[j] >= 0) *(u32x4 *)(&xs[lds][xdst[j]]) = stg[slot][j];
   };
-  // multiply chunk c (weight ring slot w, activation slot par = c & 1); load
-  // the activations of chunk c+2 and the weights of chunk c+PD; stage chunk
-  // c+1 (loaded one step ago).  w and par are compile-time at every call.
-  auto step = [&](int c, int w, int par) {
+  // multiply chunk c (weight ring slot w = c % PD, LDS slot par = c & 1);
+  // load the activations of chunk c+XA (register slot xc = c % XA, whose
+  // chunk c went to LDS one step ago) and the weights of chunk c+PD; stage
+  // chunk c+1 (register slot xn = (c+1) % XA, loaded XA-1 steps ago) into
+  // the other LDS slot.  All slots are compile-time at every call.
+  auto step = [&](int c, int w, int par, int xc, int xn) {
     const uint16_t *xl = xs[par];
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
@@ -155,30 +164,30 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
                                                                 __builtin_bit_cast(bf16x8, bx[cb]), acc[rb][cb], 0, 0,
                                                                 0);
     }
-    xload(par, c + 2);
+    xload(xc, c + XA);
     wload(w, c + PD);
-    xstore(par ^ 1, par ^ 1);
+    xstore(par ^ 1, xn);
     __syncthreads();
   };
 
-  xload(0, 0);
-  xload(1, 1);
+#pragma unroll
+  for (int u = 0; u < XA; ++u) xload(u, u);
 #pragma unroll
   for (int u = 0; u < PD; ++u) wload(u, u);
   xstore(0, 0);
   __syncthreads();
-  // rounds of P2 chunks (a multiple of PD and of 2, so both ring positions
-  // are constants); the round's loads are the same every time, which keeps
-  // the wait counts exact across the loop's back edge
-  constexpr int P2 = PD % 2 == 0 ? PD : 2 * PD;
+  // rounds of P2 chunks (a common multiple of PD, XA and 2, so every ring
+  // position is a constant); the round's loads are the same every time,
+  // which keeps the wait counts exact across the loop's back edge
+  constexpr int P2 = lcm3(PD, XA, 2);
   int c0 = 0;
   for (; c0 + P2 <= nch; c0 += P2) {
 #pragma unroll
-    for (int u = 0; u < P2; ++u) step(c0 + u, u % PD, u & 1);
+    for (int u = 0; u < P2; ++u) step(c0 + u, u % PD, u & 1, u % XA, (u + 1) % XA);
   }
 #pragma unroll
   for (int u = 0; u + 1 < P2; ++u)
-    if (c0 + u < nch) step(c0 + u, u % PD, u & 1);
+    if (c0 + u < nch) step(c0 + u, u % PD, u & 1, u % XA, (u + 1) % XA);
   // lane holds D[n = rb*16 + 4*gq + i][m = cb*16 + r]: Y[m][n .. n+3]
   if constexpr (GLU) {
     // hb[m][c]: the tile's TC gate/up columns c for activation row m
