@@ -46,7 +46,7 @@ __device__ __forceinline__ bool split_range(int npages, int target, int s, int *
 // eight waves (at most 1024 pages, page ids staged in LDS), the waves merged
 // in LDS and the normalised rows written to a.O directly.
 template <int NW>
-__global__ __launch_bounds__(NW * 64) void k_attn_decode_bf16(AttnArgs a) {
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) void k_attn_decode_bf16(AttnArgs a) {
   constexpr int DH = 128;
   constexpr bool SINGLE = NW == 8;
   const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
@@ -117,23 +117,66 @@ __global__ __launch_bounds__(NW * 64) void k_attn_decode_bf16(AttnArgs a) {
   const int vpage = gq >> 1, vpos = 8 * (gq & 1);
   const int npairs = (pe - pb + 1) >> 1;
   const int last = pe - pb - 1;  // a missing second page re-reads the first (masked)
-  // K/V of pair q into registers (q past the last pair re-reads the last one:
-  // loads stay unconditional, so each wait covers its own pair only)
-  auto load_pair = [&](int q, u32x4 (&ka)[4], u32x4 (&kb)[4], u32x4 (&vf)[8]) __attribute__((always_inline)) {
-    q = min(q, npairs - 1);
-    const int phys0 = page_id(2 * q);
-    const int phys1 = page_id(min(2 * q + 1, last));
-    const int kphys = kpage ? phys1 : phys0;
-    const int vphys = vpage ? phys1 : phys0;
-    const uint16_t *kp = kbase + ((size_t)kphys * n_kv + g) * 16 * DH + kpos * DH + gq * 8;
-    const uint16_t *vp = vbase + ((size_t)vphys * n_kv + g) * DH * 16 + r * 16 + vpos;
+  // K/V of pair q into registers: each page's K (16 positions x 128) and
+  // V (128 dimensions x 16) are 4 KB contiguous, read by four wave
+  // instructions of 1 KB each with the non-temporal hint (whole cache lines,
+  // streamed once).  raw[i], i < 8: K of page i/4, positions 4(i%4) + lane/16,
+  // piece lane%16; raw[8 + i]: V of page i/4, dimensions 32(i%4) + lane/2,
+  // positions 8(lane%2)..+7.  A page outside the split (pairs past the last,
+  // the missing second page of an odd count) is read through an empty buffer
+  // resource: zeros, no memory traffic, and no branch around the loads.
+  const int pg_last = pe - pb;
+  auto load_pair = [&](int q, u32x4 (&raw)[16]) __attribute__((always_inline)) {
+    const int j0 = 2 * q, j1 = 2 * q + 1;
+    const int phys0 = __builtin_amdgcn_readfirstlane(page_id(min(j0, last)));
+    const int phys1 = __builtin_amdgcn_readfirstlane(page_id(min(j1, last)));
+    const size_t o0 = ((size_t)phys0 * n_kv + g) * 16 * DH, o1 = ((size_t)phys1 * n_kv + g) * 16 * DH;
+    const int n0 = j0 < pg_last ? 16 * DH * 2 : 0, n1 = j1 < pg_last ? 16 * DH * 2 : 0;
+    const auto rk0 = buf_rsrc(kbase + o0, n0), rk1 = buf_rsrc(kbase + o1, n1);
+    const auto rv0 = buf_rsrc(vbase + o0, n0), rv1 = buf_rsrc(vbase + o1, n1);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      raw[i] = buf_load_nt(rk0, i * 1024 + lane * 16);
+      raw[4 + i] = buf_load_nt(rk1, i * 1024 + lane * 16);
+      raw[8 + i] = buf_load_nt(rv0, i * 1024 + lane * 16);
+      raw[12 + i] = buf_load_nt(rv1, i * 1024 + lane * 16);
+    }
+  };
+  // Operand layouts through the wave's LDS region (8 KB, K then V).  K: row
+  // R = 16 page + position (256 bytes), piece p in slot p ^ kswz(R), so the
+  // 16 rows one operand read touches (4 positions x 2 halves x 2 pages) fall
+  // in distinct slots.  V: slot 2 (128 page + dim) + (half ^ bit 3 of dim),
+  // so 16 consecutive dimensions at one half fall in distinct banks.
+  __shared__ u32x4 kvt[NW][512];
+  u32x4 *reg = kvt[wave];
+  auto kswz = [](int R) { return (R & 15) ^ ((R >> 4) << 2); };
+  auto stage = [&](const u32x4 (&raw)[16], u32x4 (&ka)[4], u32x4 (&kb)[4], u32x4 (&vf)[8])
+      __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int R = (i >> 2) * 16 + (i & 3) * 4 + (lane >> 4);
+      reg[R * 16 + ((lane & 15) ^ kswz(R))] = raw[i];
+    }
+    wave_lds_fence();
+    const int RA = kpage * 16 + kpos, RB = RA + 4;
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-      ka[s] = *(const u32x4 *)(kp + s * 32);
-      kb[s] = *(const u32x4 *)(kp + 4 * DH + s * 32);
+      ka[s] = reg[RA * 16 + ((s * 4 + gq) ^ kswz(RA))];
+      kb[s] = reg[RB * 16 + ((s * 4 + gq) ^ kswz(RB))];
     }
+    wave_lds_fence();
 #pragma unroll
-    for (int c = 0; c < 8; ++c) vf[c] = *(const u32x4 *)(vp + c * 16 * 16);
+    for (int i = 0; i < 8; ++i) {
+      const int dim = (i & 3) * 32 + (lane >> 1);
+      reg[((i >> 2) * 128 + dim) * 2 + ((lane & 1) ^ ((dim >> 3) & 1))] = raw[8 + i];
+    }
+    wave_lds_fence();
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      const int dim = r + 16 * c;
+      vf[c] = reg[(vpage * 128 + dim) * 2 + ((gq & 1) ^ ((dim >> 3) & 1))];
+    }
+    wave_lds_fence();
   };
   auto pair = [&](int q, const u32x4 (&ka)[4], const u32x4 (&kb)[4], u32x4 (&vf)[8]) __attribute__((always_inline)) {
     const int pg0 = pb + 2 * q;  // first page of the pair
@@ -194,18 +237,18 @@ __global__ __launch_bounds__(NW * 64) void k_attn_decode_bf16(AttnArgs a) {
       acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vf[c]),
                                                        __builtin_bit_cast(bf16x8, pf), acc[c], 0, 0, 0);
   };
-  // Two register sets: the pair after next loads while this one is multiplied.
-  u32x4 kaA[4], kbA[4], vfA[8], kaB[4], kbB[4], vfB[8];
-  if (wave < npairs) load_pair(wave, kaA, kbA, vfA);
-  // (the scheduling barriers keep each prefetch in front of the multiplies
-  // of the pair already in registers)
-  for (int q = wave; q < npairs; q += 2 * NW) {
-    load_pair(q + NW, kaB, kbB, vfB);
+  // One register set of loaded pages per wave: once a pair is staged into
+  // LDS, the wave's next pair loads while this one is multiplied (eight
+  // waves x 16 KB in flight per workgroup).  The scheduling barrier keeps
+  // the loads in front of the multiplies.
+  u32x4 raw[16];
+  if (wave < npairs) load_pair(wave, raw);
+  for (int q = wave; q < npairs; q += NW) {
+    u32x4 ka[4], kb[4], vf[8];
+    stage(raw, ka, kb, vf);
+    load_pair(q + NW, raw);
     __builtin_amdgcn_sched_barrier(0);
-    pair(q, kaA, kbA, vfA);
-    load_pair(q + 2 * NW, kaA, kbA, vfA);
-    __builtin_amdgcn_sched_barrier(0);
-    if (q + NW < npairs) pair(q + NW, kaB, kbB, vfB);  // uniform over the wave
+    pair(q, ka, kb, vf);
   }
   l_run += __shfl_xor(l_run, 16, 64);
   l_run += __shfl_xor(l_run, 32, 64);

@@ -48,6 +48,29 @@ __device__ __forceinline__ float rows4_max(float x) {
   return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 
+// Buffer resource over `bytes` bytes at p (raw, unswizzled, 32-bit data
+// format): a raw buffer load at an offset >= bytes returns zeros and reads no
+// memory, so a resource of zero bytes turns a wave's loads into no-ops without
+// a branch.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void *p, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, bytes, 0x00020000);
+}
+// 16 bytes at byte offset off, with the non-temporal hint (streamed data,
+// read once).
+__device__ __forceinline__ u32x4 buf_load_nt(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 2));
+}
+
+// Orders a wave's LDS accesses around a hand-over between its own lanes
+// (stores by some lanes, loads of that data by others): the hardware runs a
+// wave's LDS operations in issue order, so only the compiler has to be kept
+// from moving accesses across this point.
+__device__ __forceinline__ void wave_lds_fence() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // Zero the bf16 lanes of v (positions first .. first+7) at positions >= nvalid.
 __device__ __forceinline__ u32x4 mask8(u32x4 v, int first, int nvalid) {
 #pragma unroll

@@ -48,6 +48,15 @@ constexpr int lcm3(int a, int b, int c) {
 // end re-read the last one), and the loop body always runs PD chunks, so the
 // compiler's wait counts stay exact across the loop's back edge.
 //
+// Weight loads: each wave instruction reads eight whole 128-byte row pieces
+// (eight lanes per row) with the non-temporal hint, so every request is a
+// full cache line that is used once and not kept; the wave then moves the
+// pieces into the MFMA operand layout (16 rows x 64 bytes per instruction)
+// through its own LDS region, half a chunk at a time.  Loading the operand
+// layout directly would cover only half of each line per instruction, and
+// the streaming read is slower that way (about 6.3 against 6.9 TB/s for a
+// plain read of the output matrix).
+//
 // Each workgroup starts at its own chunk of the split, (tile * 7) mod chunks,
 // and wraps around: workgroups running at the same time then read different
 // column ranges of their rows instead of all hitting the same few memory
@@ -103,9 +112,19 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
   }
   const int nw = nloc + wave * 16 * RB;             // first row of this wave within the segment
   const int ny = blockIdx.x * ROWS + wave * 16 * RB;  // first output column of this wave
-  const uint16_t *wrow[RB];
+  // weight pointers of the coalesced loads: row block rb, row group j (rows
+  // rb*16 + j*8 + lane/8), 16-byte piece lane%8 of a 128-byte half chunk
+  const int lr8 = lane >> 3, lp8 = lane & 7;
+  const uint16_t *wrow[RB][2];
 #pragma unroll
-  for (int rb = 0; rb < RB; ++rb) wrow[rb] = Wseg + (size_t)min(nw + rb * 16 + r, segrows - 1) * K + kbeg + gq * 8;
+  for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+      wrow[rb][j] = Wseg + (size_t)min(nw + rb * 16 + j * 8 + lr8, segrows - 1) * K + kbeg + lp8 * 8;
+  // the wave's LDS region: RB*16 rows of one half chunk (8 pieces of 16
+  // bytes); piece p of row R sits in slot p ^ (R & 7)
+  __shared__ u32x4 wt[NW][RB * 16 * 8];
+  u32x4 *wreg = wt[wave];
   const uint16_t *xsrc[PPT];
   int xdst[PPT];
 #pragma unroll
@@ -132,12 +151,16 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
 #pragma unroll
     for (int j = 0; j < PPT; ++j) stg[slot][j] = *(const u32x4 *)(xsrc[j] + ko);
   };
+  // a[slot][rb][2h + j]: half h of row group j of row block rb
   auto wload = [&](int slot, int c) {
     const int ko = koff(c);
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-      for (int s = 0; s < 4; ++s) a[slot][rb][s] = *(const u32x4 *)(wrow[rb] + ko + s * 32);
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          a[slot][rb][2 * h + j] = __builtin_nontemporal_load((const u32x4 *)(wrow[rb][j] + ko + h * 64));
   };
   auto xstore = [&](int lds, int slot) {
 #pragma unroll
@@ -152,17 +175,33 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
   auto step = [&](int c, int w, int par, int xc, int xn) {
     const uint16_t *xl = xs[par];
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      u32x4 bx[MB];
-#pragma unroll
-      for (int cb = 0; cb < MB; ++cb) bx[cb] = *(const u32x4 *)(&xl[(cb * 16 + r) * kLdsRow + s * 32 + gq * 8]);
+    for (int h = 0; h < 2; ++h) {
+      // half h of the wave's weight rows into its LDS region (the reads of
+      // the previous half were issued before: LDS operations of a wave run
+      // in order)
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-        for (int cb = 0; cb < MB; ++cb)
-          acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a[w][rb][s]),
-                                                                __builtin_bit_cast(bf16x8, bx[cb]), acc[rb][cb], 0, 0,
-                                                                0);
+        for (int j = 0; j < 2; ++j) wreg[(rb * 16 + j * 8 + lr8) * 8 + (lp8 ^ lr8)] = a[w][rb][2 * h + j];
+      wave_lds_fence();
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        const int s = 2 * h + s2;
+        u32x4 bx[MB], wf[RB];
+#pragma unroll
+        for (int cb = 0; cb < MB; ++cb) bx[cb] = *(const u32x4 *)(&xl[(cb * 16 + r) * kLdsRow + s * 32 + gq * 8]);
+        // operand of row block rb: row rb*16 + r, piece 4*s2 + gq of the half
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) wf[rb] = wreg[(rb * 16 + r) * 8 + ((4 * s2 + gq) ^ (r & 7))];
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+          for (int cb = 0; cb < MB; ++cb)
+            acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wf[rb]),
+                                                                  __builtin_bit_cast(bf16x8, bx[cb]), acc[rb][cb], 0,
+                                                                  0, 0);
+      }
+      wave_lds_fence();
     }
     xload(xc, c + XA);
     wload(w, c + PD);
