@@ -63,10 +63,13 @@ constexpr int lcm3(int a, int b, int c) {
 // channels (row strides are powers of two).  The order is a function of the
 // row tile and the split only.
 //
-// GLU: the workgroup owns NW/2*16*RB rows of segment 0 (gate, the first
-// half of the waves) and the same rows of segment 1 (up, the second half);
-// instead of storing Y it finishes the MLP intermediate in its epilogue (see
-// GluEpi).
+// GLU (RB = 1): each wave owns eight rows of segment 0 (gate) and the same
+// eight rows of segment 1 (up) as one 16-row MFMA block, so a lane's
+// accumulators for gate row n sit four lanes-groups away from those of up
+// row n (lane + 32); the workgroup owns NW*8 gate rows.  Instead of storing
+// Y the epilogue finishes the MLP intermediate in registers (see GluEpi):
+// the branch rows' coupling partner, the primary row of the same sequence,
+// is held by the same lane.
 template <int MB, int RB, int PD, int NW, bool GLU = false, int XA = 2>
 __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const uint16_t *__restrict__ X, int ldx,
                                                        int M, float *__restrict__ Y, int ldy,
@@ -92,14 +95,10 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
   int nloc = blockIdx.x * ROWS;
   const uint16_t *Wseg = (const uint16_t *)segs.w[0];
   int segrows = segs.rows[0];
-  constexpr int HW = NW / 2, TC = HW * 16 * RB;  // GLU: waves per half, gate (= up) rows per tile
+  static_assert(!GLU || RB == 1, "GLU waves own one 8 + 8 row block");
+  const int g0 = blockIdx.x * NW * 8 + wave * 8;  // GLU: first gate (= up) row of this wave
   if (GLU) {
-    static_assert(!GLU || NW % 2 == 0, "GLU tiles split the waves in two halves");
-    nloc = blockIdx.x * TC - (wave >= HW ? TC : 0);  // + wave*16*RB below: rows (wave%HW)*16*RB of the tile
-    if (wave >= HW) {
-      Wseg = (const uint16_t *)segs.w[1];
-      segrows = segs.rows[1];
-    }
+    // (no segment walk: rows come from w[0] and w[1] below)
   } else if (nloc >= segs.rows[0] && segs.rows[1] > 0) {
     nloc -= segs.rows[0];
     Wseg = (const uint16_t *)segs.w[1];
@@ -120,7 +119,8 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
   for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
     for (int j = 0; j < 2; ++j)
-      wrow[rb][j] = Wseg + (size_t)min(nw + rb * 16 + j * 8 + lr8, segrows - 1) * K + kbeg + lp8 * 8;
+      wrow[rb][j] = GLU ? (const uint16_t *)segs.w[j] + (size_t)min(g0 + lr8, segs.rows[0] - 1) * K + kbeg + lp8 * 8
+                        : Wseg + (size_t)min(nw + rb * 16 + j * 8 + lr8, segrows - 1) * K + kbeg + lp8 * 8;
   // the wave's LDS region: RB*16 rows of one half chunk (8 pieces of 16
   // bytes); piece p of row R sits in slot p ^ (R & 7)
   __shared__ u32x4 wt[NW][RB * 16 * 8];
@@ -229,55 +229,62 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
     if (c0 + u < nch) step(c0 + u, u % PD, u & 1, u % XA, (u + 1) % XA);
   // lane holds D[n = rb*16 + 4*gq + i][m = cb*16 + r]: Y[m][n .. n+3]
   if constexpr (GLU) {
-    // hb[m][c]: the tile's TC gate/up columns c for activation row m
-    // (reuses the activation slots: the loop's last barrier has passed)
-    constexpr int HC = TC + 1;
-    static_assert(XR * HC * 4 <= (int)sizeof(xs), "GLU staging exceeds the activation slots");
-    float *hb = (float *)&xs[0][0];
-    const int c0 = (wave % HW) * 16 * RB;
-    if (wave >= HW)
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-        for (int cb = 0; cb < MB; ++cb)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) hb[(cb * 16 + r) * HC + c0 + rb * 16 + 4 * gq + i] = acc[rb][cb][i];
-    __syncthreads();
-    if (wave < HW)
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-        for (int cb = 0; cb < MB; ++cb)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int idx = (cb * 16 + r) * HC + c0 + rb * 16 + 4 * gq + i;
-            const float g = acc[rb][cb][i];
-            hb[idx] = g / (1.0f + expf(-g)) * hb[idx];
-          }
-    __syncthreads();
+    // lane (r, gq) holds D[n = 4gq + i][m = cb*16 + r]: gate rows n < 8
+    // (gq < 2), up rows n >= 8 (gq >= 2, the up value of gate row n sits in
+    // lane + 32).  H = SiLU(gate) * up (Eq. (13)); branch rows add b * H1 of
+    // their sequence's primary row (Eq. (14)), block cb - p*Bp/16 of the
+    // same lane (primary and branches in one tile, M <= 16*MB, m0 = 0) or the
+    // retained H1.
     const int Bp = ep.rows.Bp, row0 = ep.rows.p0 * Bp;
-    for (int e = t; e < XR * TC; e += NW * 64) {
-      const int mm = e / TC, cc = e % TC;
-      const int gm = m0 + mm;  // row of this call (relative to its first row)
+    float h[MB][4];
+#pragma unroll
+    for (int cb = 0; cb < MB; ++cb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float g = acc[0][cb][i];
+        const float u = __shfl_xor(g, 32, 64);
+        h[cb][i] = g / (1.0f + expf(-g)) * u;
+      }
+    if (gq >= 2) return;
+    const int n = g0 + 4 * gq;  // this lane's four columns n .. n+3 of H
+    if (n >= ep.f) return;
+#pragma unroll
+    for (int cb = 0; cb < MB; ++cb) {
+      const int gm = m0 + cb * 16 + r;  // row of this call (relative to its first row)
       if (gm >= M) continue;
       const int path = ep.rows.p0 + gm / Bp, b = gm % Bp;
       if (b >= ep.rows.B) continue;
-      const int n = blockIdx.x * TC + cc;
-      const float h = hb[mm * HC + cc];
-      float out;
+      float o[4];
       if (path == 0) {
-        out = h;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[i] = h[cb][i];
         const Retain &rt = ep.ret;
         if (rt.ptr && (rt.src_row < 0 || rt.src_row == b))
-          rt.ptr[(size_t)(rt.src_row < 0 ? b : rt.dst_row) * ep.f + n] = h;
+          *(float4 *)&rt.ptr[(size_t)(rt.src_row < 0 ? b : rt.dst_row) * ep.f + n] = make_float4(o[0], o[1], o[2], o[3]);
       } else {
-        // H2~ = H2 + b * H1 for every branch: the primary row of the same
-        // sequence is this tile's row b (primary and branches in one tile,
-        // M <= 16*MB, m0 = 0) or comes from the retained H1
-        const float h1 = ep.rows.p0 == 0 ? hb[b * HC + cc] : ep.H1_in[(size_t)b * ep.f + n];
-        out = h + ep.bvec[n] * h1;
+        const float4 bv = *(const float4 *)&ep.bvec[n];
+        float h1[4];
+        if (ep.rows.p0 == 0) {
+          // the primary row b sits in block cb - path*Bp/16 of this lane
+          const int cb1 = cb - path * (Bp / 16);
+#pragma unroll
+          for (int c2 = 0; c2 < MB; ++c2)
+            if (c2 == cb1)
+#pragma unroll
+              for (int i = 0; i < 4; ++i) h1[i] = h[c2][i];
+        } else {
+          const float4 x = *(const float4 *)&ep.H1_in[(size_t)b * ep.f + n];
+          h1[0] = x.x; h1[1] = x.y; h1[2] = x.z; h1[3] = x.w;
+        }
+        o[0] = h[cb][0] + bv.x * h1[0];
+        o[1] = h[cb][1] + bv.y * h1[1];
+        o[2] = h[cb][2] + bv.z * h1[2];
+        o[3] = h[cb][3] + bv.w * h1[3];
       }
-      ep.Xh[(size_t)(row0 + gm) * ep.ldh + n] = f2bf(out);
+      uint2 pk;
+      pk.x = pack2(o[0], o[1]);
+      pk.y = pack2(o[2], o[3]);
+      *(uint2 *)&ep.Xh[(size_t)(row0 + gm) * ep.ldh + n] = pk;
     }
     return;
   }
@@ -342,14 +349,47 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
       o[2] = a2;
     }
   }
+  // Output rows are written in whole 128-byte lines: a lane's accumulators
+  // hold four columns of one row, so one store instruction would cover 16
+  // rows x 64 bytes; the tile goes through LDS first (rows padded by four
+  // floats, so the 16 rows of one accumulator write fall in distinct banks).
   float *Ys = Y + (long long)split * y_split_stride;
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb)
+  if constexpr (RB >= 2) {
+    // per wave: 16 rows x RB*16 columns at a time, in its own LDS region
+    constexpr int WC = RB * 16, PITCH = WC + 4, LPR = WC / 4;  // columns, pitch, lanes per row
+    static_assert(GLU || 16 * PITCH * 4 <= (int)sizeof(wt[0]), "output staging exceeds the wave's region");
+    float *ost = (float *)&wt[wave][0];
 #pragma unroll
     for (int cb = 0; cb < MB; ++cb) {
-      const int m = m0 + cb * 16 + r;
-      if (m < M && rvalid[rb]) *(floatx4 *)(Ys + (size_t)m * ldy + ny + rb * 16 + gq * 4) = acc[rb][cb];
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) *(floatx4 *)&ost[r * PITCH + rb * 16 + gq * 4] = acc[rb][cb];
+      wave_lds_fence();
+#pragma unroll
+      for (int j = 0; j < 16 * LPR / 64; ++j) {
+        const int row = j * (64 / LPR) + lane / LPR, col = (lane % LPR) * 4;
+        const int m = m0 + cb * 16 + row;
+        const floatx4 v = *(const floatx4 *)&ost[row * PITCH + col];
+        if (m < M && rvalid[col >> 4]) *(floatx4 *)(Ys + (size_t)m * ldy + ny + col) = v;
+      }
+      wave_lds_fence();
     }
+  } else {
+    // per workgroup: the XR x ROWS tile in the activation slots (free after
+    // the loop's last barrier), then each row stored by ROWS/4 threads
+    constexpr int PITCH = ROWS + 4, TPR = ROWS / 4;
+    static_assert(GLU || XR * PITCH * 4 <= (int)sizeof(xs), "output staging exceeds the activation slots");
+    float *ost = (float *)&xs[0][0];
+#pragma unroll
+    for (int cb = 0; cb < MB; ++cb) *(floatx4 *)&ost[(cb * 16 + r) * PITCH + wave * 16 + gq * 4] = acc[0][cb];
+    __syncthreads();
+    const int nt0 = blockIdx.x * ROWS;
+    for (int e = t; e < XR * TPR; e += NW * 64) {
+      const int row = e / TPR, col = (e % TPR) * 4;
+      const int m = m0 + row;
+      if (m < M && nloc + col < segrows)
+        *(floatx4 *)(Ys + (size_t)m * ldy + nt0 + col) = *(const floatx4 *)&ost[row * PITCH + col];
+    }
+  }
 }
 
 // fp32: 64 output columns x 16 rows per workgroup, reduction staged through LDS.
@@ -419,9 +459,11 @@ GemmConfig gemm_config(int n_full, int K, int dtype, int seg_gran, int max_rows)
     // thin matrices: split the reduction so that at most one workgroup per
     // compute unit runs (a second round of workgroups costs a whole round);
     // the fp32 slabs of up to max_rows stacked rows never exceed the weight
-    // bytes, and every split keeps at least one chunk.  Tiles of 64 rows
-    // (4 waves) unless 128-row tiles (8 waves) keep more compute units busy;
-    // fewer splits also mean fewer slabs for the consumer to add.
+    // bytes, and every split keeps at least one chunk.  Tiles of 128 rows
+    // (8 waves) unless 64-row tiles (4 waves) keep more compute units busy:
+    // with one workgroup per unit, eight waves keep twice the weight bytes in
+    // flight, and a unit's share of a thin matrix is small enough for its
+    // read to be bound by load latency rather than bandwidth.
     const int nc = K / kChunk;
     auto splits = [&](int tiles) {
       int S = 256 / tiles;
@@ -430,7 +472,7 @@ GemmConfig gemm_config(int n_full, int K, int dtype, int seg_gran, int max_rows)
     };
     const int t4 = std::max(1, n_full / 64), t8 = std::max(1, n_full / 128);
     const int s4 = splits(t4), s8 = splits(t8);
-    if (seg_gran % 128 == 0 && t8 * s8 > t4 * s4)
+    if (seg_gran % 128 == 0 && t8 * s8 >= t4 * s4)
       g = GemmConfig{1, 1, s8, 8};
     else
       g = GemmConfig{1, 2, s4, 4};
@@ -458,7 +500,7 @@ void launch_mb(const GemmConfig &g, dim3 grid, hipStream_t st, const WSegs &segs
 template <int MB>
 void launch_glu_mb(dim3 grid, hipStream_t st, const WSegs &segs, int K, const uint16_t *X, int ldx, int M,
                    const GluEpi &ep) {
-  hipLaunchKernelGGL((k_gemm_bf16<MB, 1, 1, 8, true>), grid, dim3(512), 0, st, segs, K, X, ldx, M, nullptr, 0, 0LL,
+  hipLaunchKernelGGL((k_gemm_bf16<MB, 1, 2, 8, true>), grid, dim3(512), 0, st, segs, K, X, ldx, M, nullptr, 0, 0LL,
                      nullptr, ep);
 }
 }  // namespace
@@ -471,8 +513,9 @@ int gemm_stats_tiles(int N, const GemmConfig &g, int dtype) {
   return (dtype == 1 && g.S == 1) ? (N + gemm_rows_per_wg(g) - 1) / gemm_rows_per_wg(g) : 0;
 }
 
-// Tiles of 64 gate + 64 up rows; enough of them to fill the chip, and a
-// branch row's primary partner in the same activation tile (M <= 128).
+// Tiles of 64 gate + 64 up rows (eight waves of 8 + 8); enough of them to
+// fill the chip, and a branch row's primary partner in the same activation
+// tile (M <= 128).
 bool gemm_glu_ok(int f, int M, int np, int dtype) {
   return dtype == 1 && f % 64 == 0 && f / 64 >= 192 && (np == 1 || M <= 128);
 }
