@@ -256,7 +256,6 @@ struct MoeGemm {
   const int *counts, *offsets, *arow;
   void *Y;  // gate/up: [A][N] bf16 intermediates; down: [A][N] fp32 outputs
   int ldy;
-  int mtiles;
 };
 struct MoeCombine {
   Rows rows;

@@ -161,119 +161,98 @@ __global__ __launch_bounds__(64) void k_moe_topk(MoeRoute a) {
   }
 }
 
-// Entry q of the active rows' selections -> (row, slot j); padding slots
-// j >= k carry expert -1.
-__device__ __forceinline__ int moe_entry(const MoeDispatch &a, int q, int &row, int &j) {
-  const int B = a.rows.B, n = a.rows.np * B * 8;
-  const int pp = q / (B * 8), rem = q % (B * 8), b = rem / 8;
-  j = rem % 8;
-  row = prow(a.rows, a.rows.p0 + pp, b);
-  const int k = (a.rows.p0 + pp) == 0 ? a.k1 : a.k2;
-  return (q < n && j < k) ? a.idx[(size_t)row * 8 + j] : -1;
-}
-
 // Expert-grouped order as a stable counting sort of the assignments
-// (path, b, slot) by expert, for up to 64 chunks of 64 entries (one
-// workgroup).  A lane's rank among equal experts of its chunk comes from a
-// loop over the wave's lanes (v_readlane broadcasts); per-chunk counts are
-// prefix-summed per expert in chunk order.
-__global__ __launch_bounds__(256) void k_moe_dispatch(MoeDispatch a) {
-  constexpr int MAXC = 64;
-  __shared__ int ccnt[MAXC][257];
-  __shared__ int offs[257];
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int n = a.rows.np * a.rows.B * 8;
-  const int nch = (n + 63) / 64;
-  for (int q = t; q < nch * 257; q += blockDim.x) (&ccnt[0][0])[q] = 0;
-  __syncthreads();
-  for (int c = wave; c < nch; c += 4) {
-    int row, j;
-    const int e = moe_entry(a, c * 64 + lane, row, j);
-    int before = 0, total = 0;
-    for (int o = 0; o < 64; ++o) {
-      const int v = __builtin_amdgcn_readlane(e, o);  // uniform source lane: no LDS round trip
-      if (v == e) {
-        ++total;
-        if (o < lane) ++before;
-      }
+// (path, b, slot) by expert.  A row selects an expert at most once, so the
+// assignments of expert e, in order, are the active rows that selected e, in
+// row order.  Thread (e, c) owns expert e and the c-th of RC equal ranges of
+// the active rows (1024 threads = RC x E rounded up to a power of two): it
+// counts its range's selections of e, the counts are prefix-summed per
+// expert over the ranges and across experts (one wave scan), and the thread
+// then writes its range's positions.  Fixed order, no atomics.
+__global__ __launch_bounds__(1024) void k_moe_dispatch(MoeDispatch a) {
+  __shared__ int cnt[1024];
+  __shared__ int eoff[256];
+  const int t = threadIdx.x, lane = t & 63;
+  const int E = a.E;
+  const int epad = E <= 1 ? 1 : 1 << (32 - __clz(E - 1));
+  const int RC = 1024 / epad;
+  const int e = t % epad, c = t / epad;
+  const int B = a.rows.B, R = a.rows.np * B;
+  const int r0 = c * R / RC, r1 = (c + 1) * R / RC;
+  // slot j of active row q, or -1 past the path's k (all eight slots of a
+  // row in two 16-byte loads, so a range's loads are in flight together)
+  auto sel = [&](int q, int (&v)[8]) {
+    const int path = a.rows.p0 + q / B;
+    const int k = path == 0 ? a.k1 : a.k2;
+    const int4 *p = (const int4 *)(a.idx + (size_t)prow(a.rows, path, q % B) * 8);
+    const int4 x = p[0], y = p[1];
+    v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w; v[4] = y.x; v[5] = y.y; v[6] = y.z; v[7] = y.w;
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (j >= k) v[j] = -1;
+    return prow(a.rows, path, q % B);
+  };
+  int n = 0;
+  if (e < E)
+    for (int q = r0; q < r1; ++q) {
+      int v[8];
+      sel(q, v);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) n += v[j] == e;
     }
-    if (e >= 0 && before == 0) ccnt[c][e] = total;
-  }
+  cnt[t] = n;
   __syncthreads();
-  if (t < a.E) {
+  if (t < E) {
     int acc = 0;
-    for (int c = 0; c < nch; ++c) {
-      const int v = ccnt[c][t];
-      ccnt[c][t] = acc;
+    for (int cc = 0; cc < RC; ++cc) {
+      const int v = cnt[cc * epad + t];
+      cnt[cc * epad + t] = acc;
       acc += v;
     }
-    offs[t] = acc;  // count for now
+    a.counts[t] = acc;
+    eoff[t] = acc;
   }
   __syncthreads();
-  if (t == 0) {
-    int acc = 0;
-    for (int e = 0; e < a.E; ++e) {
-      const int ce = offs[e];
-      a.counts[e] = ce;
-      a.offsets[e] = acc;
-      offs[e] = acc;
-      acc += ce;
+  if (t < 64) {
+    // exclusive scan over experts: lane l sums experts 4l..4l+3
+    int v[4], s = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int ee = 4 * lane + i;
+      v[i] = ee < E ? eoff[ee] : 0;
+      s += v[i];
     }
-    a.offsets[a.E] = acc;
-  }
-  __syncthreads();
-  for (int c = wave; c < nch; c += 4) {
-    int row, j;
-    const int e = moe_entry(a, c * 64 + lane, row, j);
-    int before = 0;
-    for (int o = 0; o < 64; ++o) {
-      const int v = __builtin_amdgcn_readlane(e, o);
-      if (v == e && o < lane) ++before;
+    int incl = s;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int u = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += u;
     }
-    if (e >= 0) {
-      const int pos = offs[e] + ccnt[c][e] + before;
-      a.arow[pos] = row;
-      a.aslot[(size_t)row * 8 + j] = pos;
-    }
-  }
-}
-
-// Same order for more than 4096 entries (long prompts): thread e scans all
-// entries in order.
-__global__ __launch_bounds__(256) void k_moe_dispatch_scan(MoeDispatch a) {
-  __shared__ int cnt[256];
-  const int e = threadIdx.x;
-  const int n = a.rows.np * a.rows.B * 8;
-  int c = 0;
-  if (e < a.E) {
-    for (int q = 0; q < n; ++q) {
-      int row, j;
-      if (moe_entry(a, q, row, j) == e) ++c;
-    }
-    cnt[e] = c;
-  }
-  __syncthreads();
-  if (e == 0) {
-    int acc = 0;
-    for (int i = 0; i < a.E; ++i) {
-      a.offsets[i] = acc;
-      a.counts[i] = cnt[i];
-      const int ci = cnt[i];
-      cnt[i] = acc;
-      acc += ci;
-    }
-    a.offsets[a.E] = acc;
-  }
-  __syncthreads();
-  if (e < a.E) {
-    int pos = cnt[e];
-    for (int q = 0; q < n; ++q) {
-      int row, j;
-      if (moe_entry(a, q, row, j) == e) {
-        a.arow[pos] = row;
-        a.aslot[(size_t)row * 8 + j] = pos;
-        ++pos;
+    int off = incl - s;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int ee = 4 * lane + i;
+      if (ee < E) {
+        eoff[ee] = off;
+        a.offsets[ee] = off;
       }
+      off += v[i];
+    }
+    if (lane == 63) a.offsets[E] = incl;
+  }
+  __syncthreads();
+  if (e < E) {
+    int pos = eoff[e] + cnt[t];
+    for (int q = r0; q < r1; ++q) {
+      int v[8];
+      const int row = sel(q, v);
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (v[j] == e) {
+          a.arow[pos] = row;
+          a.aslot[(size_t)row * 8 + j] = pos;
+          ++pos;
+        }
     }
   }
 }
@@ -284,7 +263,14 @@ constexpr int kLdsRow = kChunk + 8;
 // Expert projections over gathered rows.  GATEUP: workgroup = (expert,
 // 64 hidden units); wave w owns hidden units h0+16w..+15 with row block 0 =
 // gate rows and row block 1 = up rows, so SwiGLU is lane-local.  DOWN:
-// workgroup = (expert, 64 output columns), wave w owns 16 of them.
+// workgroup = (expert, 64 output columns), wave w owns 16 of them.  The
+// workgroup takes all rows of its expert in passes of 16*MB (one pass unless
+// the expert is crowded; a further pass reads its weights again); an
+// untouched expert's workgroups return before any weight read.
+//
+// Weight loads as in the dense projections: whole 128-byte row pieces with
+// the non-temporal hint (eight rows per wave instruction), moved into the
+// MFMA operand layout through the wave's LDS region half a chunk at a time.
 template <int MB, bool GATEUP>
 __global__ __launch_bounds__(256) void k_moe_gemm(MoeGemm a) {
   constexpr int RB = GATEUP ? 2 : 1;
@@ -294,37 +280,35 @@ __global__ __launch_bounds__(256) void k_moe_gemm(MoeGemm a) {
   constexpr int PPT = (PIECES + 255) / 256;
   __shared__ uint16_t xs[PD][XR * kLdsRow];
   __shared__ int rows_s[XR];
+  __shared__ u32x4 wt[4][RB * 16 * 8];
   const int tiles = a.N / 64;
   const int e = blockIdx.x / tiles, tile = blockIdx.x % tiles;
   const int Me = a.counts[e];
-  const int m0 = blockIdx.z * XR;
-  if (m0 >= Me) return;  // untouched expert (or beyond its rows): no weight read
+  if (Me <= 0) return;  // untouched expert: no weight read
   const int base = a.offsets[e];
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6, r = lane & 15, gq = lane >> 4;
   const int K = a.K, nch = K / kChunk;
-  if (t < XR) rows_s[t] = (m0 + t < Me) ? (GATEUP ? a.arow[base + m0 + t] : base + m0 + t) : -1;
-  const int nb = (min(Me - m0, XR) + 15) / 16;  // live activation blocks
   const int n0 = tile * 64 + wave * 16;
-  const uint16_t *wrow[RB];
-  if (GATEUP) {
-    wrow[0] = (const uint16_t *)a.W0 + ((size_t)e * a.N + n0 + r) * K + gq * 8;
-    wrow[RB - 1] = (const uint16_t *)a.W1 + ((size_t)e * a.N + n0 + r) * K + gq * 8;
-  } else {
-    wrow[0] = (const uint16_t *)a.W0 + ((size_t)e * a.N + n0 + r) * K + gq * 8;
-  }
-  __syncthreads();
-  floatx4 acc[RB][MB];
+  // coalesced weight loads: row block rb, row group j (rows j*8 + lane/8 of
+  // the block), 16-byte piece lane%8 of a 128-byte half chunk
+  const int lr8 = lane >> 3, lp8 = lane & 7;
+  const uint16_t *wrow[RB][2];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-    for (int cb = 0; cb < MB; ++cb) acc[rb][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < 2; ++j)
+      wrow[rb][j] = (const uint16_t *)(rb == 0 ? a.W0 : a.W1) + ((size_t)e * a.N + n0 + j * 8 + lr8) * K + lp8 * 8;
+  u32x4 *wreg = wt[wave];
   u32x4 w[PD][RB][4];
   u32x4 stage[PPT];
   auto wload = [&](int slot, int c) {
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-      for (int s = 0; s < 4; ++s) w[slot][rb][s] = *(const u32x4 *)(wrow[rb] + c * kChunk + s * 32);
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          w[slot][rb][2 * h + j] = __builtin_nontemporal_load((const u32x4 *)(wrow[rb][j] + c * kChunk + h * 64));
   };
   auto xload = [&](int c) {
 #pragma unroll
@@ -343,59 +327,83 @@ __global__ __launch_bounds__(256) void k_moe_gemm(MoeGemm a) {
       if (p < PIECES) *(u32x4 *)(&xs[slot][(p >> 4) * kLdsRow + (p & 15) * 8]) = stage[j];
     }
   };
+  for (int m0 = 0; m0 < Me; m0 += XR) {
+    if (m0 > 0) __syncthreads();  // the previous pass is done with rows_s and xs
+    if (t < XR) rows_s[t] = (m0 + t < Me) ? (GATEUP ? a.arow[base + m0 + t] : base + m0 + t) : -1;
+    const int nb = (min(Me - m0, XR) + 15) / 16;  // live activation blocks
+    __syncthreads();
+    floatx4 acc[RB][MB];
 #pragma unroll
-  for (int u = 0; u < PD; ++u)
-    if (u < nch) {
-      xload(u);
-      xstore(u);
-      wload(u, u);
-    }
-  __syncthreads();
-  for (int c0 = 0; c0 < nch; c0 += PD) {
+    for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-    for (int u = 0; u < PD; ++u) {
-      const int c = c0 + u;
-      if (c < nch) {
-        const bool more = c + PD < nch;
-        if (more) xload(c + PD);
+      for (int cb = 0; cb < MB; ++cb) acc[rb][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int s = 0; s < 4; ++s) {
+    for (int u = 0; u < PD; ++u)
+      if (u < nch) {
+        xload(u);
+        xstore(u);
+        wload(u, u);
+      }
+    __syncthreads();
+    for (int c0 = 0; c0 < nch; c0 += PD) {
 #pragma unroll
-          for (int cb = 0; cb < MB; ++cb) {
-            if (cb < nb) {
-              const u32x4 bx = *(const u32x4 *)(&xs[u][(cb * 16 + r) * kLdsRow + s * 32 + gq * 8]);
+      for (int u = 0; u < PD; ++u) {
+        const int c = c0 + u;
+        if (c < nch) {
+          const bool more = c + PD < nch;
+          if (more) xload(c + PD);
 #pragma unroll
-              for (int rb = 0; rb < RB; ++rb)
-                acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                    __builtin_bit_cast(bf16x8, w[u][rb][s]), __builtin_bit_cast(bf16x8, bx), acc[rb][cb], 0, 0, 0);
+          for (int h = 0; h < 2; ++h) {
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+              for (int j = 0; j < 2; ++j) wreg[(rb * 16 + j * 8 + lr8) * 8 + (lp8 ^ lr8)] = w[u][rb][2 * h + j];
+            wave_lds_fence();
+#pragma unroll
+            for (int s2 = 0; s2 < 2; ++s2) {
+              const int s = 2 * h + s2;
+              u32x4 wf[RB];
+#pragma unroll
+              for (int rb = 0; rb < RB; ++rb) wf[rb] = wreg[(rb * 16 + r) * 8 + ((4 * s2 + gq) ^ (r & 7))];
+#pragma unroll
+              for (int cb = 0; cb < MB; ++cb) {
+                if (cb < nb) {
+                  const u32x4 bx = *(const u32x4 *)(&xs[u][(cb * 16 + r) * kLdsRow + s * 32 + gq * 8]);
+#pragma unroll
+                  for (int rb = 0; rb < RB; ++rb)
+                    acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        __builtin_bit_cast(bf16x8, wf[rb]), __builtin_bit_cast(bf16x8, bx), acc[rb][cb], 0, 0, 0);
+                }
+              }
             }
+            wave_lds_fence();
           }
+          if (more) wload(u, c + PD);
+          __syncthreads();
+          if (more) xstore(u);
         }
-        if (more) wload(u, c + PD);
-        __syncthreads();
-        if (more) xstore(u);
       }
     }
-  }
-  // lane holds D[n = n0 + 4gq + i][m = m0 + cb*16 + r]
+    // lane holds D[n = n0 + 4gq + i][m = m0 + cb*16 + r]
 #pragma unroll
-  for (int cb = 0; cb < MB; ++cb) {
-    const int m = m0 + cb * 16 + r;
-    if (cb >= nb || m >= Me) continue;
-    const size_t orow = (size_t)(base + m);
-    if (GATEUP) {
-      uint16_t h[4];
+    for (int cb = 0; cb < MB; ++cb) {
+      const int m = m0 + cb * 16 + r;
+      if (cb >= nb || m >= Me) continue;
+      const size_t orow = (size_t)(base + m);
+      if (GATEUP) {
+        uint16_t h[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float g = acc[0][cb][i], up = acc[RB - 1][cb][i];
-        h[i] = f2bf(g / (1.0f + expf(-g)) * up);
+        for (int i = 0; i < 4; ++i) {
+          const float g = acc[0][cb][i], up = acc[RB - 1][cb][i];
+          h[i] = f2bf(g / (1.0f + expf(-g)) * up);
+        }
+        uint2 v;
+        v.x = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
+        v.y = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
+        *(uint2 *)((uint16_t *)a.Y + orow * a.ldy + n0 + gq * 4) = v;
+      } else {
+        *(floatx4 *)((float *)a.Y + orow * a.ldy + n0 + gq * 4) = acc[0][cb];
       }
-      uint2 v;
-      v.x = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
-      v.y = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
-      *(uint2 *)((uint16_t *)a.Y + orow * a.ldy + n0 + gq * 4) = v;
-    } else {
-      *(floatx4 *)((float *)a.Y + orow * a.ldy + n0 + gq * 4) = acc[0][cb];
     }
   }
 }
@@ -526,7 +534,7 @@ __global__ void k_moe_combine(MoeCombine a) {
 
 template <bool GATEUP>
 hipError_t launch_moe_gemm_t(const MoeGemm &a, int MB, hipStream_t st) {
-  dim3 grid(a.E * (a.N / 64), 1, a.mtiles);
+  dim3 grid(a.E * (a.N / 64), 1, 1);
   switch (MB) {
     case 1: hipLaunchKernelGGL((k_moe_gemm<1, GATEUP>), grid, dim3(256), 0, st, a); break;
     default: hipLaunchKernelGGL((k_moe_gemm<2, GATEUP>), grid, dim3(256), 0, st, a); break;
@@ -543,20 +551,16 @@ hipError_t launch_moe_route(const MoeRoute &a, hipStream_t st) {
 }
 
 hipError_t launch_moe_dispatch(const MoeDispatch &a, hipStream_t st) {
-  if (a.rows.np * a.rows.B * 8 <= 64 * 64)
-    hipLaunchKernelGGL(k_moe_dispatch, dim3(1), dim3(256), 0, st, a);
-  else
-    hipLaunchKernelGGL(k_moe_dispatch_scan, dim3(1), dim3(256), 0, st, a);
+  if (a.E < 1 || a.E > 256) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_moe_dispatch, dim3(1), dim3(1024), 0, st, a);
   return hipGetLastError();
 }
 
-// 32-row activation tiles: an expert usually gets a handful of rows; the
-// rare crowded expert takes more tiles (its weights are then read again).
+// 32-row activation passes: an expert usually gets a handful of rows; the
+// rare crowded expert takes more passes (its weights are then read again).
 hipError_t launch_moe_gemm(const MoeGemm &a, bool gateup, int max_rows, hipStream_t st) {
   const int MB = max_rows > 16 ? 2 : 1;
-  MoeGemm b = a;
-  b.mtiles = (max_rows + 16 * MB - 1) / (16 * MB);
-  return gateup ? launch_moe_gemm_t<true>(b, MB, st) : launch_moe_gemm_t<false>(b, MB, st);
+  return gateup ? launch_moe_gemm_t<true>(a, MB, st) : launch_moe_gemm_t<false>(a, MB, st);
 }
 
 hipError_t launch_moe_combine(const MoeCombine &a, int dtype, hipStream_t st) {
