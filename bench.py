@@ -21,7 +21,7 @@ kernel's launch time and fraction of the HBM peak, the roofline of the
 dominant kernel (the output-matrix projection: its weight bytes over its
 event-timed launch), and the CPU oracle timed per mode on a bounded sample.
 
-    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--no-cpu-baseline]
+    python bench.py [--gpus 1] [--steps 200] [--warmup 50] [--no-cpu-baseline]
 """
 import argparse
 import json
@@ -412,8 +412,10 @@ def time_full24(steps):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    # the GPU's clocks settle over the first few tens of steps: warm up long
+    # enough that the timed block sees the steady state (0.4 ms per step)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=8.0,
                     help="minimum CPU time of the oracle baseline per mode (whole steps)")
