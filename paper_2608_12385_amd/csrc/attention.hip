@@ -55,7 +55,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
   int pb = 0, pe = npages;
   if (SINGLE && npages > 1024) return;  // excluded by the host
   if (!SINGLE && !split_range(npages, a.pages_per_split, split, &pb, &pe)) return;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane & 15, gq = lane >> 4;
   const int n_kv = a.kv.n_kv;
   const int G = a.n_q / n_kv;
@@ -66,10 +66,15 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
   const int *ptab = a.kv.page_table + (size_t)b * a.kv.mpps;
   __shared__ int pid_s[SINGLE ? 1024 : 1];
   int myid0 = 0, myid1 = 0;
-  if constexpr (SINGLE) {
-    for (int i = threadIdx.x; i < npages; i += NW * 64) pid_s[i] = ptab[i];
-    __syncthreads();
-  } else {
+  u32x4 qf[4];
+  // Fused finish of the QKV projection (single mode, a.fused): the workgroup
+  // turns the projection's split-K slabs into its query rows (qs) and the
+  // primary's new cache entry of KV head g, with the slabs added in split
+  // order and the same rope_pair / couple as k_qkv_finish, so the bits equal
+  // the unfused path's.
+  constexpr int QLD = DH + 4;  // row pitch of qs (floats): rows start on different banks
+  __shared__ float qs[SINGLE ? 16 : 1][SINGLE ? QLD : 1];
+  if constexpr (!SINGLE) {
     myid0 = (pb + lane < pe) ? ptab[pb + lane] : 0;
     myid1 = (pb + 64 + lane < pe) ? ptab[pb + 64 + lane] : 0;
   }
@@ -82,8 +87,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
   // Rows past the group's queries read row 0 and are zeroed: all eight
   // loads are issued at once (a load guarded per element compiles to a
   // branch and a full wait each, 32 round trips before the first page).
-  u32x4 qf[4];
-  {
+  if (!(SINGLE && a.fused)) {
     const bool valid = r < nrows;
     const int path = a.rows.p0 + (valid ? r / G : 0);
     const int head = g * G + (valid ? r % G : 0);
@@ -126,12 +130,13 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
   // the missing second page of an odd count) is read through an empty buffer
   // resource: zeros, no memory traffic, and no branch around the loads.
   const int pg_last = pe - pb;
-  auto load_pair = [&](int q, u32x4 (&raw)[16]) __attribute__((always_inline)) {
+  auto load_pair = [&](int q, u32x4 (&raw)[16], bool from_table, bool live = true) __attribute__((always_inline)) {
     const int j0 = 2 * q, j1 = 2 * q + 1;
-    const int phys0 = __builtin_amdgcn_readfirstlane(page_id(min(j0, last)));
-    const int phys1 = __builtin_amdgcn_readfirstlane(page_id(min(j1, last)));
+    const int phys0 = __builtin_amdgcn_readfirstlane(from_table ? ptab[pb + min(j0, last)] : page_id(min(j0, last)));
+    const int phys1 = __builtin_amdgcn_readfirstlane(from_table ? ptab[pb + min(j1, last)] : page_id(min(j1, last)));
     const size_t o0 = ((size_t)phys0 * n_kv + g) * 16 * DH, o1 = ((size_t)phys1 * n_kv + g) * 16 * DH;
-    const int n0 = j0 < pg_last ? 16 * DH * 2 : 0, n1 = j1 < pg_last ? 16 * DH * 2 : 0;
+    const int n0 = __builtin_amdgcn_readfirstlane(live && j0 < pg_last ? 16 * DH * 2 : 0);
+    const int n1 = __builtin_amdgcn_readfirstlane(live && j1 < pg_last ? 16 * DH * 2 : 0);
     const auto rk0 = buf_rsrc(kbase + o0, n0), rk1 = buf_rsrc(kbase + o1, n1);
     const auto rv0 = buf_rsrc(vbase + o0, n0), rv1 = buf_rsrc(vbase + o1, n1);
 #pragma unroll
@@ -242,11 +247,141 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
   // waves x 16 KB in flight per workgroup).  The scheduling barrier keeps
   // the loads in front of the multiplies.
   u32x4 raw[16];
-  if (wave < npairs) load_pair(wave, raw);
+  if constexpr (SINGLE) {
+    // Fused finish, one pass: thread t < 64 G finishes the rotary pair
+    // (i, i + 64) of query head g G + t / 64 on every path of the call;
+    // threads 64 G .. 64 G + 191 append the primary's key pair / value
+    // dimension of KV head g.  All loads a thread needs (its columns' slabs,
+    // the angle, the coupling, the cache page) are issued before the wave's
+    // first page pair, which is requested from the page table directly
+    // unless it holds the position this call appends; then the sums wait
+    // only for the older loads and the pages stay in flight.
+    const QKVFinish &f = a.fin;
+    const int t = threadIdx.x, pos = len - 1, np = a.rows.np;
+    const bool prim = f.mode != MODE_BRANCH;  // then path p0 = 0 is the primary
+    const int hh = t / (DH / 2), i = t % (DH / 2), u = t - G * (DH / 2);
+    const int c0 = (g * G + hh) * DH + i, c1 = c0 + DH / 2;
+    const int dkv = n_kv * DH;
+    auto at = [&](int path, int col) { return (size_t)(path * a.rows.Bp + b) * f.ldp + col; };
+    int ncol = 0;
+    size_t idx[4] = {0, 0, 0, 0};
+    if (a.fused) {
+      if (u < 0) {
+#pragma unroll
+        for (int pp = 0; pp < 2; ++pp)
+          if (pp < np) {
+            idx[2 * pp] = at(a.rows.p0 + pp, c0);
+            idx[2 * pp + 1] = at(a.rows.p0 + pp, c1);
+          }
+        ncol = 2 * min(np, 2);
+      } else if (prim && u < DH / 2) {
+        idx[0] = at(0, dq + g * DH + u);
+        idx[1] = at(0, dq + g * DH + u + DH / 2);
+        ncol = 2;
+      } else if (prim && u < DH / 2 + DH) {
+        idx[0] = at(0, dq + dkv + g * DH + u - DH / 2);
+        ncol = 1;
+      }
+    }
+    // slabs 0..7 of the thread's columns, as 32 unconditional loads (a loop
+    // or a guarded load here would wait for every outstanding load before
+    // the first page request): slabs past S re-read slab S - 1 and columns
+    // past ncol column 0, and neither is added below
+#pragma unroll
+    for (int j = 1; j < 4; ++j)
+      if (j >= ncol) idx[j] = idx[0];
+    float v[8][4];
+    if (ncol > 0) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[k][j] = f.part[min(k, f.S - 1) * f.split_stride + idx[j]];
+    }
+    float2 csi = make_float2(0.f, 0.f), aa = make_float2(0.f, 0.f), q1 = make_float2(0.f, 0.f);
+    int page = 0;
+    if (ncol > 0) {
+      csi = f.rope[(size_t)pos * (DH / 2) + (u < 0 ? i : u % (DH / 2))];
+      if (u < 0 && np + (prim ? 0 : 1) > 1) aa = make_float2(f.a[c0], f.a[c1]);
+      if (u < 0 && !prim) q1 = make_float2(f.Q1_in[(size_t)b * dq + c0], f.Q1_in[(size_t)b * dq + c1]);
+      if (u >= 0) page = ptab[pos >> 4];
+    }
+    const int pid0 = t < npages ? ptab[t] : 0;
+    const bool early = wave < npairs && (!a.fused || 2 * wave + 1 < npages - 1);
+    // issued by every wave (empty resources when not early: no traffic), so
+    // that the waits below count the same loads on every path
+    load_pair(wave, raw, true, early);
+    if (ncol > 0) {
+      // split-K sums in split order, as psum adds them (adding +0 for the
+      // slabs past S leaves the bits alone: a sum 0 + v + ... is never -0)
+      float x[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) x[j] += k < f.S ? v[k][j] : 0.f;
+      for (int k = 8; k < f.S; ++k)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (j < ncol) x[j] += f.part[k * f.split_stride + idx[j]];
+      if (u < 0) {
+        if (prim) {
+          // Q1 = RoPE(.) (Eqs. (8)-(9)), kept for a later branch pass when asked
+          q1 = rope_pair(x[0], x[1], csi);
+          qs[hh][i] = q1.x;
+          qs[hh][i + DH / 2] = q1.y;
+          const Retain &rt = f.ret;
+          if (rt.ptr && (rt.src_row < 0 || rt.src_row == b)) {
+            float *kp = rt.ptr + (size_t)(rt.src_row < 0 ? b : rt.dst_row) * dq;
+            kp[c0] = q1.x;
+            kp[c1] = q1.y;
+          }
+        }
+        // branch rows: Q2~ = RoPE(.) + a * Q1 (Eqs. (10)-(11)); paths past
+        // the first two of the call (several branches) sum their slabs here
+#pragma unroll
+        for (int pp = 0; pp < 2; ++pp)
+          if (pp < np && !(prim && pp == 0)) {
+            const float2 q2 = rope_pair(x[2 * pp], x[2 * pp + 1], csi);
+            qs[pp * G + hh][i] = couple(aa.x, q1.x, q2.x);
+            qs[pp * G + hh][i + DH / 2] = couple(aa.y, q1.y, q2.y);
+          }
+        for (int pp = 2; pp < np; ++pp) {
+          const float2 q2 = rope_pair(psum(f.part, f.split_stride, f.S, at(a.rows.p0 + pp, c0)),
+                                      psum(f.part, f.split_stride, f.S, at(a.rows.p0 + pp, c1)), csi);
+          qs[pp * G + hh][i] = couple(aa.x, q1.x, q2.x);
+          qs[pp * G + hh][i + DH / 2] = couple(aa.y, q1.y, q2.y);
+        }
+      } else if (u < DH / 2) {
+        // the primary appends K = RoPE(.) and V of head g at position pos (Sec. 4.4)
+        const float2 k = rope_pair(x[0], x[1], csi);
+        uint16_t *kc = (uint16_t *)a.kv.k + (((size_t)page * n_kv + g) * 16 + (pos & 15)) * DH;
+        kc[u] = f2bf(k.x);
+        kc[u + DH / 2] = f2bf(k.y);
+      } else {
+        ((uint16_t *)a.kv.v)[(((size_t)page * n_kv + g) * DH + u - DH / 2) * 16 + (pos & 15)] = f2bf(x[0]);
+      }
+    }
+    if (threadIdx.x < npages) pid_s[threadIdx.x] = pid0;
+    for (int i = threadIdx.x + NW * 64; i < npages; i += NW * 64) pid_s[i] = ptab[i];
+    __syncthreads();  // page ids and the query rows in LDS, the appended cache entry written
+    if (!early && wave < npairs) load_pair(wave, raw, false);
+  } else {
+    if (wave < npairs) load_pair(wave, raw, false);
+  }
+  if (SINGLE && a.fused) {
+    // query operand from the rows staged above (rows past the group's are zero)
+    const float z = r < nrows ? 1.f : 0.f;
+    const int rq = r < nrows ? r : 0;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const float4 u = *(const float4 *)&qs[rq][s * 32 + gq * 8] * z;
+      const float4 w = *(const float4 *)&qs[rq][s * 32 + gq * 8 + 4] * z;
+      qf[s] = u32x4{pack2(u.x, u.y), pack2(u.z, u.w), pack2(w.x, w.y), pack2(w.z, w.w)};
+    }
+  }
   for (int q = wave; q < npairs; q += NW) {
     u32x4 ka[4], kb[4], vf[8];
     stage(raw, ka, kb, vf);
-    load_pair(q + NW, raw);
+    load_pair(q + NW, raw, false);
     __builtin_amdgcn_sched_barrier(0);
     pair(q, ka, kb, vf);
   }
@@ -406,6 +541,14 @@ __global__ void k_attn_combine(AttnArgs a, T *O, int ldo) {
 hipError_t launch_attn_decode(const AttnArgs &a, hipStream_t st) {
   // the bf16 kernel holds two page ids per lane, the fp32 one 1024 positions in LDS
   if (a.pages_per_split < 1 || a.pages_per_split > (a.dtype == 1 ? 128 : 64)) return hipErrorInvalidValue;
+  // the fused query finish exists only in the single-workgroup kernel, for
+  // decode positions (one per sequence) and the same rows as the attention
+  if (a.fused && !(a.dtype == 1 && a.single && a.fin.pos_arr == a.pos_arr && a.fin.d_h == 128 &&
+                   a.fin.n_q == a.n_q && a.fin.n_kv == a.kv.n_kv && a.fin.rows.p0 == a.rows.p0 &&
+                   a.fin.rows.np == a.rows.np && a.fin.rows.Bp == a.rows.Bp && a.fin.rows.B == a.rows.B &&
+                   a.rows.np >= 1 && (a.fin.mode == MODE_BRANCH) == (a.rows.p0 >= 1) &&
+                   a.n_q / a.kv.n_kv * 64 + (a.fin.mode == MODE_BRANCH ? 0 : 192) <= 512))
+    return hipErrorInvalidValue;
   dim3 grid(a.max_splits, a.kv.n_kv, a.rows.B);
   if (a.dtype == 1 && a.single)
     hipLaunchKernelGGL(k_attn_decode_bf16<8>, dim3(1, a.kv.n_kv, a.rows.B), dim3(512), 0, st, a);

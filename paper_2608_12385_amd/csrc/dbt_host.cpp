@@ -614,7 +614,16 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
   qf.ret = Retain{c.retain && !cm ? ret_q : nullptr, c.ret_src, c.ret_dst};
   qf.kv = kvl;
   qf.dtype = cf.dtype;
-  if (!qkv_fused) HIPCHK(launch_qkv_finish(qf, st));
+  // Decode with one attention workgroup per (sequence, KV head): the
+  // attention kernel finishes the queries and appends the cache entry itself.
+  int maxlen = 0;
+  if (!c.prefill)
+    for (int b = 0; b < c.rows.B; ++b) maxlen = std::max(maxlen, kv->len[b] + 1);
+  const bool attn_single = !c.prefill && cf.dtype == DBT_BF16 && c.rows.B * cf.n_kv_heads >= 256 &&
+                           (maxlen + kPage - 1) / kPage <= 1024;
+  const bool finish_in_attn = attn_single && cf.head_dim == 128 &&
+                              cf.n_q_heads / cf.n_kv_heads * 64 + (amode == MODE_BRANCH ? 0 : 192) <= 512;
+  if (!qkv_fused && !finish_in_attn) HIPCHK(launch_qkv_finish(qf, st));
 
   // 2. attention over the primary cache
   if (c.prefill) {
@@ -634,9 +643,9 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
     // When the batch fills the chip (B x n_kv >= 256 workgroups), each
     // (sequence, KV head) is read by one eight-wave workgroup and no partials
     // are merged.  The choice depends on the batch, never on the branch.
-    int maxlen = 0;
-    for (int b = 0; b < c.rows.B; ++b) maxlen = std::max(maxlen, kv->len[b] + 1);
-    aa.single = cf.dtype == DBT_BF16 && c.rows.B * cf.n_kv_heads >= 256 && (maxlen + kPage - 1) / kPage <= 1024;
+    aa.single = attn_single;
+    aa.fused = finish_in_attn;
+    aa.fin = qf;
     aa.O = O;
     aa.ldo = dq;
     {

@@ -191,6 +191,11 @@ struct AttnArgs {
   int single;
   void *O;
   int ldo;
+  // single mode: the queries and the cache append are computed by the
+  // attention kernel itself from the QKV projection's split-K slabs (fin),
+  // exactly as k_qkv_finish would (one launch fewer); Q is then not read
+  int fused;
+  QKVFinish fin;
 };
 hipError_t launch_attn_decode(const AttnArgs &a, hipStream_t st);
 hipError_t launch_attn_combine(const AttnArgs &a, void *O, int ldo, hipStream_t st);
