@@ -18,7 +18,6 @@ namespace {
 
 __device__ __forceinline__ int phys_row(const Rows &r, int path, int b) { return path * r.Bp + b; }
 
-// Sum of the split-K partial slabs in split order (S <= 16).
 
 // ---------------------------------------------------------------------------
 
@@ -65,6 +64,26 @@ __device__ __forceinline__ float4 psum4(const float *part, long long stride, int
   for (int k = 0; k < S; ++k) s = add4(s, ((const float4 *)(part + k * stride))[idx4]);
   return s;
 }
+// Split-K slabs 0..7 of float4 element idx4, requested as eight
+// unconditional loads (slabs past S re-read slab S - 1 and are not added):
+// the loads of several rows are then all in flight before the first sum
+// waits, where a loop over S would wait for every outstanding load first.
+__device__ __forceinline__ void slabs_issue(const float *part, long long stride, int S, size_t idx4,
+                                            float4 (&v)[8]) {
+#pragma unroll
+  for (int k = 0; k < 8; ++k) v[k] = ((const float4 *)(part + (long long)min(k, S - 1) * stride))[idx4];
+}
+// Their sum in split order, the same additions as psum4 (adding +0 for the
+// slabs past S leaves the bits alone: a sum 0 + v + ... is never -0).
+__device__ __forceinline__ float4 slabs_sum(const float *part, long long stride, int S, size_t idx4,
+                                            const float4 (&v)[8]) {
+  const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+  float4 s = z;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) s = add4(s, k < S ? v[k] : z);
+  for (int k = 8; k < S; ++k) s = add4(s, ((const float4 *)(part + k * stride))[idx4]);
+  return s;
+}
 
 // out = x / sqrt(mean(x^2) + eps) * g (x read from global, fp32)
 template <typename T>
@@ -80,9 +99,11 @@ __device__ void norm_row(const float *x, const float *g, float eps, int d, T *ou
 // The same norm on a row a thread holds in registers: v[k] is element
 // (float4) i = threadIdx.x + k * blockDim.x of the row, valid while i < d/4.
 // The row is not read back from memory.
+// gv[k] holds the gain of element i, loaded by the caller ahead of time
+// (its load then overlaps the row's own loads or the reduction).
 template <typename T, int R>
-__device__ __forceinline__ void norm_regs(const float4 (&v)[R], const float *g, float eps, int d, T *out,
-                                          float *red) {
+__device__ __forceinline__ void norm_regs_g(const float4 (&v)[R], const float4 (&gv)[R], float eps, int d, T *out,
+                                            float *red) {
   float ss = 0.f;
 #pragma unroll
   for (int k = 0; k < R; ++k)
@@ -92,8 +113,19 @@ __device__ __forceinline__ void norm_regs(const float4 (&v)[R], const float *g, 
 #pragma unroll
   for (int k = 0; k < R; ++k) {
     const int i = threadIdx.x + k * blockDim.x;
-    if (i < d / 4) st4<T>(out, i, mul4(v[k], inv, ((const float4 *)g)[i]));
+    if (i < d / 4) st4<T>(out, i, mul4(v[k], inv, gv[k]));
   }
+}
+template <typename T, int R>
+__device__ __forceinline__ void norm_regs(const float4 (&v)[R], const float *g, float eps, int d, T *out,
+                                          float *red) {
+  float4 gv[R];
+#pragma unroll
+  for (int k = 0; k < R; ++k) {
+    const int i = threadIdx.x + k * blockDim.x;
+    gv[k] = i < d / 4 ? ((const float4 *)g)[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  norm_regs_g<T, R>(v, gv, eps, d, out, red);
 }
 
 // Tokens outside [0, vocab) read as a zero embedding row (no out-of-bounds read).
@@ -141,14 +173,15 @@ __global__ void k_load_hidden(const float *h1, const float *h2, const float *g_n
   const int row = phys_row(rows, path, b);
   const float4 *h = (const float4 *)((path == 0 ? h1 : h2 + (size_t)(path - 1) * rows.B * d) + (size_t)b * d);
   float4 *s = (float4 *)(S + (size_t)row * d);
-  float4 v[R];
+  float4 v[R], gv[R];
 #pragma unroll
   for (int k = 0; k < R; ++k) {
     const int i = threadIdx.x + k * blockDim.x;
     v[k] = i < d / 4 ? h[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+    gv[k] = i < d / 4 ? ((const float4 *)g_next)[i] : make_float4(0.f, 0.f, 0.f, 0.f);
     if (i < d / 4) s[i] = v[k];
   }
-  norm_regs<T, R>(v, g_next, eps, d, Xn + (size_t)row * ldx, red);
+  norm_regs_g<T, R>(v, gv, eps, d, Xn + (size_t)row * ldx, red);
 }
 
 template <typename T>
@@ -247,15 +280,20 @@ __global__ void k_resid_norm(const float *part, long long stride, int S, int ldp
   const bool keep = gc.g && path == 0 && gc.ret.ptr && (gc.ret.src_row < 0 || gc.ret.src_row == b);
   float4 *kept = keep ? (float4 *)(gc.ret.ptr + (size_t)(gc.ret.src_row < 0 ? b : gc.ret.dst_row) * d) : nullptr;
   const int r1 = phys_row(rows, 0, b);
-  float4 v[R];
+  float4 v[R], gv[R];
 #pragma unroll
   for (int k = 0; k < R; ++k) {
     const int i = threadIdx.x + k * blockDim.x;
-    v[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+    v[k] = gv[k] = make_float4(0.f, 0.f, 0.f, 0.f);
     if (i >= d / 4) continue;
+    gv[k] = ((const float4 *)g)[i];
     if (!gc.g || path == 0) {
-      const float4 a1 = psum4(part, stride, S, ((size_t)row * ldp) / 4 + i);
-      v[k] = add4(s[i], a1);
+      float4 sl[8];
+      slabs_issue(part, stride, S, ((size_t)row * ldp) / 4 + i, sl);
+      const float4 x = s[i];
+      __builtin_amdgcn_sched_barrier(0);  // the sums after every load
+      const float4 a1 = slabs_sum(part, stride, S, ((size_t)row * ldp) / 4 + i, sl);
+      v[k] = add4(x, a1);
       if (keep) kept[i] = a1;
     } else {
       // compute-matched branch row: S_bar2 = S2 + g_A * A1
@@ -267,7 +305,7 @@ __global__ void k_resid_norm(const float *part, long long stride, int S, int ldp
     }
     s[i] = v[k];
   }
-  norm_regs<T, R>(v, g, eps, d, Xn + (size_t)row * ldx, red);
+  norm_regs_g<T, R>(v, gv, eps, d, Xn + (size_t)row * ldx, red);
 }
 
 // SwiGLU and the MLP-intermediate coupling H2~ = H2 + b * H1 (Eq. (14)).
@@ -311,51 +349,56 @@ __global__ void k_down_finish(const float *part, long long stride, int S, int ld
                               Rows rows, const float *cvec, const float *M1_in, Retain ret,
                               float *Sres, const float *g_next, float eps, T *Xn, int ldx) {
   __shared__ float red[16];
-  const int b = blockIdx.x;
-  const bool prim = mode != MODE_BRANCH, br = mode != MODE_PRIMARY;
-  const int r1 = phys_row(rows, 0, b);
-  const int pb0 = rows.p0 > 1 ? rows.p0 : 1, pb1 = rows.p0 + rows.np;
-  float4 *s1 = (float4 *)(Sres + (size_t)r1 * d);
-  const bool keep = ret.ptr && (ret.src_row < 0 || ret.src_row == b);
+  // one workgroup per (sequence, path); a branch row sums the primary's
+  // slabs itself (the same additions, so the same M1 bits) for its coupling
+  const int b = blockIdx.x, path = rows.p0 + blockIdx.y;
+  const bool prim = mode != MODE_BRANCH;
+  if (path == 0 && !prim) return;
+  const int r1 = phys_row(rows, 0, b), row = phys_row(rows, path, b);
+  float4 *s = (float4 *)(Sres + (size_t)row * d);
+  const bool keep = path == 0 && ret.ptr && (ret.src_row < 0 || ret.src_row == b);
   float4 *kept = keep ? (float4 *)(ret.ptr + (size_t)(ret.src_row < 0 ? b : ret.dst_row) * d) : nullptr;
-  constexpr int MP = 4;  // paths of one sequence: the primary and up to three branches
-  float4 v[MP][R];
+  float4 v[R], gv[R];
 #pragma unroll
   for (int k = 0; k < R; ++k) {
     const int i = threadIdx.x + k * blockDim.x;
-#pragma unroll
-    for (int p = 0; p < MP; ++p) v[p][k] = make_float4(0.f, 0.f, 0.f, 0.f);
+    v[k] = gv[k] = make_float4(0.f, 0.f, 0.f, 0.f);
     if (i >= d / 4) continue;
-    float4 m1;
-    if (prim) {
-      m1 = psum4(part, stride, S, ((size_t)r1 * ldp) / 4 + i);
-      v[0][k] = add4(s1[i], m1);
-      s1[i] = v[0][k];
+    // every load of the element first, the slabs unconditionally (a load
+    // under a condition lets the compiler start the sums before the next
+    // loads): slabs of the primary row and of this row (the same row twice
+    // for the primary), the residual, the coupling (a stand-in address for
+    // the primary) and the kept M1 of a branch-only call
+    const size_t i1 = ((size_t)r1 * ldp) / 4 + i, i2 = ((size_t)row * ldp) / 4 + i;
+    float4 sl1[8], sl2[8];
+#pragma unroll
+    for (int k2 = 0; k2 < 8; ++k2) {
+      const long long o = (long long)min(k2, S - 1) * stride;
+      sl1[k2] = ((const float4 *)(part + o))[i1];
+      sl2[k2] = ((const float4 *)(part + o))[i2];
+    }
+    const float4 x = s[i];
+    const float4 c = (path >= 1 ? (const float4 *)cvec : s)[i];
+    if constexpr (R <= 2) gv[k] = (g_next ? (const float4 *)g_next : s)[i];  // (registers allow)
+    float4 m1 = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (!prim) m1 = ((const float4 *)(M1_in + (size_t)b * d))[i];
+    __builtin_amdgcn_sched_barrier(0);  // the sums after every load
+    if (prim) m1 = slabs_sum(part, stride, S, i1, sl1);
+    if (path == 0) {
+      v[k] = add4(x, m1);
       if (keep) kept[i] = m1;
     } else {
-      m1 = ((const float4 *)(M1_in + (size_t)b * d))[i];
+      const float4 m2 = slabs_sum(part, stride, S, i2, sl2);
+      const float4 t = make_float4(m2.x + c.x * m1.x, m2.y + c.y * m1.y, m2.z + c.z * m1.z, m2.w + c.w * m1.w);
+      v[k] = add4(x, t);
     }
-    if (br)
-#pragma unroll
-      for (int p = 1; p < MP; ++p) {
-        if (p < pb0 || p >= pb1) continue;
-        const int r2 = phys_row(rows, p, b);
-        float4 *s2 = (float4 *)(Sres + (size_t)r2 * d);
-        const float4 m2 = psum4(part, stride, S, ((size_t)r2 * ldp) / 4 + i);
-        const float4 c = ((const float4 *)cvec)[i];
-        const float4 t = make_float4(m2.x + c.x * m1.x, m2.y + c.y * m1.y, m2.z + c.z * m1.z, m2.w + c.w * m1.w);
-        v[p][k] = add4(s2[i], t);
-        s2[i] = v[p][k];
-      }
+    s[i] = v[k];
   }
   if (!g_next) return;
-  if (prim) norm_regs<T, R>(v[0], g_next, eps, d, Xn + (size_t)r1 * ldx, red);
-  if (br)
-#pragma unroll
-    for (int p = 1; p < MP; ++p) {
-      if (p < pb0 || p >= pb1) continue;
-      norm_regs<T, R>(v[p], g_next, eps, d, Xn + (size_t)phys_row(rows, p, b) * ldx, red);
-    }
+  if constexpr (R <= 2)
+    norm_regs_g<T, R>(v, gv, eps, d, Xn + (size_t)row * ldx, red);
+  else
+    norm_regs<T, R>(v, g_next, eps, d, Xn + (size_t)row * ldx, red);
 }
 
 // ---------------------------------------------------------------------------
@@ -735,7 +778,7 @@ hipError_t launch_swiglu_finish(const float *part, long long stride, int S, int 
 hipError_t launch_down_finish(const float *part, long long stride, int S, int ldp, int d, int mode,
                               Rows rows, const float *cvec, const float *M1_in, Retain ret, float *Sres,
                               const float *g_next, float eps, int dtype, void *Xn, int ldx, hipStream_t st) {
-  dim3 grid(rows.B);
+  dim3 grid(rows.B, rows.np);
   if (dtype == 1) {
     DBT_ROW_LAUNCH(k_down_finish, uint16_t, d, grid, dim3(row_threads(d)), 0, st, part, stride, S, ldp, d, mode, rows,
                    cvec, M1_in, ret, Sres, g_next, eps, (uint16_t *)Xn, ldx)
