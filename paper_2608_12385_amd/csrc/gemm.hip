@@ -12,6 +12,8 @@
 // primary rows come out bit-identical with or without the branch rows.
 //
 // fp32 weights: an LDS-tiled vector kernel (small models).
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -172,7 +174,8 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
   // chunk c went to LDS one step ago) and the weights of chunk c+PD; stage
   // chunk c+1 (register slot xn = (c+1) % XA, loaded XA-1 steps ago) into
   // the other LDS slot.  All slots are compile-time at every call.
-  auto step = [&](int c, int w, int par, int xc, int xn) {
+  auto step = [&](auto guard, int c, int w, int par, int xc, int xn) {
+    constexpr bool GUARD = decltype(guard)::value;  // skip loads and staging past the last chunk
     const uint16_t *xl = xs[par];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
@@ -203,9 +206,9 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
       }
       wave_lds_fence();
     }
-    xload(xc, c + XA);
-    wload(w, c + PD);
-    xstore(par ^ 1, xn);
+    if (!GUARD || c + XA < nch) xload(xc, c + XA);
+    if (!GUARD || c + PD < nch) wload(w, c + PD);
+    if (!GUARD || c + 1 < nch) xstore(par ^ 1, xn);
     __syncthreads();
   };
 
@@ -220,13 +223,30 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
   // which keeps the wait counts exact across the loop's back edge
   constexpr int P2 = lcm3(PD, XA, 2);
   int c0 = 0;
-  for (; c0 + P2 <= nch; c0 += P2) {
+  if constexpr (NW <= 8) {
+    // Rounds whose loads all fall inside the split run unguarded; the last
+    // steps (at most P2 + LA - 1) skip the loads past the last chunk, which
+    // would otherwise re-read it and hold the waves for one more memory
+    // round trip at the end (W_O 10.5 -> 9.3 us, down 29.0 -> 26.4 us by the
+    // last workgroup's end).  Sixteen-wave tiles keep the plain tail: its
+    // unrolled steps would exceed their 128 registers.
+    constexpr int LA = PD > XA ? PD : XA;
+    for (; c0 + P2 + LA <= nch; c0 += P2) {
 #pragma unroll
-    for (int u = 0; u < P2; ++u) step(c0 + u, u % PD, u & 1, u % XA, (u + 1) % XA);
+      for (int u = 0; u < P2; ++u) step(std::false_type{}, c0 + u, u % PD, u & 1, u % XA, (u + 1) % XA);
+    }
+#pragma unroll
+    for (int u = 0; u < P2 + LA - 1; ++u)
+      if (c0 + u < nch) step(std::true_type{}, c0 + u, u % PD, u & 1, u % XA, (u + 1) % XA);
+  } else {
+    for (; c0 + P2 <= nch; c0 += P2) {
+#pragma unroll
+      for (int u = 0; u < P2; ++u) step(std::false_type{}, c0 + u, u % PD, u & 1, u % XA, (u + 1) % XA);
+    }
+#pragma unroll
+    for (int u = 0; u + 1 < P2; ++u)
+      if (c0 + u < nch) step(std::false_type{}, c0 + u, u % PD, u & 1, u % XA, (u + 1) % XA);
   }
-#pragma unroll
-  for (int u = 0; u + 1 < P2; ++u)
-    if (c0 + u < nch) step(c0 + u, u % PD, u & 1, u % XA, (u + 1) % XA);
   // lane holds D[n = rb*16 + 4*gq + i][m = cb*16 + r]: Y[m][n .. n+3]
   if constexpr (GLU) {
     // lane (r, gq) holds D[n = 4gq + i][m = cb*16 + r]: gate rows n < 8
