@@ -81,7 +81,13 @@ __device__ __forceinline__ float4 slabs_sum(const float *part, long long stride,
   float4 s = z;
 #pragma unroll
   for (int k = 0; k < 8; ++k) s = add4(s, k < S ? v[k] : z);
-  for (int k = 8; k < S; ++k) s = add4(s, ((const float4 *)(part + k * stride))[idx4]);
+  for (int k0 = 8; k0 < S; k0 += 8) {  // more than eight splits: eight more per round trip
+    float4 w[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) w[k] = ((const float4 *)(part + (long long)min(k0 + k, S - 1) * stride))[idx4];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) s = add4(s, k0 + k < S ? w[k] : z);
+  }
   return s;
 }
 
