@@ -73,7 +73,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
   // order and the same rope_pair / couple as k_qkv_finish, so the bits equal
   // the unfused path's.
   constexpr int QLD = DH + 4;  // row pitch of qs (floats): rows start on different banks
-  __shared__ float qs[SINGLE ? 16 : 1][SINGLE ? QLD : 1];
+  __shared__ float qs[16][QLD];
   if constexpr (!SINGLE) {
     myid0 = (pb + lane < pe) ? ptab[pb + lane] : 0;
     myid1 = (pb + 64 + lane < pe) ? ptab[pb + 64 + lane] : 0;
@@ -87,7 +87,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
   // Rows past the group's queries read row 0 and are zeroed: all eight
   // loads are issued at once (a load guarded per element compiles to a
   // branch and a full wait each, 32 round trips before the first page).
-  if (!(SINGLE && a.fused)) {
+  if (!a.fused) {
     const bool valid = r < nrows;
     const int path = a.rows.p0 + (valid ? r / G : 0);
     const int head = g * G + (valid ? r % G : 0);
@@ -247,18 +247,21 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
   // waves x 16 KB in flight per workgroup).  The scheduling barrier keeps
   // the loads in front of the multiplies.
   u32x4 raw[16];
-  if constexpr (SINGLE) {
-    // Fused finish, one pass: thread t < 64 G finishes the rotary pair
-    // (i, i + 64) of query head g G + t / 64 on every path of the call;
-    // threads 64 G .. 64 G + 191 append the primary's key pair / value
-    // dimension of KV head g.  All loads a thread needs (its columns' slabs,
-    // the angle, the coupling, the cache page) are issued before the wave's
-    // first page pair, which is requested from the page table directly
-    // unless it holds the position this call appends; then the sums wait
-    // only for the older loads and the pages stay in flight.
+  {
+    // Fused finish (a.fused): thread t < 64 G finishes the rotary pair
+    // (i, i + 64) of query head g G + t / 64 on every path of the call (every
+    // split of a sequence computes its queries); threads 64 G .. 64 G + 191
+    // of the workgroup that holds the sequence's last page append the
+    // primary's key pair / value dimension of KV head g.  All loads a thread
+    // needs (its columns' slabs, the angle, the coupling, the cache page) are
+    // issued before the wave's first page pair, which is requested from the
+    // page table directly unless it holds the appended position; then the
+    // sums wait only for the older loads and the pages stay in flight.
+    // Append threads beyond the workgroup (four waves) take a second pass.
     const QKVFinish &f = a.fin;
     const int t = threadIdx.x, pos = len - 1, np = a.rows.np;
     const bool prim = f.mode != MODE_BRANCH;  // then path p0 = 0 is the primary
+    const bool appends = a.fused && prim && pe == npages;
     const int hh = t / (DH / 2), i = t % (DH / 2), u = t - G * (DH / 2);
     const int c0 = (g * G + hh) * DH + i, c1 = c0 + DH / 2;
     const int dkv = n_kv * DH;
@@ -274,11 +277,11 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
             idx[2 * pp + 1] = at(a.rows.p0 + pp, c1);
           }
         ncol = 2 * min(np, 2);
-      } else if (prim && u < DH / 2) {
+      } else if (appends && u < DH / 2) {
         idx[0] = at(0, dq + g * DH + u);
         idx[1] = at(0, dq + g * DH + u + DH / 2);
         ncol = 2;
-      } else if (prim && u < DH / 2 + DH) {
+      } else if (appends && u < DH / 2 + DH) {
         idx[0] = at(0, dq + dkv + g * DH + u - DH / 2);
         ncol = 1;
       }
@@ -305,8 +308,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
       if (u < 0 && !prim) q1 = make_float2(f.Q1_in[(size_t)b * dq + c0], f.Q1_in[(size_t)b * dq + c1]);
       if (u >= 0) page = ptab[pos >> 4];
     }
-    const int pid0 = t < npages ? ptab[t] : 0;
-    const bool early = wave < npairs && (!a.fused || 2 * wave + 1 < npages - 1);
+    const int pid0 = SINGLE && t < npages ? ptab[t] : 0;
+    const bool early = wave < npairs && (!appends || pb + 2 * wave + 1 < npages - 1);
     // issued by every wave (empty resources when not early: no traffic), so
     // that the waits below count the same loads on every path
     load_pair(wave, raw, true, early);
@@ -360,14 +363,32 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
         ((uint16_t *)a.kv.v)[(((size_t)page * n_kv + g) * DH + u - DH / 2) * 16 + (pos & 15)] = f2bf(x[0]);
       }
     }
-    if (threadIdx.x < npages) pid_s[threadIdx.x] = pid0;
-    for (int i = threadIdx.x + NW * 64; i < npages; i += NW * 64) pid_s[i] = ptab[i];
-    __syncthreads();  // page ids and the query rows in LDS, the appended cache entry written
+    if (appends)
+      for (int t2 = t + NW * 64; t2 < G * (DH / 2) + DH / 2 + DH; t2 += NW * 64) {
+        const int u2 = t2 - G * (DH / 2);
+        if (u2 < 0) continue;  // queries: all in the first pass (G <= NW)
+        const int page2 = ptab[pos >> 4];
+        const float2 cs2 = f.rope[(size_t)pos * (DH / 2) + u2 % (DH / 2)];
+        if (u2 < DH / 2) {
+          const int k0 = dq + g * DH + u2;
+          const float2 k = rope_pair(psum(f.part, f.split_stride, f.S, at(0, k0)),
+                                     psum(f.part, f.split_stride, f.S, at(0, k0 + DH / 2)), cs2);
+          uint16_t *kc = (uint16_t *)a.kv.k + (((size_t)page2 * n_kv + g) * 16 + (pos & 15)) * DH;
+          kc[u2] = f2bf(k.x);
+          kc[u2 + DH / 2] = f2bf(k.y);
+        } else {
+          const float vv = psum(f.part, f.split_stride, f.S, at(0, dq + dkv + g * DH + u2 - DH / 2));
+          ((uint16_t *)a.kv.v)[(((size_t)page2 * n_kv + g) * DH + u2 - DH / 2) * 16 + (pos & 15)] = f2bf(vv);
+        }
+      }
+    if constexpr (SINGLE) {
+      if (threadIdx.x < npages) pid_s[threadIdx.x] = pid0;
+      for (int i = threadIdx.x + NW * 64; i < npages; i += NW * 64) pid_s[i] = ptab[i];
+    }
+    if (SINGLE || a.fused) __syncthreads();  // page ids and query rows in LDS, the appended entry written
     if (!early && wave < npairs) load_pair(wave, raw, false);
-  } else {
-    if (wave < npairs) load_pair(wave, raw, false);
   }
-  if (SINGLE && a.fused) {
+  if (a.fused) {
     // query operand from the rows staged above (rows past the group's are zero)
     const float z = r < nrows ? 1.f : 0.f;
     const int rq = r < nrows ? r : 0;
@@ -541,13 +562,14 @@ __global__ void k_attn_combine(AttnArgs a, T *O, int ldo) {
 hipError_t launch_attn_decode(const AttnArgs &a, hipStream_t st) {
   // the bf16 kernel holds two page ids per lane, the fp32 one 1024 positions in LDS
   if (a.pages_per_split < 1 || a.pages_per_split > (a.dtype == 1 ? 128 : 64)) return hipErrorInvalidValue;
-  // the fused query finish exists only in the single-workgroup kernel, for
-  // decode positions (one per sequence) and the same rows as the attention
-  if (a.fused && !(a.dtype == 1 && a.single && a.fin.pos_arr == a.pos_arr && a.fin.d_h == 128 &&
+  // the fused query finish: bf16 cache, decode positions (one per
+  // sequence), the same rows as the attention, every query head of a KV
+  // head in the first pass (G <= waves)
+  if (a.fused && !(a.dtype == 1 && a.fin.pos_arr == a.pos_arr && a.fin.d_h == 128 &&
                    a.fin.n_q == a.n_q && a.fin.n_kv == a.kv.n_kv && a.fin.rows.p0 == a.rows.p0 &&
                    a.fin.rows.np == a.rows.np && a.fin.rows.Bp == a.rows.Bp && a.fin.rows.B == a.rows.B &&
                    a.rows.np >= 1 && (a.fin.mode == MODE_BRANCH) == (a.rows.p0 >= 1) &&
-                   a.n_q / a.kv.n_kv * 64 + (a.fin.mode == MODE_BRANCH ? 0 : 192) <= 512))
+                   a.n_q / a.kv.n_kv <= (a.single ? 8 : 4)))
     return hipErrorInvalidValue;
   dim3 grid(a.max_splits, a.kv.n_kv, a.rows.B);
   if (a.dtype == 1 && a.single)

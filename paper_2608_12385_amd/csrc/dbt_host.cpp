@@ -614,15 +614,15 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
   qf.ret = Retain{c.retain && !cm ? ret_q : nullptr, c.ret_src, c.ret_dst};
   qf.kv = kvl;
   qf.dtype = cf.dtype;
-  // Decode with one attention workgroup per (sequence, KV head): the
-  // attention kernel finishes the queries and appends the cache entry itself.
+  // Decode on the bf16 cache: the attention kernel finishes the queries and
+  // appends the cache entry itself.
   int maxlen = 0;
   if (!c.prefill)
     for (int b = 0; b < c.rows.B; ++b) maxlen = std::max(maxlen, kv->len[b] + 1);
   const bool attn_single = !c.prefill && cf.dtype == DBT_BF16 && c.rows.B * cf.n_kv_heads >= 256 &&
                            (maxlen + kPage - 1) / kPage <= 1024;
-  const bool finish_in_attn = attn_single && cf.head_dim == 128 &&
-                              cf.n_q_heads / cf.n_kv_heads * 64 + (amode == MODE_BRANCH ? 0 : 192) <= 512;
+  const bool finish_in_attn = !c.prefill && cf.dtype == DBT_BF16 && cf.head_dim == 128 &&
+                              cf.n_q_heads / cf.n_kv_heads <= (attn_single ? 8 : 4);
   if (!qkv_fused && !finish_in_attn) HIPCHK(launch_qkv_finish(qf, st));
 
   // 2. attention over the primary cache
