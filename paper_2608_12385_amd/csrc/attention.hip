@@ -40,15 +40,19 @@ __device__ __forceinline__ bool split_range(int npages, int target, int s, int *
   return *pb < *pe;
 }
 
-// Requires d_h == 128, np*G <= 16 and pages_per_split <= 128.
-// NW = 4: one split of the sequence per workgroup, partials merged by
-// k_attn_combine.  NW = 8 (a.single): the whole sequence in one workgroup of
-// eight waves (at most 1024 pages, page ids staged in LDS), the waves merged
-// in LDS and the normalised rows written to a.O directly.
-template <int NW>
+// Requires d_h == 128 and np*G <= 16.
+// <4, false>: one split of the sequence per workgroup of four waves (at most
+// 128 pages, two page ids per lane), partials merged by k_attn_combine.
+// <8, false>: the same with eight waves and splits of up to 1024 pages (page
+// ids staged in LDS), for long sequences: one round of longer workgroups.
+// <8, true> (a.single): the whole sequence in one workgroup of eight waves
+// (at most 1024 pages), the waves merged in LDS and the normalised rows
+// written to a.O directly.
+template <int NW, bool SINGLE>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) void k_attn_decode_bf16(AttnArgs a) {
   constexpr int DH = 128;
-  constexpr bool SINGLE = NW == 8;
+  constexpr bool LDSIDS = NW == 8;  // page ids of the split staged in LDS (else two per lane)
+  static_assert(!SINGLE || LDSIDS, "the single-workgroup kernel has eight waves");
   const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int len = a.pos_arr[b] + 1;
   const int npages = (len + 15) >> 4;
@@ -64,7 +68,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
   const float scale = kLog2e / sqrtf((float)DH);
   // page ids of the split: lane i holds pages pb + i and pb + 64 + i
   const int *ptab = a.kv.page_table + (size_t)b * a.kv.mpps;
-  __shared__ int pid_s[SINGLE ? 1024 : 1];
+  __shared__ int pid_s[LDSIDS ? 1024 : 1];
   int myid0 = 0, myid1 = 0;
   u32x4 qf[4];
   // Fused finish of the QKV projection (single mode, a.fused): the workgroup
@@ -74,12 +78,12 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
   // the unfused path's.
   constexpr int QLD = DH + 4;  // row pitch of qs (floats): rows start on different banks
   __shared__ float qs[16][QLD];
-  if constexpr (!SINGLE) {
+  if constexpr (!LDSIDS) {
     myid0 = (pb + lane < pe) ? ptab[pb + lane] : 0;
     myid1 = (pb + 64 + lane < pe) ? ptab[pb + 64 + lane] : 0;
   }
   auto page_id = [&](int j) {
-    if constexpr (SINGLE) return pid_s[j];
+    if constexpr (LDSIDS) return pid_s[j];
     else return __shfl(j < 64 ? myid0 : myid1, j & 63, 64);
   };
 
@@ -308,7 +312,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
       if (u < 0 && !prim) q1 = make_float2(f.Q1_in[(size_t)b * dq + c0], f.Q1_in[(size_t)b * dq + c1]);
       if (u >= 0) page = ptab[pos >> 4];
     }
-    const int pid0 = SINGLE && t < npages ? ptab[t] : 0;
+    const int pid0 = LDSIDS && t < pe - pb ? ptab[pb + t] : 0;
     const bool early = wave < npairs && (!appends || pb + 2 * wave + 1 < npages - 1);
     // issued by every wave (empty resources when not early: no traffic), so
     // that the waits below count the same loads on every path
@@ -381,11 +385,11 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
           ((uint16_t *)a.kv.v)[(((size_t)page2 * n_kv + g) * DH + u2 - DH / 2) * 16 + (pos & 15)] = f2bf(vv);
         }
       }
-    if constexpr (SINGLE) {
-      if (threadIdx.x < npages) pid_s[threadIdx.x] = pid0;
-      for (int i = threadIdx.x + NW * 64; i < npages; i += NW * 64) pid_s[i] = ptab[i];
+    if constexpr (LDSIDS) {
+      if (threadIdx.x < pe - pb) pid_s[threadIdx.x] = pid0;
+      for (int i = threadIdx.x + NW * 64; i < pe - pb; i += NW * 64) pid_s[i] = ptab[pb + i];
     }
-    if (SINGLE || a.fused) __syncthreads();  // page ids and query rows in LDS, the appended entry written
+    if (LDSIDS || a.fused) __syncthreads();  // page ids and query rows in LDS, the appended entry written
     if (!early && wave < npairs) load_pair(wave, raw, false);
   }
   if (a.fused) {
@@ -560,8 +564,10 @@ __global__ void k_attn_combine(AttnArgs a, T *O, int ldo) {
 }  // namespace
 
 hipError_t launch_attn_decode(const AttnArgs &a, hipStream_t st) {
-  // the bf16 kernel holds two page ids per lane, the fp32 one 1024 positions in LDS
-  if (a.pages_per_split < 1 || a.pages_per_split > (a.dtype == 1 ? 128 : 64)) return hipErrorInvalidValue;
+  // split lengths: the four-wave bf16 kernel holds two page ids per lane, the
+  // eight-wave one 1024 in LDS, the fp32 one 1024 positions in LDS
+  const int max_pps = a.dtype != 1 ? 64 : a.wide ? 1024 : 128;
+  if (!a.single && (a.pages_per_split < 1 || a.pages_per_split > max_pps)) return hipErrorInvalidValue;
   // the fused query finish: bf16 cache, decode positions (one per
   // sequence), the same rows as the attention, every query head of a KV
   // head in the first pass (G <= waves)
@@ -569,13 +575,15 @@ hipError_t launch_attn_decode(const AttnArgs &a, hipStream_t st) {
                    a.fin.n_q == a.n_q && a.fin.n_kv == a.kv.n_kv && a.fin.rows.p0 == a.rows.p0 &&
                    a.fin.rows.np == a.rows.np && a.fin.rows.Bp == a.rows.Bp && a.fin.rows.B == a.rows.B &&
                    a.rows.np >= 1 && (a.fin.mode == MODE_BRANCH) == (a.rows.p0 >= 1) &&
-                   a.n_q / a.kv.n_kv <= (a.single ? 8 : 4)))
+                   a.n_q / a.kv.n_kv <= (a.single || a.wide ? 8 : 4)))
     return hipErrorInvalidValue;
   dim3 grid(a.max_splits, a.kv.n_kv, a.rows.B);
   if (a.dtype == 1 && a.single)
-    hipLaunchKernelGGL(k_attn_decode_bf16<8>, dim3(1, a.kv.n_kv, a.rows.B), dim3(512), 0, st, a);
+    hipLaunchKernelGGL((k_attn_decode_bf16<8, true>), dim3(1, a.kv.n_kv, a.rows.B), dim3(512), 0, st, a);
+  else if (a.dtype == 1 && a.wide)
+    hipLaunchKernelGGL((k_attn_decode_bf16<8, false>), grid, dim3(512), 0, st, a);
   else if (a.dtype == 1)
-    hipLaunchKernelGGL(k_attn_decode_bf16<4>, grid, dim3(256), 0, st, a);
+    hipLaunchKernelGGL((k_attn_decode_bf16<4, false>), grid, dim3(256), 0, st, a);
   else
     hipLaunchKernelGGL(k_attn_decode_f32, grid, dim3(256), 0, st, a);
   return hipGetLastError();

@@ -51,7 +51,7 @@ constexpr int kPage = 16;
 // about 512 workgroups.  The target is fixed when the model is created, so a
 // row's result depends only on its own query and cache.
 // The fp32 kernel holds a split's scores in LDS (at most 64 pages).
-constexpr int kSplitTargetBf16 = 86, kSplitMinBf16 = 16, kSplitTargetF32 = 64;
+constexpr int kSplitTargetBf16 = 86, kSplitMinBf16 = 16, kSplitTargetF32 = 64, kSplitWideMin = 256;
 constexpr int kMixChunk = 4096;
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -64,6 +64,7 @@ struct Layout {
   int Bp_max = 0, R_max = 0, rows_max = 0, max_in = 0, nqkv = 0, f = 0;
   GemmConfig g_qkv{1, 1, 1}, g_o{1, 1, 1}, g_gu{1, 1, 1}, g_d{1, 1, 1}, g_lm{1, 1, 1};
   int split_target = 0, max_splits = 0, nch = 0, nstat = 0;
+  bool wide = false;  // attention splits in eight-wave workgroups (see the layout set-up)
   bool moe = false;
   // Decode gate/up on the fused SwiGLU kernel: fixed per model (from the
   // largest stacked call), so every call of a step sums each output element
@@ -152,6 +153,15 @@ Layout make_layout(const dbt_config *c) {
     const int pairs = c->max_batch * c->n_kv_heads;
     const int want = pairs >= 256 ? 1 : (512 + pairs - 1) / pairs;  // splits per pair
     L.split_target = std::clamp((maxpages + want - 1) / want, kSplitMinBf16, kSplitTargetBf16);
+    // long caches and few (sequence, KV head) pairs: one round of eight-wave
+    // workgroups, each reading up to 1024 pages, instead of several rounds
+    // of four-wave ones (fewer prologues, partial stores and splits to merge)
+    const int want8 = (256 + pairs - 1) / pairs;
+    const int target8 = (maxpages + want8 - 1) / want8;
+    if (pairs < 256 && target8 >= kSplitWideMin) {
+      L.wide = true;
+      L.split_target = std::min(target8, 1024);
+    }
   } else {
     L.split_target = kSplitTargetF32;
   }
@@ -622,7 +632,7 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
   const bool attn_single = !c.prefill && cf.dtype == DBT_BF16 && c.rows.B * cf.n_kv_heads >= 256 &&
                            (maxlen + kPage - 1) / kPage <= 1024;
   const bool finish_in_attn = !c.prefill && cf.dtype == DBT_BF16 && cf.head_dim == 128 &&
-                              cf.n_q_heads / cf.n_kv_heads <= (attn_single ? 8 : 4);
+                              cf.n_q_heads / cf.n_kv_heads <= (attn_single || L.wide ? 8 : 4);
   if (!qkv_fused && !finish_in_attn) HIPCHK(launch_qkv_finish(qf, st));
 
   // 2. attention over the primary cache
@@ -644,6 +654,7 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
     // (sequence, KV head) is read by one eight-wave workgroup and no partials
     // are merged.  The choice depends on the batch, never on the branch.
     aa.single = attn_single;
+    aa.wide = L.wide;
     aa.fused = finish_in_attn;
     aa.fin = qf;
     aa.O = O;

@@ -191,7 +191,10 @@ struct AttnArgs {
   int single;
   void *O;
   int ldo;
-  // single mode: the queries and the cache append are computed by the
+  // bf16, not single: splits of up to 1024 pages in workgroups of eight waves
+  // (else up to 128 pages in workgroups of four)
+  int wide;
+  // bf16 decode: the queries and the cache append are computed by the
   // attention kernel itself from the QKV projection's split-K slabs (fin),
   // exactly as k_qkv_finish would (one launch fewer); Q is then not read
   int fused;
