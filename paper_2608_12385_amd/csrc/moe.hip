@@ -31,52 +31,69 @@ __device__ __forceinline__ int prow(const Rows &r, int path, int b) { return pat
 // Router logits: workgroup = (sequence, 16 experts).  The fp32 MLP inputs
 // RMSNorm(S_bar) * g of the active rows are rebuilt in LDS; wave w computes
 // experts 4w..4w+3 of the group for both rows, lanes covering the model
-// dimension 8 elements at a time.
+// dimension 8 elements at a time (NIT = d / 512 pieces per lane).  Every
+// load (the rows, the gain, the wave's four router rows) is issued at the
+// start, so the kernel waits for memory once.
+template <int NIT>
 __global__ __launch_bounds__(256) void k_moe_logits(MoeRoute a) {
   __shared__ float u[2][4096 + 4];
   __shared__ float red[16];
   const int b = blockIdx.x, e0 = blockIdx.y * 16;
   const bool prim = a.mode != MODE_BRANCH, br = a.mode != MODE_PRIMARY;
-  const int d = a.d, E = a.E;
+  const int E = a.E;
+  constexpr int d = NIT * 512, NV = (d / 4 + 255) / 256;  // float4 per thread and row
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  u32x4 wv[4][NIT];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = min(e0 + wave * 4 + q, E - 1);
+    const uint16_t *wr = (const uint16_t *)a.Wr + (size_t)e * d;
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) wv[q][it] = *(const u32x4 *)(wr + (it * 64 + lane) * 8);
+  }
+  float4 sv[2][NV], gv[NV];
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const int i = min((int)threadIdx.x + k * 256, d / 4 - 1);
+    gv[k] = ((const float4 *)a.g)[i];
+#pragma unroll
+    for (int p = 0; p < 2; ++p) sv[p][k] = ((const float4 *)(a.Sbar + (size_t)prow(a.rows, p, b) * d))[i];
+  }
   for (int p = 0; p < 2; ++p) {
     if ((p == 0 && !prim) || (p == 1 && !br)) continue;
-    const float4 *s = (const float4 *)(a.Sbar + (size_t)prow(a.rows, p, b) * d);
     float ss = 0.f;
-    for (int i = threadIdx.x; i < d / 4; i += blockDim.x) {
-      const float4 v = s[i];
-      ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
-    }
+#pragma unroll
+    for (int k = 0; k < NV; ++k)
+      if ((int)threadIdx.x + k * 256 < d / 4) {
+        const float4 v = sv[p][k];
+        ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+      }
     ss = block_sum(ss, red);
     const float inv = 1.0f / sqrtf(ss / (float)d + a.eps);
-    for (int i = threadIdx.x; i < d / 4; i += blockDim.x) {
-      const float4 v = s[i], g = ((const float4 *)a.g)[i];
-      u[p][4 * i + 0] = v.x * inv * g.x;
-      u[p][4 * i + 1] = v.y * inv * g.y;
-      u[p][4 * i + 2] = v.z * inv * g.z;
-      u[p][4 * i + 3] = v.w * inv * g.w;
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+      const int i = threadIdx.x + k * 256;
+      if (i < d / 4) {
+        const float4 v = sv[p][k], g = gv[k];
+        u[p][4 * i + 0] = v.x * inv * g.x;
+        u[p][4 * i + 1] = v.y * inv * g.y;
+        u[p][4 * i + 2] = v.z * inv * g.z;
+        u[p][4 * i + 3] = v.w * inv * g.w;
+      }
     }
   }
   __syncthreads();
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  constexpr int MAXIT = 8;  // d <= 4096 = 8 * 64 lanes * 8 elements
-  const int nit = d / 512;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int e = e0 + wave * 4 + q;
     if (e >= E) break;
-    const uint16_t *wr = (const uint16_t *)a.Wr + (size_t)e * d;
-    u32x4 wv[MAXIT];
-#pragma unroll
-    for (int it = 0; it < MAXIT; ++it)
-      wv[it] = it < nit ? *(const u32x4 *)(wr + (it * 64 + lane) * 8) : u32x4{0u, 0u, 0u, 0u};
     float s0 = 0.f, s1 = 0.f;
 #pragma unroll
-    for (int it = 0; it < MAXIT; ++it) {
-      if (it >= nit) break;
+    for (int it = 0; it < NIT; ++it) {
       const int base = (it * 64 + lane) * 8;
 #pragma unroll
       for (int h = 0; h < 4; ++h) {
-        const float w0 = __uint_as_float(wv[it][h] << 16), w1 = __uint_as_float(wv[it][h] & 0xffff0000u);
+        const float w0 = __uint_as_float(wv[q][it][h] << 16), w1 = __uint_as_float(wv[q][it][h] & 0xffff0000u);
         if (prim) s0 = fmaf(u[0][base + 2 * h + 1], w1, fmaf(u[0][base + 2 * h], w0, s0));
         if (br) s1 = fmaf(u[1][base + 2 * h + 1], w1, fmaf(u[1][base + 2 * h], w0, s1));
       }
@@ -545,7 +562,18 @@ hipError_t launch_moe_gemm_t(const MoeGemm &a, int MB, hipStream_t st) {
 }  // namespace
 
 hipError_t launch_moe_route(const MoeRoute &a, hipStream_t st) {
-  hipLaunchKernelGGL(k_moe_logits, dim3(a.rows.B, (a.E + 15) / 16), dim3(256), 0, st, a);
+  if (a.E < 1 || a.E > 256 || a.d % 512 != 0 || a.d > 4096) return hipErrorInvalidValue;
+  const dim3 grid(a.rows.B, (a.E + 15) / 16);
+  switch (a.d / 512) {
+    case 1: hipLaunchKernelGGL(k_moe_logits<1>, grid, dim3(256), 0, st, a); break;
+    case 2: hipLaunchKernelGGL(k_moe_logits<2>, grid, dim3(256), 0, st, a); break;
+    case 3: hipLaunchKernelGGL(k_moe_logits<3>, grid, dim3(256), 0, st, a); break;
+    case 4: hipLaunchKernelGGL(k_moe_logits<4>, grid, dim3(256), 0, st, a); break;
+    case 5: hipLaunchKernelGGL(k_moe_logits<5>, grid, dim3(256), 0, st, a); break;
+    case 6: hipLaunchKernelGGL(k_moe_logits<6>, grid, dim3(256), 0, st, a); break;
+    case 7: hipLaunchKernelGGL(k_moe_logits<7>, grid, dim3(256), 0, st, a); break;
+    default: hipLaunchKernelGGL(k_moe_logits<8>, grid, dim3(256), 0, st, a); break;
+  }
   hipLaunchKernelGGL(k_moe_topk, dim3(a.rows.B), dim3(64), 0, st, a);
   return hipGetLastError();
 }
