@@ -363,14 +363,14 @@ class Session:
         torch.cuda.current_stream().synchronize()
         return t
 
-    def decode(self, tokens=None, h1=None, h2=None, branch_on=True, grouped=True, batch=None):
+    def decode(self, tokens=None, h1=None, h2=None, branch_on=True, grouped=True, batch=None, logits=True):
         torch = self.torch
         tk = None if tokens is None else torch.as_tensor(np.asarray(tokens, np.int32)).to(self.device)
         h1d = None if h1 is None else torch.as_tensor(np.ascontiguousarray(h1, np.float32)).to(self.device)
         h2d = None if h2 is None else torch.as_tensor(np.ascontiguousarray(h2, np.float32)).to(self.device)
         B = batch if batch is not None else (len(tokens) if tokens is not None else h1.shape[0])
         sin = self.step_in(B, tk, h1d, h2d)
-        out, t = self.outputs(B, routing=True)
+        out, t = self.outputs(B, logits=logits, routing=True)
         if grouped:
             dbt_decode_step(self.model, self.kv, sin, int(branch_on), out, self.stream)
         else:

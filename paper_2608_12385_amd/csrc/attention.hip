@@ -40,6 +40,16 @@ __device__ __forceinline__ bool split_range(int npages, int target, int s, int *
   return *pb < *pe;
 }
 
+// Factor of physical row R whose QKV projection took its rows straight from
+// the step inputs (XNorm): 1/rms of the row from the per-split sums of
+// squares, added in split order (1 otherwise: the sums are left as they are).
+__device__ __forceinline__ float row_scale(const QKVFinish &f, int R) {
+  if (!f.ss) return 1.f;
+  float t = 0.f;
+  for (int k = 0; k < f.ss_S; ++k) t += f.ss[(size_t)k * f.ss_ld + R];
+  return 1.0f / sqrtf(t / (float)f.d_model + f.eps);
+}
+
 // Requires d_h == 128 and np*G <= 16.
 // <4, false>: one split of the sequence per workgroup of four waves (at most
 // 128 pages, two page ids per lane), partials merged by k_attn_combine.
@@ -304,6 +314,18 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
 #pragma unroll
         for (int j = 0; j < 4; ++j) v[k][j] = f.part[min(k, f.S - 1) * f.split_stride + idx[j]];
     }
+    // rows from the step inputs (f.ss): the row sums of squares of the
+    // thread's rows (path p0 + pp; the appended entry is the primary's),
+    // eight splits as unconditional loads like the slabs
+    float sv[2][8];
+    const int srow0 = a.rows.p0 * a.rows.Bp + b, srow1 = srow0 + a.rows.Bp;
+    if (ncol > 0 && f.ss) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        sv[0][k] = f.ss[(size_t)min(k, f.ss_S - 1) * f.ss_ld + srow0];
+        sv[1][k] = f.ss[(size_t)min(k, f.ss_S - 1) * f.ss_ld + (u < 0 && np > 1 ? srow1 : srow0)];
+      }
+    }
     float2 csi = make_float2(0.f, 0.f), aa = make_float2(0.f, 0.f), q1 = make_float2(0.f, 0.f);
     int page = 0;
     if (ncol > 0) {
@@ -329,6 +351,22 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
 #pragma unroll
         for (int j = 0; j < 4; ++j)
           if (j < ncol) x[j] += f.part[k * f.split_stride + idx[j]];
+      if (f.ss) {
+        // RMSNorm of the input row applied after the projection (see XNorm)
+        float rs[2];
+#pragma unroll
+        for (int pp = 0; pp < 2; ++pp) {
+          float t2 = 0.f;
+#pragma unroll
+          for (int k = 0; k < 8; ++k) t2 += k < f.ss_S ? sv[pp][k] : 0.f;
+          for (int k = 8; k < f.ss_S; ++k) t2 += f.ss[(size_t)k * f.ss_ld + (pp ? srow1 : srow0)];
+          rs[pp] = 1.0f / sqrtf(t2 / (float)f.d_model + f.eps);
+        }
+        x[0] *= rs[0];
+        x[1] *= rs[0];
+        x[2] *= rs[1];
+        x[3] *= rs[1];
+      }
       if (u < 0) {
         if (prim) {
           // Q1 = RoPE(.) (Eqs. (8)-(9)), kept for a later branch pass when asked
@@ -352,8 +390,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
             qs[pp * G + hh][i + DH / 2] = couple(aa.y, q1.y, q2.y);
           }
         for (int pp = 2; pp < np; ++pp) {
-          const float2 q2 = rope_pair(psum(f.part, f.split_stride, f.S, at(a.rows.p0 + pp, c0)),
-                                      psum(f.part, f.split_stride, f.S, at(a.rows.p0 + pp, c1)), csi);
+          const float rsp = row_scale(f, (a.rows.p0 + pp) * a.rows.Bp + b);
+          const float2 q2 = rope_pair(psum(f.part, f.split_stride, f.S, at(a.rows.p0 + pp, c0)) * rsp,
+                                      psum(f.part, f.split_stride, f.S, at(a.rows.p0 + pp, c1)) * rsp, csi);
           qs[pp * G + hh][i] = couple(aa.x, q1.x, q2.x);
           qs[pp * G + hh][i + DH / 2] = couple(aa.y, q1.y, q2.y);
         }
@@ -373,15 +412,16 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
         if (u2 < 0) continue;  // queries: all in the first pass (G <= NW)
         const int page2 = ptab[pos >> 4];
         const float2 cs2 = f.rope[(size_t)pos * (DH / 2) + u2 % (DH / 2)];
+        const float rs0 = row_scale(f, b);
         if (u2 < DH / 2) {
           const int k0 = dq + g * DH + u2;
-          const float2 k = rope_pair(psum(f.part, f.split_stride, f.S, at(0, k0)),
-                                     psum(f.part, f.split_stride, f.S, at(0, k0 + DH / 2)), cs2);
+          const float2 k = rope_pair(psum(f.part, f.split_stride, f.S, at(0, k0)) * rs0,
+                                     psum(f.part, f.split_stride, f.S, at(0, k0 + DH / 2)) * rs0, cs2);
           uint16_t *kc = (uint16_t *)a.kv.k + (((size_t)page2 * n_kv + g) * 16 + (pos & 15)) * DH;
           kc[u2] = f2bf(k.x);
           kc[u2 + DH / 2] = f2bf(k.y);
         } else {
-          const float vv = psum(f.part, f.split_stride, f.S, at(0, dq + dkv + g * DH + u2 - DH / 2));
+          const float vv = psum(f.part, f.split_stride, f.S, at(0, dq + dkv + g * DH + u2 - DH / 2)) * rs0;
           ((uint16_t *)a.kv.v)[(((size_t)page2 * n_kv + g) * DH + u2 - DH / 2) * 16 + (pos & 15)] = f2bf(vv);
         }
       }

@@ -75,7 +75,7 @@ struct Layout {
   size_t moe_idx = 0, moe_logits = 0, moe_w = 0, moe_aslot = 0, moe_counts = 0, moe_offsets = 0, moe_arow = 0, moe_h = 0,
          moe_y = 0, ret_idx = 0;
   size_t rope = 0, pos = 0, S = 0, Xn = 0, Xh = 0, Q = 0, O = 0, P = 0, apart = 0, astat = 0,
-         logits = 0, mstats = 0, ret_q = 0, ret_h = 0, ret_m = 0, ret_a = 0, btok = 0, slast = 0,
+         logits = 0, mstats = 0, xss = 0, ret_q = 0, ret_h = 0, ret_m = 0, ret_a = 0, btok = 0, slast = 0,
          state_total = 0, total = 0;  // [0, state_total): state; [state_total, total): step buffers
 };
 
@@ -202,6 +202,7 @@ Layout make_layout(const dbt_config *c) {
   L.nstat = gemm_stats_tiles(std::max(c->vocab, 1), L.g_lm, c->dtype);
   if (L.nstat == 0) L.nstat = std::max(L.nch, 1);
   L.mstats = take((size_t)L.R_max * L.nstat * 3 * 4);
+  L.xss = take((size_t)std::max(L.g_qkv.S, 1) * L.R_max * 4);
   if (L.moe) {
     L.amax = L.rows_max * 8;
     L.moe_idx = take((size_t)L.rows_max * 8 * 4);
@@ -369,7 +370,40 @@ struct LayerCall {
   int rows_layout;   // prefill: T; decode: (1 + n_branches)*Bp
   bool last_norm;    // apply the next norm after the layer
   const dbt_step_out *out;  // routing outputs (MoE), may be NULL
+  // layer 0 reads its rows straight from the step inputs (XNorm; no norm
+  // kernel before it) when set; sb is then applied by its QKV projection
+  const HIn *hin;
+  const StepBegin *sb;
 };
+
+// Whether the decode step's attention kernel finishes the QKV projection
+// (split-K sums, rotary embedding, query coupling, cache append) for a batch
+// of B sequences whose longest cache is maxlen positions after the append.
+bool attn_finishes_qkv(const dbt_model *m, int B, int maxlen, bool *single_out = nullptr);
+
+// Whether the first layer of a layer-only model takes its rows straight from
+// the step inputs (XNorm) for a decode step of B sequences.  Decided from
+// the model and batch only, so the grouped, primary-only and two-pass steps
+// (and a branch pass) all use the same arithmetic for a row.
+bool input_fold(const dbt_model *m, const dbt_kv *kv, int B);
+
+bool attn_finishes_qkv(const dbt_model *m, int B, int maxlen, bool *single_out) {
+  const dbt_config &cf = m->cfg;
+  const bool single = cf.dtype == DBT_BF16 && B * cf.n_kv_heads >= 256 && (maxlen + kPage - 1) / kPage <= 1024;
+  if (single_out) *single_out = single;
+  return cf.dtype == DBT_BF16 && cf.head_dim == 128 && cf.n_q_heads / cf.n_kv_heads <= (single || m->L.wide ? 8 : 4);
+}
+
+bool input_fold(const dbt_model *m, const dbt_kv *kv, int B) {
+  const dbt_config &cf = m->cfg;
+  if (cf.has_embeddings || cf.dtype != DBT_BF16 || cf.d_model % 128) return false;
+  int maxlen = 0;
+  for (int b = 0; b < B; ++b) maxlen = std::max(maxlen, kv->len[b] + 1);
+  // the largest call of a step: every path's rows, or the primary's alone
+  // when only it attends (compute-matched)
+  const int Bp = round16(B), M = (cf.compute_matched ? 1 : 1 + n_branches(cf)) * Bp;
+  return attn_finishes_qkv(m, B, maxlen) && gemm_xnorm_ok(m->L.g_qkv, M);
+}
 
 // MoE MLP of layer l for the active rows: route, dispatch, touched experts,
 // shared expert (with the b coupling), combine (with the c coupling).
@@ -556,9 +590,11 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
   // only and the branch takes g_A * A1 in the residual step.
   const bool cm = cf.compute_matched != 0;
   float *ret_a = cm ? m->at<float>(L.ret_a) + rq * d : nullptr;
+  const HIn hin0 = l == 0 && c.hin ? *c.hin : HIn{};
   if (cm && c.mode == MODE_BRANCH) {
+    if (hin0.h1 && c.sb) HIPCHK(launch_step_begin(*c.sb, m->at<int>(L.pos), kv->page_table, kv->mpps, st));
     HIPCHK(launch_resid_norm(P, 0, 0, d, S, W.mlp_norm, cf.rms_eps, d, cf.dtype, c.rows, Xn, d, st,
-                             GatedCopy{W.g_attn_copy, ret_a, Retain{}}));
+                             GatedCopy{W.g_attn_copy, ret_a, Retain{}}, hin0));
     return run_moe_mlp(m, l, c, st);
   }
   const Rows arows = cm ? Rows{c.rows.B, c.rows.Bp, 0, 1} : c.rows;
@@ -598,9 +634,34 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
     tq.ret_dst = c.ret_dst;
   }
   const bool qkv_fused = tq.rope && gemm_tile_args_ok(tq, false);
+  // Decode on the bf16 cache: the attention kernel finishes the queries and
+  // appends the cache entry itself.
+  int maxlen = 0;
+  if (!c.prefill)
+    for (int b = 0; b < c.rows.B; ++b) maxlen = std::max(maxlen, kv->len[b] + 1);
+  bool attn_single = false;
+  const bool finish_in_attn = !c.prefill && attn_finishes_qkv(m, c.rows.B, maxlen, &attn_single);
+  const bool xin = l == 0 && c.hin && c.hin->h1;
+  if (xin && (c.prefill || !finish_in_attn || cf.dtype != DBT_BF16 || !gemm_xnorm_ok(g_qkv, aM)))
+    return fail(DBT_ERR_STATE, "internal: first-layer input fold on an unsupported call");
   if (qkv_fused) {
     Timed tm(m, DBT_STAGE_QKV, st);
     HIPCHK(launch_gemm_tile(tq, false, st));
+  } else if (xin) {
+    XNorm xn{};
+    xn.h = *c.hin;
+    xn.rows = arows;
+    xn.g = W.attn_norm;
+    xn.ss = m->at<float>(L.xss);
+    xn.ss_ld = L.R_max;
+    if (c.sb) {
+      xn.sb = *c.sb;
+      xn.pos_arr = m->at<int>(L.pos);
+      xn.page_table = kv->page_table;
+      xn.mpps = kv->mpps;
+    }
+    Timed tm(m, DBT_STAGE_QKV, st);
+    HIPCHK(launch_gemm_xnorm(qkv, nq, d, xn, aM, P + (size_t)axrow0 * nq, nq, stride, g_qkv, st));
   } else {
     Timed tm(m, DBT_STAGE_QKV, st);
     HIPCHK(project(qkv, nq, d, Xn + (size_t)axrow0 * d * es, d, aM, P + (size_t)axrow0 * nq, nq, stride, g_qkv));
@@ -624,15 +685,13 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
   qf.ret = Retain{c.retain && !cm ? ret_q : nullptr, c.ret_src, c.ret_dst};
   qf.kv = kvl;
   qf.dtype = cf.dtype;
-  // Decode on the bf16 cache: the attention kernel finishes the queries and
-  // appends the cache entry itself.
-  int maxlen = 0;
-  if (!c.prefill)
-    for (int b = 0; b < c.rows.B; ++b) maxlen = std::max(maxlen, kv->len[b] + 1);
-  const bool attn_single = !c.prefill && cf.dtype == DBT_BF16 && c.rows.B * cf.n_kv_heads >= 256 &&
-                           (maxlen + kPage - 1) / kPage <= 1024;
-  const bool finish_in_attn = !c.prefill && cf.dtype == DBT_BF16 && cf.head_dim == 128 &&
-                              cf.n_q_heads / cf.n_kv_heads <= (attn_single || L.wide ? 8 : 4);
+  if (xin) {
+    qf.ss = m->at<float>(L.xss);
+    qf.ss_ld = L.R_max;
+    qf.ss_S = S_qkv;
+    qf.d_model = d;
+    qf.eps = cf.rms_eps;
+  }
   if (!qkv_fused && !finish_in_attn) HIPCHK(launch_qkv_finish(qf, st));
 
   // 2. attention over the primary cache
@@ -675,7 +734,7 @@ dbt_status run_layer(dbt_model *m, dbt_kv *kv, int l, const LayerCall &c, hipStr
   }
   const GatedCopy gca = cm ? GatedCopy{W.g_attn_copy, ret_a, Retain{c.retain ? ret_a : nullptr, c.ret_src, c.ret_dst}}
                            : GatedCopy{};
-  HIPCHK(launch_resid_norm(P, stride, S_o, d, S, W.mlp_norm, cf.rms_eps, d, cf.dtype, c.rows, Xn, d, st, gca));
+  HIPCHK(launch_resid_norm(P, stride, S_o, d, S, W.mlp_norm, cf.rms_eps, d, cf.dtype, c.rows, Xn, d, st, gca, hin0));
 
   if (L.moe) return run_moe_mlp(m, l, c, st);
 
@@ -854,9 +913,11 @@ dbt_status copy_rows(float *dst, const float *src, int B, int d, hipStream_t st)
 }
 
 // Branch-only pass over all layers (ungrouped pass 2 and the boundary).
-dbt_status branch_pass(dbt_model *m, dbt_kv *kv, int B, int Bp, hipStream_t st, const dbt_step_out *out = nullptr) {
+dbt_status branch_pass(dbt_model *m, dbt_kv *kv, int B, int Bp, hipStream_t st, const dbt_step_out *out = nullptr,
+                       const HIn *hin = nullptr) {
   LayerCall lc{};
   lc.out = out;
+  lc.hin = hin;
   const int nb = n_branches(m->cfg);
   lc.rows = Rows{B, Bp, 1, nb};
   lc.mode = MODE_BRANCH;
@@ -891,8 +952,14 @@ dbt_status decode_step_impl(dbt_model *m, dbt_kv *kv, const dbt_step_in *in, int
   const bool on = branch_on != 0;
   const int nb = n_branches(cf);
   const Rows rows{B, Bp, 0, on ? 1 + nb : 1};
-  if ((s = load_inputs(m, kv, in, in->tokens, rows, st, &sb))) return s;
+  const bool fold = input_fold(m, kv, B);
+  const HIn hin{in->h1_in, in->h2_in, B};
+  if (!fold && (s = load_inputs(m, kv, in, in->tokens, rows, st, &sb))) return s;
   LayerCall lc{};
+  if (fold) {
+    lc.hin = &hin;
+    lc.sb = &sb;
+  }
   lc.rows = rows;
   lc.mode = on ? MODE_GROUPED : MODE_PRIMARY;
   lc.retain = false;
@@ -1095,8 +1162,14 @@ dbt_status dbt_decode_step_ungrouped(dbt_model *m, dbt_kv *kv, const dbt_step_in
   if ((s = flush(kv, pos.data(), B, st, &sb))) return s;
   // pass 1: every primary layer, keeping Q1, H1, M1
   const Rows prim{B, Bp, 0, 1};
-  if ((s = load_inputs(m, kv, in, in->tokens, prim, st, &sb))) return s;
+  const bool fold = input_fold(m, kv, B);
+  const HIn hin{in->h1_in, in->h2_in, B};
+  if (!fold && (s = load_inputs(m, kv, in, in->tokens, prim, st, &sb))) return s;
   LayerCall lc{};
+  if (fold) {
+    lc.hin = &hin;
+    lc.sb = &sb;
+  }
   lc.rows = prim;
   lc.mode = MODE_PRIMARY;
   lc.retain = true;
@@ -1110,8 +1183,8 @@ dbt_status dbt_decode_step_ungrouped(dbt_model *m, dbt_kv *kv, const dbt_step_in
   if (cf.vocab > 0 && (s = lm_head(m, prim, st))) return s;
   // pass 2: every branch layer
   const Rows br{B, Bp, 1, n_branches(cf)};
-  if ((s = load_inputs(m, kv, in, in->tokens, br, st))) return s;
-  if ((s = branch_pass(m, kv, B, Bp, st, out))) return s;
+  if (!fold && (s = load_inputs(m, kv, in, in->tokens, br, st))) return s;
+  if ((s = branch_pass(m, kv, B, Bp, st, out, fold ? &hin : nullptr))) return s;
   for (int b = 0; b < B; ++b) kv->len[b] += 1;
   if (out) {
     if ((s = readout(m, B, Bp, true, out, st))) return s;

@@ -278,11 +278,15 @@ __global__ void k_qkv_finish(QKVFinish f) {
 // call) or the kept A1 (branch-only call); primary rows can keep A1.
 template <typename T, int R>
 __global__ void k_resid_norm(const float *part, long long stride, int S, int ldp, float *Sres,
-                             const float *g, float eps, int d, Rows rows, T *Xn, int ldx, GatedCopy gc) {
+                             const float *g, float eps, int d, Rows rows, T *Xn, int ldx, GatedCopy gc, HIn hin) {
   __shared__ float red[16];
   const int b = blockIdx.x, path = rows.p0 + blockIdx.y;
   const int row = phys_row(rows, path, b);
   float4 *s = (float4 *)(Sres + (size_t)row * d);
+  // the residual: Sres, or the step input of the row (first layer, XNorm)
+  const float4 *sin = hin.h1 ? (const float4 *)((path == 0 ? hin.h1 : hin.h2 + (size_t)(path - 1) * hin.B * d) +
+                                                (size_t)b * d)
+                             : s;
   const bool keep = gc.g && path == 0 && gc.ret.ptr && (gc.ret.src_row < 0 || gc.ret.src_row == b);
   float4 *kept = keep ? (float4 *)(gc.ret.ptr + (size_t)(gc.ret.src_row < 0 ? b : gc.ret.dst_row) * d) : nullptr;
   const int r1 = phys_row(rows, 0, b);
@@ -296,7 +300,7 @@ __global__ void k_resid_norm(const float *part, long long stride, int S, int ldp
     if (!gc.g || path == 0) {
       float4 sl[8];
       slabs_issue(part, stride, S, ((size_t)row * ldp) / 4 + i, sl);
-      const float4 x = s[i];
+      const float4 x = sin[i];
       __builtin_amdgcn_sched_barrier(0);  // the sums after every load
       const float4 a1 = slabs_sum(part, stride, S, ((size_t)row * ldp) / 4 + i, sl);
       v[k] = add4(x, a1);
@@ -306,7 +310,7 @@ __global__ void k_resid_norm(const float *part, long long stride, int S, int ldp
       const float4 a1 = rows.p0 == 0 ? psum4(part, stride, S, ((size_t)r1 * ldp) / 4 + i)
                                      : ((const float4 *)(gc.in + (size_t)b * d))[i];
       const float4 ga = ((const float4 *)gc.g)[i];
-      const float4 x = s[i];
+      const float4 x = sin[i];
       v[k] = make_float4(x.x + ga.x * a1.x, x.y + ga.y * a1.y, x.z + ga.z * a1.z, x.w + ga.w * a1.w);
     }
     s[i] = v[k];
@@ -490,12 +494,13 @@ __global__ void k_mix_stats(MixArgs m) {
 // never be the fp32 argmax), and every entry of a kept tile is evaluated.
 // With the branches off the value is the primary logit itself and only tiles
 // attaining the row maximum are scanned.  The lowest index wins ties.  The
-// kernel is short: one memory round trip for the statistics and one per kept
-// tile, and little code (a cold instruction cache is a large part of such a
-// kernel's time).
-template <int NP>
+// kernel is short: one memory round trip for the statistics and one for up
+// to 16 kept tiles (float4 loads of 8 x 4 entries per thread and path), and
+// little code (a cold instruction cache is a large part of such a kernel's
+// time).
+template <int NP, int VEC>
 __global__ __launch_bounds__(256) void k_mix_select(MixArgs m) {
-  constexpr int SB = 8, MAXT = 4096;
+  constexpr int SB = VEC == 1 ? 8 : (NP <= 2 ? 8 : 4), MAXT = 4096;
   __shared__ float red[NP][3][4];
   __shared__ float lb_s[4];
   __shared__ int list[MAXT];
@@ -619,31 +624,47 @@ __global__ __launch_bounds__(256) void k_mix_select(MixArgs m) {
     __syncthreads();
   }
   nkeep = min(nkeep, MAXT);
-  const int tw = m.tile_w, total = nkeep * tw;
+  // units of VEC consecutive entries (VEC divides the tile width and V, so
+  // a unit never straddles a tile or the end); loads are unconditional (an
+  // entry past the list re-reads the last unit and is not merged)
+  const int tw = m.tile_w, units = tw / VEC, total = nkeep * units;
   float best = -INFINITY;
   int bi = 0x7fffffff;
   for (int e0 = 0; e0 < total; e0 += 256 * SB) {
     int vi[SB];
-    float a[NP][SB];
+    float a[NP][SB][VEC];
 #pragma unroll
     for (int i = 0; i < SB; ++i) {
-      const int e = e0 + t + 256 * i;
-      vi[i] = e < total ? list[e / tw] * tw + e % tw : m.V;
+      const int e = e0 + t + 256 * i, k = e < total ? e / units : 0;
+      vi[i] = e < total ? list[k] * tw + (e - k * units) * VEC : m.V;
+      const int vc = min(vi[i], m.V - VEC);
 #pragma unroll
-      for (int j = 0; j < NP; ++j) a[j][i] = vi[i] < m.V ? z[j][vi[i]] : -INFINITY;
-    }
-#pragma unroll
-    for (int i = 0; i < SB; ++i) {
-      if (vi[i] >= m.V) continue;
-      float val = a[0][i];
-      if (NP > 1) {
-        float qs = 0.f;
-#pragma unroll
-        for (int j = 1; j < NP; ++j) qs += __expf(a[j][i] - lse[j]);
-        val = alpha * __expf(a[0][i] - lse[0]) + wq * qs;
+      for (int j = 0; j < NP; ++j) {
+        if constexpr (VEC == 4) {
+          const float4 x = *(const float4 *)(z[j] + vc);
+          a[j][i][0] = x.x;
+          a[j][i][1] = x.y;
+          a[j][i][2] = x.z;
+          a[j][i][3] = x.w;
+        } else {
+          a[j][i][0] = z[j][vc];
+        }
       }
-      argmax_merge(best, bi, val, vi[i]);
     }
+#pragma unroll
+    for (int i = 0; i < SB; ++i)
+#pragma unroll
+      for (int c = 0; c < VEC; ++c) {
+        if (vi[i] + c >= m.V) continue;
+        float val = a[0][i][c];
+        if (NP > 1) {
+          float qs = 0.f;
+#pragma unroll
+          for (int j = 1; j < NP; ++j) qs += __expf(a[j][i][c] - lse[j]);
+          val = alpha * __expf(a[0][i][c] - lse[0]) + wq * qs;
+        }
+        argmax_merge(best, bi, val, vi[i] + c);
+      }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
@@ -744,6 +765,7 @@ hipError_t launch_rmsnorm_rows(const float *S, const float *g, float eps, int d,
 }
 
 hipError_t launch_qkv_finish(const QKVFinish &f, hipStream_t st) {
+  if (f.ss) return hipErrorInvalidValue;  // rows from the step inputs: finished by the attention kernel only
   const int half = f.d_h / 2;
   const int total = f.mode != MODE_BRANCH ? (f.n_q + 2 * f.n_kv) * half : f.n_q * half;
   dim3 grid((total + 255) / 256, f.rows.B);
@@ -756,14 +778,15 @@ hipError_t launch_qkv_finish(const QKVFinish &f, hipStream_t st) {
 
 hipError_t launch_resid_norm(const float *part, long long stride, int S, int ldp, float *Sres,
                              const float *g, float eps, int d, int dtype, Rows rows, void *Xn, int ldx,
-                             hipStream_t st, const GatedCopy &gc) {
+                             hipStream_t st, const GatedCopy &gc, const HIn &hin) {
   dim3 grid(rows.B, rows.np);
+  if (hin.h1 && hin.B < rows.B) return hipErrorInvalidValue;
   if (dtype == 1) {
     DBT_ROW_LAUNCH(k_resid_norm, uint16_t, d, grid, dim3(row_threads(d)), 0, st, part, stride, S, ldp, Sres, g, eps,
-                   d, rows, (uint16_t *)Xn, ldx, gc)
+                   d, rows, (uint16_t *)Xn, ldx, gc, hin)
   } else {
     DBT_ROW_LAUNCH(k_resid_norm, float, d, grid, dim3(row_threads(d)), 0, st, part, stride, S, ldp, Sres, g, eps, d,
-                   rows, (float *)Xn, ldx, gc)
+                   rows, (float *)Xn, ldx, gc, hin)
   }
   return hipGetLastError();
 }
@@ -816,11 +839,18 @@ hipError_t launch_mixture(const MixArgs &m, hipStream_t st) {
     hipLaunchKernelGGL(k_mix_stats, dim3(nch, m.rows.np * m.rows.B), dim3(256), 0, st, m);
   }
   const dim3 grid(m.rows.B), block(256);
-  switch (m.rows.np) {
-    case 1: hipLaunchKernelGGL(k_mix_select<1>, grid, block, 0, st, m); break;
-    case 2: hipLaunchKernelGGL(k_mix_select<2>, grid, block, 0, st, m); break;
-    case 3: hipLaunchKernelGGL(k_mix_select<3>, grid, block, 0, st, m); break;
-    default: hipLaunchKernelGGL(k_mix_select<4>, grid, block, 0, st, m); break;
+  // float4 units when rows are 16-byte aligned and units stay inside tiles;
+  // the primary alone keeps scalar loads (its scan reads about one tile, and
+  // the wider loop's code costs more than it saves there)
+  const bool v4 = m.rows.np > 1 && m.V % 4 == 0 && m.tile_w % 4 == 0;
+  switch (m.rows.np * 2 + (v4 ? 1 : 0)) {
+    case 2: hipLaunchKernelGGL((k_mix_select<1, 1>), grid, block, 0, st, m); break;
+    case 4: hipLaunchKernelGGL((k_mix_select<2, 1>), grid, block, 0, st, m); break;
+    case 5: hipLaunchKernelGGL((k_mix_select<2, 4>), grid, block, 0, st, m); break;
+    case 6: hipLaunchKernelGGL((k_mix_select<3, 1>), grid, block, 0, st, m); break;
+    case 7: hipLaunchKernelGGL((k_mix_select<3, 4>), grid, block, 0, st, m); break;
+    case 8: hipLaunchKernelGGL((k_mix_select<4, 1>), grid, block, 0, st, m); break;
+    default: hipLaunchKernelGGL((k_mix_select<4, 4>), grid, block, 0, st, m); break;
   }
   return hipGetLastError();
 }

@@ -72,11 +72,19 @@ constexpr int lcm3(int a, int b, int c) {
 // Y the epilogue finishes the MLP intermediate in registers (see GluEpi):
 // the branch rows' coupling partner, the primary row of the same sequence,
 // is held by the same lane.
-template <int MB, int RB, int PD, int NW, bool GLU = false, int XA = 2>
+// XF: the activations are the fp32 inputs of XNorm (first layer of a
+// layer-only model): each staged piece is bf16(h * g), and the workgroups of
+// the first row tile write each row's sum of squares of h over their split
+// (the 16 pieces of a chunk row sit in 16 consecutive lanes; summed over the
+// chunks in order, then across the lanes by a fixed butterfly).
+struct NoX {};
+template <bool XF> using XArg = std::conditional_t<XF, XNorm, NoX>;
+
+template <int MB, int RB, int PD, int NW, bool GLU = false, int XA = 2, bool XF = false>
 __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const uint16_t *__restrict__ X, int ldx,
                                                        int M, float *__restrict__ Y, int ldy,
                                                        long long y_split_stride, float *__restrict__ row_stats,
-                                                       GluEpi ep) {
+                                                       GluEpi ep, XArg<XF> xa) {
   constexpr int XR = 16 * MB;
   constexpr int PIECES = XR * (kChunk / 8);  // 16-byte pieces of one activation chunk
   constexpr int PPT = (PIECES + NW * 64 - 1) / (NW * 64);
@@ -128,13 +136,31 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
   __shared__ u32x4 wt[NW][RB * 16 * 8];
   u32x4 *wreg = wt[wave];
   const uint16_t *xsrc[PPT];
-  int xdst[PPT];
+  const float *xsf[PPT];  // XF: the piece's fp32 input row
+  int xdst[PPT], gcol[PPT];
 #pragma unroll
   for (int j = 0; j < PPT; ++j) {
     const int p = t + NW * 64 * j, row = min(p >> 4, XR - 1), col = (p & 15) * 8;
     xsrc[j] = X + (size_t)min(m0 + row, M - 1) * ldx + kbeg + col;
     xdst[j] = p < PIECES ? row * kLdsRow + col : -1;
+    gcol[j] = kbeg + col;
+    if constexpr (XF) {
+      const int mm = min(m0 + row, M - 1);
+      const int path = xa.rows.p0 + mm / xa.rows.Bp, b = min(mm % xa.rows.Bp, xa.h.B - 1);
+      xsf[j] = (path == 0 ? xa.h.h1 : xa.h.h2 + (size_t)(path - 1) * xa.h.B * K) + (size_t)b * K + kbeg + col;
+    }
   }
+  if constexpr (XF) {
+    // the step's positions and new page-table entries, for the kernels after
+    // this one (the first to read them is the attention)
+    if (blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0 && xa.pos_arr) {
+      if (t < xa.sb.n_pos) xa.pos_arr[xa.sb.b0 + t] = xa.sb.pos[t];
+      if (t < xa.sb.n_pt) xa.page_table[(size_t)xa.sb.pt_b[t] * xa.mpps + xa.sb.pt_slot[t]] = xa.sb.pt_page[t];
+    }
+  }
+  float ssq[PPT];  // XF: sums of squares of the staged pieces
+#pragma unroll
+  for (int j = 0; j < PPT; ++j) ssq[j] = 0.f;
 
   floatx4 acc[RB][MB];
 #pragma unroll
@@ -144,6 +170,9 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
 
   static_assert(XA >= 2, "activation chunks are loaded at least two steps ahead");
   u32x4 a[PD][RB][4], stg[XA][PPT];
+  // XF: h of each piece (two float4) and g of their columns (two float4:
+  // every piece of a thread has the same columns, NW*64 being a multiple of 16)
+  float4 stf[XF ? XA : 1][XF ? PPT : 1][2], stg_g[XF ? XA : 1][2];
   auto koff = [&](int c) {  // logical chunk c (clamped) of this workgroup's rotated order
     c = min(c, nch - 1) + crot;
     return (c >= nch ? c - nch : c) * kChunk;
@@ -151,7 +180,18 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
   auto xload = [&](int slot, int c) {
     const int ko = koff(c);
 #pragma unroll
-    for (int j = 0; j < PPT; ++j) stg[slot][j] = *(const u32x4 *)(xsrc[j] + ko);
+    for (int j = 0; j < PPT; ++j) {
+      if constexpr (XF) {
+        stf[slot][j][0] = *(const float4 *)(xsf[j] + ko);
+        stf[slot][j][1] = *(const float4 *)(xsf[j] + ko + 4);
+        if (j == 0) {
+          stg_g[slot][0] = *(const float4 *)(xa.g + gcol[0] + ko);
+          stg_g[slot][1] = *(const float4 *)(xa.g + gcol[0] + ko + 4);
+        }
+      } else {
+        stg[slot][j] = *(const u32x4 *)(xsrc[j] + ko);
+      }
+    }
   };
   // a[slot][rb][2h + j]: half h of row group j of row block rb
   auto wload = [&](int slot, int c) {
@@ -167,7 +207,17 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
   auto xstore = [&](int lds, int slot) {
 #pragma unroll
     for (int j = 0; j < PPT; ++j)
-      if (PIECES % (NW * 64) == 0 || xdst[j] >= 0) *(u32x4 *)(&xs[lds][xdst[j]]) = stg[slot][j];
+      if (PIECES % (NW * 64) == 0 || xdst[j] >= 0) {
+        if constexpr (XF) {
+          const float4 u = stf[slot][j][0], v = stf[slot][j][1], gu = stg_g[slot][0], gv = stg_g[slot][1];
+          ssq[j] += ((u.x * u.x + u.y * u.y) + (u.z * u.z + u.w * u.w)) +
+                    ((v.x * v.x + v.y * v.y) + (v.z * v.z + v.w * v.w));
+          *(u32x4 *)(&xs[lds][xdst[j]]) = u32x4{pack2(u.x * gu.x, u.y * gu.y), pack2(u.z * gu.z, u.w * gu.w),
+                                                pack2(v.x * gv.x, v.y * gv.y), pack2(v.z * gv.z, v.w * gv.w)};
+        } else {
+          *(u32x4 *)(&xs[lds][xdst[j]]) = stg[slot][j];
+        }
+      }
   };
   // multiply chunk c (weight ring slot w = c % PD, LDS slot par = c & 1);
   // load the activations of chunk c+XA (register slot xc = c % XA, whose
@@ -246,6 +296,19 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(WSegs segs, int K, const 
 #pragma unroll
     for (int u = 0; u + 1 < P2; ++u)
       if (c0 + u < nch) step(std::false_type{}, c0 + u, u % PD, u & 1, u % XA, (u + 1) % XA);
+  }
+  if constexpr (XF) {
+#pragma unroll
+    for (int j = 0; j < PPT; ++j) {
+      float v = ssq[j];
+      v += __shfl_xor(v, 1, 64);
+      v += __shfl_xor(v, 2, 64);
+      v += __shfl_xor(v, 4, 64);
+      v += __shfl_xor(v, 8, 64);
+      const int p = t + NW * 64 * j, row = p >> 4;
+      if (blockIdx.x == 0 && (p & 15) == 0 && p < PIECES && m0 + row < M)
+        xa.ss[(size_t)split * xa.ss_ld + xa.rows.p0 * xa.rows.Bp + m0 + row] = v;
+    }
   }
   // lane holds D[n = rb*16 + 4*gq + i][m = cb*16 + r]: Y[m][n .. n+3]
   if constexpr (GLU) {
@@ -510,24 +573,41 @@ void launch_mb(const GemmConfig &g, dim3 grid, hipStream_t st, const WSegs &segs
                int M, float *Y, int ldy, long long yss, float *rs) {
   const GluEpi none{};
   if (g.NW == 16)
-    hipLaunchKernelGGL((k_gemm_bf16<MB, 2, 1, 16>), grid, dim3(1024), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs, none);
+    hipLaunchKernelGGL((k_gemm_bf16<MB, 2, 1, 16>), grid, dim3(1024), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs, none, NoX{});
   else if (g.NW == 8 && g.RB == 2)
-    hipLaunchKernelGGL((k_gemm_bf16<MB, 2, 1, 8>), grid, dim3(512), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs, none);
+    hipLaunchKernelGGL((k_gemm_bf16<MB, 2, 1, 8>), grid, dim3(512), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs, none, NoX{});
   else if (g.NW == 8)
-    hipLaunchKernelGGL((k_gemm_bf16<MB, 1, 1, 8>), grid, dim3(512), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs, none);
+    hipLaunchKernelGGL((k_gemm_bf16<MB, 1, 1, 8>), grid, dim3(512), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs, none, NoX{});
   else if (g.RB == 2)
-    hipLaunchKernelGGL((k_gemm_bf16<MB, 2, 2, 4>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs, none);
+    hipLaunchKernelGGL((k_gemm_bf16<MB, 2, 2, 4>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs, none, NoX{});
   else
-    hipLaunchKernelGGL((k_gemm_bf16<MB, 1, 2, 4>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs, none);
+    hipLaunchKernelGGL((k_gemm_bf16<MB, 1, 2, 4>), grid, dim3(256), 0, st, segs, K, X, ldx, M, Y, ldy, yss, rs, none, NoX{});
 }
 
 template <int MB>
 void launch_glu_mb(dim3 grid, hipStream_t st, const WSegs &segs, int K, const uint16_t *X, int ldx, int M,
                    const GluEpi &ep) {
   hipLaunchKernelGGL((k_gemm_bf16<MB, 1, 2, 8, true>), grid, dim3(512), 0, st, segs, K, X, ldx, M, nullptr, 0, 0LL,
-                     nullptr, ep);
+                     nullptr, ep, NoX{});
+}
+
+template <int MB>
+void launch_xnorm_mb(const GemmConfig &g, dim3 grid, hipStream_t st, const WSegs &segs, int K, const XNorm &xn, int M,
+                     float *Y, int ldy, long long yss) {
+  const GluEpi none{};
+  if (g.NW == 8)
+    hipLaunchKernelGGL((k_gemm_bf16<MB, 1, 1, 8, false, 2, true>), grid, dim3(512), 0, st, segs, K, nullptr, 0, M, Y,
+                       ldy, yss, nullptr, none, xn);
+  else
+    hipLaunchKernelGGL((k_gemm_bf16<MB, 2, 2, 4, false, 2, true>), grid, dim3(256), 0, st, segs, K, nullptr, 0, M, Y,
+                       ldy, yss, nullptr, none, xn);
 }
 }  // namespace
+
+bool gemm_xnorm_ok(const GemmConfig &g, int M) {
+  // up to 96 stacked rows (more would spill the fp32 staging registers)
+  return M >= 1 && M <= 96 && ((g.NW == 8 && g.RB == 1 && g.PD == 1) || (g.NW == 4 && g.RB == 2 && g.PD == 2));
+}
 
 static int gemm_rows_per_wg(const GemmConfig &g) { return g.NW * 16 * g.RB; }
 
@@ -562,6 +642,27 @@ hipError_t launch_gemm_glu(const uint16_t *w_gate, const uint16_t *w_up, int f, 
     case 6: launch_glu_mb<6>(grid, st, segs, K, Xb, ldx, M, ep); break;
     case 7: launch_glu_mb<7>(grid, st, segs, K, Xb, ldx, M, ep); break;
     default: launch_glu_mb<8>(grid, st, segs, K, Xb, ldx, M, ep); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_xnorm(const WSegs &segs, int N, int K, const XNorm &xn, int M, float *Y, int ldy,
+                             long long y_split_stride, const GemmConfig &g, hipStream_t st) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  if (!gemm_xnorm_ok(g, M) || K % kChunk || !xn.h.h1 || !xn.g || !xn.ss || xn.rows.Bp < 1 || xn.h.B < 1)
+    return hipErrorInvalidValue;
+  const int mb_total = (M + 15) / 16;
+  const int MB = mb_total >= 8 ? 8 : mb_total;
+  dim3 grid((N + gemm_rows_per_wg(g) - 1) / gemm_rows_per_wg(g), g.S, (mb_total + MB - 1) / MB);
+  switch (MB) {
+    case 1: launch_xnorm_mb<1>(g, grid, st, segs, K, xn, M, Y, ldy, y_split_stride); break;
+    case 2: launch_xnorm_mb<2>(g, grid, st, segs, K, xn, M, Y, ldy, y_split_stride); break;
+    case 3: launch_xnorm_mb<3>(g, grid, st, segs, K, xn, M, Y, ldy, y_split_stride); break;
+    case 4: launch_xnorm_mb<4>(g, grid, st, segs, K, xn, M, Y, ldy, y_split_stride); break;
+    case 5: launch_xnorm_mb<5>(g, grid, st, segs, K, xn, M, Y, ldy, y_split_stride); break;
+    case 6: launch_xnorm_mb<6>(g, grid, st, segs, K, xn, M, Y, ldy, y_split_stride); break;
+    case 7: launch_xnorm_mb<7>(g, grid, st, segs, K, xn, M, Y, ldy, y_split_stride); break;
+    default: launch_xnorm_mb<8>(g, grid, st, segs, K, xn, M, Y, ldy, y_split_stride); break;
   }
   return hipGetLastError();
 }

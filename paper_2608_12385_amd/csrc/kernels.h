@@ -134,6 +134,31 @@ hipError_t launch_load_hidden(const float *h1, const float *h2, const float *g_n
 hipError_t launch_rmsnorm_rows(const float *S, const float *g, float eps, int d, int dtype,
                                Rows rows, void *Xn, int ldx, hipStream_t st);
 
+// The first layer of a layer-only model read straight from the step's
+// residual inputs, with no norm kernel before it: RMSNorm(h) W^T =
+// (1/rms(h)) (h * g) W^T, so the QKV projection stages bf16(h * g) and
+// writes, per reduction split, each row's sum of squares of h over the
+// split's columns; the QKV finish scales each summed output by
+// 1/sqrt(sum / d + eps) and the residual step reads h as the residual.
+struct HIn {
+  const float *h1;  // [B][d] primary rows (NULL: not in use)
+  const float *h2;  // [n_b][B][d] branch rows
+  int B;
+};
+struct XNorm {
+  HIn h;
+  Rows rows;     // the call's rows: row m is path p0 + m / Bp, sequence m % Bp
+  const float *g;  // [d] attention-norm gain
+  float *ss;     // [S][ss_ld] per split: ss[s * ss_ld + p*Bp + b]
+  int ss_ld;
+  StepBegin sb;  // applied by the first workgroup (positions, page-table entries)
+  int *pos_arr, *page_table, mpps;
+};
+// Whether launch_gemm_xnorm runs this configuration.
+bool gemm_xnorm_ok(const GemmConfig &g, int M);
+hipError_t launch_gemm_xnorm(const WSegs &segs, int N, int K, const XNorm &xn, int M, float *Y, int ldy,
+                             long long y_split_stride, const GemmConfig &g, hipStream_t st);
+
 struct QKVFinish {
   const float *part;
   long long split_stride;
@@ -150,6 +175,11 @@ struct QKVFinish {
   Retain ret;
   KVRef kv;
   int dtype;
+  // rows from XNorm: each summed output of physical row R is scaled by
+  // 1/sqrt(sum_{s < ss_S} ss[s * ss_ld + R] / d_model + eps) (ss NULL: 1)
+  const float *ss;
+  int ss_ld, ss_S, d_model;
+  float eps;
 };
 hipError_t launch_qkv_finish(const QKVFinish &f, hipStream_t st);
 
@@ -160,9 +190,11 @@ struct GatedCopy {
   const float *in;  // [B][d] primary values (branch-only calls)
   Retain ret;       // keep the primary values for a later branch-only call
 };
+// hin.h1 not NULL: the residual of row (path, b) is the step input h (see
+// XNorm) instead of Sres; the sum is written to Sres either way.
 hipError_t launch_resid_norm(const float *part, long long split_stride, int S, int ldp, float *Sres,
                              const float *g, float eps, int d, int dtype, Rows rows, void *Xn, int ldx,
-                             hipStream_t st, const GatedCopy &gc = GatedCopy{});
+                             hipStream_t st, const GatedCopy &gc = GatedCopy{}, const HIn &hin = HIn{});
 
 hipError_t launch_swiglu_finish(const float *part, long long split_stride, int S, int ldp, int f,
                                 int mode, Rows rows, const float *bvec, const float *H1_in,
