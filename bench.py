@@ -42,7 +42,7 @@ METRIC = "grouped decode step µs + tokens/s; HBM GB/s vs peak; branch overhead 
 
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "lmhead_traffic_layer8b_b32_l4096.md")
 GEMM_SOURCE = os.path.join(ROOT, "paper_2608_12385_amd", "csrc", "gemm.hip")
-LMHEAD_KERNEL = "k_gemm_bf16<4, 2, 1, 16, false, 2>"   # grouped step: 64 stacked rows, 16 waves x 32 rows
+LMHEAD_KERNEL = "k_gemm_bf16<4, 2, 1, 16, false, 2, false>"   # grouped step: 64 stacked rows, 16 waves x 32 rows
 
 
 def _sha256(path):

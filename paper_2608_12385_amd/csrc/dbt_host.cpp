@@ -229,12 +229,21 @@ struct StageTimer {
 
 struct dbt_model {
   StageTimer timers[DBT_STAGE_COUNT];
+  // Second stream for the MoE shared expert, which runs beside the routing
+  // chain (created by the first MoE layer of a call that may create it;
+  // default priority), and the events of its fork and join.
+  hipStream_t side = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  bool no_fork = false;  // the current call creates no stream (allocation-free entry point)
   ~dbt_model() {
     for (auto &t : timers)
       for (auto &e : t.ev) {
         (void)hipEventDestroy(e.first);
         (void)hipEventDestroy(e.second);
       }
+    if (ev_fork) (void)hipEventDestroy(ev_fork);
+    if (ev_join) (void)hipEventDestroy(ev_join);
+    if (side) (void)hipStreamDestroy(side);
   }
   dbt_config cfg;
   dbt_weights w;
@@ -450,6 +459,59 @@ dbt_status run_moe_mlp(dbt_model *m, int l, const LayerCall &c, hipStream_t st) 
   ro.ret_idx = c.retain ? ret_idx : nullptr;
   ro.ret_src = c.ret_src;
   ro.ret_dst = c.ret_dst;
+  // The shared expert needs only the normed rows: it runs on a second stream
+  // beside the routing chain (router, top-k, dispatch: short kernels that
+  // leave most compute units idle) and the routed experts; the combine waits
+  // for both.  Neither side writes what the other reads (shared: P, Xh;
+  // routed: the MoE buffers).
+  struct Fork {
+    dbt_model *m;
+    hipStream_t st;
+    bool on;
+    ~Fork() {
+      if (!on) return;
+      (void)hipEventRecord(m->ev_join, m->side);
+      (void)hipStreamWaitEvent(st, m->ev_join, 0);
+    }
+  } fork{m, st, false};
+  hipStream_t sst = st;
+  const bool has_shared = fs > 0 && !(cf.compute_matched && c.mode == MODE_BRANCH);
+  if (has_shared && !m->no_fork) {
+    if (!m->side) {
+      HIPCHK(hipStreamCreateWithFlags(&m->side, hipStreamNonBlocking));
+      // device-scope release: the hand-off is between two queues of one GPU
+      // (a system-scope release would also write the caches back for the host)
+      HIPCHK(hipEventCreateWithFlags(&m->ev_fork, hipEventDisableTiming | hipEventReleaseToDevice));
+      HIPCHK(hipEventCreateWithFlags(&m->ev_join, hipEventDisableTiming | hipEventReleaseToDevice));
+    }
+    HIPCHK(hipEventRecord(m->ev_fork, st));
+    HIPCHK(hipStreamWaitEvent(m->side, m->ev_fork, 0));
+    sst = m->side;
+    fork.on = true;
+  }
+  // shared expert: dense SwiGLU of width fs with the b coupling on its
+  // intermediate; compute-matched variant (App. B.3): primary rows only
+  const bool cm = cf.compute_matched != 0;
+  const Rows srows = cm ? Rows{c.rows.B, c.rows.Bp, 0, 1} : c.rows;
+  const int smode = cm ? (int)MODE_PRIMARY : c.mode;
+  const int sxrow0 = srows.p0 * srows.Bp, sM = srows.np * srows.Bp;
+  long long stride = (long long)c.rows_layout * d;
+  int S_sh = 0;
+  if (fs > 0 && !(cm && c.mode == MODE_BRANCH)) {
+    GemmConfig g_sgu = L.g_sgu, g_sd = L.g_sd;
+    if (c.prefill) g_sgu.S = g_sd.S = 1;
+    WSegs gu{{W.s_gate, W.s_up, nullptr}, {fs, fs, 0}};
+    long long st_gu = (long long)c.rows_layout * 2 * fs;
+    HIPCHK(launch_gemm(gu, 2 * fs, d, cf.dtype, m->p(L.Xn) + (size_t)sxrow0 * d * es, d, sM,
+                       P + (size_t)sxrow0 * 2 * fs, 2 * fs, st_gu, g_sgu, sst));
+    HIPCHK(launch_swiglu_finish(P, st_gu, g_sgu.S, 2 * fs, fs, smode, srows, W.b, ret_h,
+                                Retain{c.retain && !cm ? ret_h : nullptr, c.ret_src, c.ret_dst}, cf.dtype,
+                                m->p(L.Xh), fs, sst));
+    WSegs sd{{W.s_down, nullptr, nullptr}, {d, 0, 0}};
+    HIPCHK(launch_gemm(sd, d, fs, cf.dtype, m->p(L.Xh) + (size_t)sxrow0 * fs * es, fs, sM, P + (size_t)sxrow0 * d,
+                       d, stride, g_sd, sst));
+    S_sh = g_sd.S;
+  }
   HIPCHK(launch_moe_route(ro, st));
   MoeDispatch di{};
   di.idx = ro.idx;
@@ -496,28 +558,10 @@ dbt_status run_moe_mlp(dbt_model *m, int l, const LayerCall &c, hipStream_t st) 
     g.ldy = d;
     HIPCHK(launch_moe_gemm(g, false, max_rows, st));
   }
-  // shared expert: dense SwiGLU of width fs with the b coupling on its
-  // intermediate; compute-matched variant (App. B.3): primary rows only
-  const bool cm = cf.compute_matched != 0;
-  const Rows srows = cm ? Rows{c.rows.B, c.rows.Bp, 0, 1} : c.rows;
-  const int smode = cm ? (int)MODE_PRIMARY : c.mode;
-  const int sxrow0 = srows.p0 * srows.Bp, sM = srows.np * srows.Bp;
-  long long stride = (long long)c.rows_layout * d;
-  int S_sh = 0;
-  if (fs > 0 && !(cm && c.mode == MODE_BRANCH)) {
-    GemmConfig g_sgu = L.g_sgu, g_sd = L.g_sd;
-    if (c.prefill) g_sgu.S = g_sd.S = 1;
-    WSegs gu{{W.s_gate, W.s_up, nullptr}, {fs, fs, 0}};
-    long long st_gu = (long long)c.rows_layout * 2 * fs;
-    HIPCHK(launch_gemm(gu, 2 * fs, d, cf.dtype, m->p(L.Xn) + (size_t)sxrow0 * d * es, d, sM,
-                       P + (size_t)sxrow0 * 2 * fs, 2 * fs, st_gu, g_sgu, st));
-    HIPCHK(launch_swiglu_finish(P, st_gu, g_sgu.S, 2 * fs, fs, smode, srows, W.b, ret_h,
-                                Retain{c.retain && !cm ? ret_h : nullptr, c.ret_src, c.ret_dst}, cf.dtype,
-                                m->p(L.Xh), fs, st));
-    WSegs sd{{W.s_down, nullptr, nullptr}, {d, 0, 0}};
-    HIPCHK(launch_gemm(sd, d, fs, cf.dtype, m->p(L.Xh) + (size_t)sxrow0 * fs * es, fs, sM, P + (size_t)sxrow0 * d,
-                       d, stride, g_sd, st));
-    S_sh = g_sd.S;
+  if (fork.on) {
+    HIPCHK(hipEventRecord(m->ev_join, m->side));
+    HIPCHK(hipStreamWaitEvent(st, m->ev_join, 0));
+    fork.on = false;
   }
   const float *g_next = nullptr;
   if (l + 1 < cf.n_layers) g_next = m->layers[l + 1].attn_norm;
@@ -1328,9 +1372,13 @@ dbt_status decode_step_in(dbt_model *m, dbt_kv *kv, const dbt_step_in *in, int32
   // the model's own step region again when the call returns, whatever it returns
   struct Restore {
     dbt_model *m;
-    ~Restore() { m->step = m->ws + m->L.state_total; }
+    ~Restore() {
+      m->step = m->ws + m->L.state_total;
+      m->no_fork = false;
+    }
   } restore{m};
   m->step = step_mem;
+  m->no_fork = true;  // no stream of its own is created here: the shared expert stays on `stream`
   return decode_step_impl(m, kv, in, branch_on, out, stream);
 }
 

@@ -598,15 +598,24 @@ void launch_xnorm_mb(const GemmConfig &g, dim3 grid, hipStream_t st, const WSegs
   if (g.NW == 8)
     hipLaunchKernelGGL((k_gemm_bf16<MB, 1, 1, 8, false, 2, true>), grid, dim3(512), 0, st, segs, K, nullptr, 0, M, Y,
                        ldy, yss, nullptr, none, xn);
-  else
+  else if (g.RB == 2)
     hipLaunchKernelGGL((k_gemm_bf16<MB, 2, 2, 4, false, 2, true>), grid, dim3(256), 0, st, segs, K, nullptr, 0, M, Y,
+                       ldy, yss, nullptr, none, xn);
+  else
+    hipLaunchKernelGGL((k_gemm_bf16<MB, 1, 2, 4, false, 2, true>), grid, dim3(256), 0, st, segs, K, nullptr, 0, M, Y,
                        ldy, yss, nullptr, none, xn);
 }
 }  // namespace
 
 bool gemm_xnorm_ok(const GemmConfig &g, int M) {
-  // up to 96 stacked rows (more would spill the fp32 staging registers)
-  return M >= 1 && M <= 96 && ((g.NW == 8 && g.RB == 1 && g.PD == 1) || (g.NW == 4 && g.RB == 2 && g.PD == 2));
+  // the thin-matrix shapes, up to the stacked rows whose fp32 staging still
+  // fits the registers (eight waves of one row block, or four of two: 96;
+  // four waves of one row block: 128)
+  if (M < 1) return false;
+  if (g.NW == 8 && g.RB == 1 && g.PD == 1) return M <= 96;
+  if (g.NW == 4 && g.RB == 2 && g.PD == 2) return M <= 96;
+  if (g.NW == 4 && g.RB == 1 && g.PD == 2) return M <= 128;
+  return false;
 }
 
 static int gemm_rows_per_wg(const GemmConfig &g) { return g.NW * 16 * g.RB; }
