@@ -534,8 +534,9 @@ GemmConfig gemm_config(int n_full, int K, int dtype, int seg_gran, int max_rows)
   if (n_full >= 65536 && seg_gran == n_full && n_full % 64 == 0) {
     // output-matrix shapes (one segment): 16 waves x 32 rows = 512 rows per
     // workgroup, so each staged activation chunk serves 512 weight rows; above
-    // 96 stacked rows (its accumulators would spill at 16 waves) 8 waves x 32
-    g = max_rows <= 96 ? GemmConfig{2, 1, 1, 16} : GemmConfig{2, 1, 1, 8};
+    // 64 stacked rows 8 waves x 32 (at 96 rows the sixteen-wave tile spills
+    // and took 208 us against 181 us for the 8B-shape head with two branches)
+    g = max_rows <= 64 ? GemmConfig{2, 1, 1, 16} : GemmConfig{2, 1, 1, 8};
   } else if (n_full >= 16384 && seg_gran % 128 == 0) {
     g = GemmConfig{2, 2, 1, 4};    // MLP up projections
   } else {
