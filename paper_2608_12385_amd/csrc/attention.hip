@@ -153,10 +153,16 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
     const int n1 = __builtin_amdgcn_readfirstlane(live && j1 < pg_last ? 16 * DH * 2 : 0);
     const auto rk0 = buf_rsrc(kbase + o0, n0), rk1 = buf_rsrc(kbase + o1, n1);
     const auto rv0 = buf_rsrc(vbase + o0, n0), rv1 = buf_rsrc(vbase + o1, n1);
+    // K pages first, then V: staging waits for the K registers while the V
+    // loads are still in flight (interleaved, the last K load came after
+    // most V loads; 1.3 us less per benchmark step in a same-box A/B)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       raw[i] = buf_load_nt(rk0, i * 1024 + lane * 16);
       raw[4 + i] = buf_load_nt(rk1, i * 1024 + lane * 16);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
       raw[8 + i] = buf_load_nt(rv0, i * 1024 + lane * 16);
       raw[12 + i] = buf_load_nt(rv1, i * 1024 + lane * 16);
     }
