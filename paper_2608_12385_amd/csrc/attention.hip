@@ -155,7 +155,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
     const auto rv0 = buf_rsrc(vbase + o0, n0), rv1 = buf_rsrc(vbase + o1, n1);
     // K pages first, then V: staging waits for the K registers while the V
     // loads are still in flight (interleaved, the last K load came after
-    // most V loads; 1.3 us less per benchmark step in a same-box A/B)
+    // most V loads; 1.3 us less per benchmark step, both builds timed
+    // alternately on one GPU)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       raw[i] = buf_load_nt(rk0, i * 1024 + lane * 16);
