@@ -450,12 +450,19 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
       qf[s] = u32x4{pack2(u.x, u.y), pack2(u.z, u.w), pack2(w.x, w.y), pack2(w.z, w.w)};
     }
   }
-  for (int q = wave; q < npairs; q += NW) {
+  // Wave w takes pairs w + NW k.  When they do not divide evenly, the waves
+  // with one pair more take their last one second instead of at the end (the
+  // last pair is often a single, partly filled page): its round trip then
+  // overlaps the other waves' streaming rather than trailing the launch alone.
+  const int per = npairs / NW, more = wave < npairs % NW && per > 0;
+  auto pair_of = [&](int k) { return more && k >= 1 ? (k == 1 ? wave + per * NW : wave + (k - 1) * NW) : wave + k * NW; };
+  const int cnt = per + (wave < npairs % NW ? 1 : 0);
+  for (int k = 0; k < cnt; ++k) {
     u32x4 ka[4], kb[4], vf[8];
     stage(raw, ka, kb, vf);
-    load_pair(q + NW, raw, false);
+    load_pair(k + 1 < cnt ? pair_of(k + 1) : npairs, raw, false);
     __builtin_amdgcn_sched_barrier(0);
-    pair(q, ka, kb, vf);
+    pair(pair_of(k), ka, kb, vf);
   }
   l_run += __shfl_xor(l_run, 16, 64);
   l_run += __shfl_xor(l_run, 32, 64);
