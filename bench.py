@@ -451,7 +451,7 @@ def main():
         print(traffic_summary(*args.traffic_summary))
         return
     if args.gpus != 1:
-        print("bench.py measures one GPU: this build runs the decode path on a single MI355X "
+        print("bench.py measures one GPU: the library runs the decode path on a single MI355X "
               "(sharding is described, not built); use --gpus 1", file=sys.stderr)
         sys.exit(2)
 

@@ -63,7 +63,7 @@ typedef enum {
   DBT_ERR_SHAPE = 2,       /* sizes inconsistent with the model */
   DBT_ERR_NO_PAGES = 3,    /* the page pool cannot hold the request */
   DBT_ERR_STATE = 4,       /* call out of order (e.g. boundary without prefill) */
-  DBT_ERR_UNSUPPORTED = 5, /* valid configuration this build does not run */
+  DBT_ERR_UNSUPPORTED = 5, /* valid configuration the library does not run */
   DBT_ERR_HIP = 6          /* HIP runtime or launch error */
 } dbt_status;
 
