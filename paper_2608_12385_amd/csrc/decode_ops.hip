@@ -73,6 +73,18 @@ __device__ __forceinline__ void slabs_issue(const float *part, long long stride,
 #pragma unroll
   for (int k = 0; k < 8; ++k) v[k] = ((const float4 *)(part + (long long)min(k, S - 1) * stride))[idx4];
 }
+// ONE: a single slab (the prompt projections) takes one load; the zeros in
+// the other places are not added.
+template <bool ONE>
+__device__ __forceinline__ void slabs_load(const float *part, long long stride, int S, size_t idx4, float4 (&v)[8]) {
+  if constexpr (ONE) {
+    v[0] = ((const float4 *)part)[idx4];
+#pragma unroll
+    for (int k = 1; k < 8; ++k) v[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+  } else {
+    slabs_issue(part, stride, S, idx4, v);
+  }
+}
 // Their sum in split order, the same additions as psum4 (adding +0 for the
 // slabs past S leaves the bits alone: a sum 0 + v + ... is never -0).
 __device__ __forceinline__ float4 slabs_sum(const float *part, long long stride, int S, size_t idx4,
@@ -276,7 +288,7 @@ __global__ void k_qkv_finish(QKVFinish f) {
 // MLP input RMSNorm.  Compute-matched variant (App. B.3): a branch row adds
 // g_A * A1, A1 being the primary row's projection output (both paths in the
 // call) or the kept A1 (branch-only call); primary rows can keep A1.
-template <typename T, int R>
+template <typename T, int R, bool ONE = false>
 __global__ void k_resid_norm(const float *part, long long stride, int S, int ldp, float *Sres,
                              const float *g, float eps, int d, Rows rows, T *Xn, int ldx, GatedCopy gc, HIn hin) {
   __shared__ float red[16];
@@ -299,7 +311,7 @@ __global__ void k_resid_norm(const float *part, long long stride, int S, int ldp
     gv[k] = ((const float4 *)g)[i];
     if (!gc.g || path == 0) {
       float4 sl[8];
-      slabs_issue(part, stride, S, ((size_t)row * ldp) / 4 + i, sl);
+      slabs_load<ONE>(part, stride, S, ((size_t)row * ldp) / 4 + i, sl);
       const float4 x = sin[i];
       __builtin_amdgcn_sched_barrier(0);  // the sums after every load
       const float4 a1 = slabs_sum(part, stride, S, ((size_t)row * ldp) / 4 + i, sl);
@@ -354,7 +366,7 @@ __global__ void k_swiglu_finish(const float *part, long long stride, int S, int 
 // After the MLP down projection: M1, M2 = M2' + c * M1 (Eq. (15)),
 // S <- S_bar + M (Eq. (16)), then the next RMSNorm (next layer's attention
 // norm, or the final norm before the output matrix).
-template <typename T, int R>
+template <typename T, int R, bool ONE = false>
 __global__ void k_down_finish(const float *part, long long stride, int S, int ldp, int d, int mode,
                               Rows rows, const float *cvec, const float *M1_in, Retain ret,
                               float *Sres, const float *g_next, float eps, T *Xn, int ldx) {
@@ -381,11 +393,16 @@ __global__ void k_down_finish(const float *part, long long stride, int S, int ld
     // the primary) and the kept M1 of a branch-only call
     const size_t i1 = ((size_t)r1 * ldp) / 4 + i, i2 = ((size_t)row * ldp) / 4 + i;
     float4 sl1[8], sl2[8];
+    if constexpr (ONE) {
+      slabs_load<true>(part, stride, S, i1, sl1);
+      slabs_load<true>(part, stride, S, i2, sl2);
+    } else {
 #pragma unroll
-    for (int k2 = 0; k2 < 8; ++k2) {
-      const long long o = (long long)min(k2, S - 1) * stride;
-      sl1[k2] = ((const float4 *)(part + o))[i1];
-      sl2[k2] = ((const float4 *)(part + o))[i2];
+      for (int k2 = 0; k2 < 8; ++k2) {
+        const long long o = (long long)min(k2, S - 1) * stride;
+        sl1[k2] = ((const float4 *)(part + o))[i1];
+        sl2[k2] = ((const float4 *)(part + o))[i2];
+      }
     }
     const float4 x = s[i];
     const float4 c = (path >= 1 ? (const float4 *)cvec : s)[i];
@@ -713,6 +730,15 @@ static int row_regs(int d) {
     default: hipLaunchKernelGGL((KERNEL<T, 8>), __VA_ARGS__); break;                                \
   }
 
+// The same with the single-slab form (ONE) of a split-K row kernel.
+#define DBT_ROW_LAUNCH_ONE(KERNEL, T, d, ...)                                                        \
+  switch (row_regs(d)) {                                                                            \
+    case 1: hipLaunchKernelGGL((KERNEL<T, 1, true>), __VA_ARGS__); break;                           \
+    case 2: hipLaunchKernelGGL((KERNEL<T, 2, true>), __VA_ARGS__); break;                           \
+    case 4: hipLaunchKernelGGL((KERNEL<T, 4, true>), __VA_ARGS__); break;                           \
+    default: hipLaunchKernelGGL((KERNEL<T, 8, true>), __VA_ARGS__); break;                          \
+  }
+
 hipError_t launch_embed(const int *tokens, int vocab, const void *e1, const void *e2, const float *g_emb,
                         const float *g_next, float eps, int d, int dtype, Rows rows, float *S,
                         void *Xn, int ldx, hipStream_t st, const StepBegin *sb, int *pos_arr, int *page_table,
@@ -781,7 +807,10 @@ hipError_t launch_resid_norm(const float *part, long long stride, int S, int ldp
                              hipStream_t st, const GatedCopy &gc, const HIn &hin) {
   dim3 grid(rows.B, rows.np);
   if (hin.h1 && hin.B < rows.B) return hipErrorInvalidValue;
-  if (dtype == 1) {
+  if (dtype == 1 && S == 1) {
+    DBT_ROW_LAUNCH_ONE(k_resid_norm, uint16_t, d, grid, dim3(row_threads(d)), 0, st, part, stride, S, ldp, Sres, g,
+                       eps, d, rows, (uint16_t *)Xn, ldx, gc, hin)
+  } else if (dtype == 1) {
     DBT_ROW_LAUNCH(k_resid_norm, uint16_t, d, grid, dim3(row_threads(d)), 0, st, part, stride, S, ldp, Sres, g, eps,
                    d, rows, (uint16_t *)Xn, ldx, gc, hin)
   } else {
@@ -808,7 +837,10 @@ hipError_t launch_down_finish(const float *part, long long stride, int S, int ld
                               Rows rows, const float *cvec, const float *M1_in, Retain ret, float *Sres,
                               const float *g_next, float eps, int dtype, void *Xn, int ldx, hipStream_t st) {
   dim3 grid(rows.B, rows.np);
-  if (dtype == 1) {
+  if (dtype == 1 && S == 1) {
+    DBT_ROW_LAUNCH_ONE(k_down_finish, uint16_t, d, grid, dim3(row_threads(d)), 0, st, part, stride, S, ldp, d, mode,
+                       rows, cvec, M1_in, ret, Sres, g_next, eps, (uint16_t *)Xn, ldx)
+  } else if (dtype == 1) {
     DBT_ROW_LAUNCH(k_down_finish, uint16_t, d, grid, dim3(row_threads(d)), 0, st, part, stride, S, ldp, d, mode, rows,
                    cvec, M1_in, ret, Sres, g_next, eps, (uint16_t *)Xn, ldx)
   } else {
